@@ -1,0 +1,191 @@
+"""Oracle for the Adaptive Pixel Compressor (Section 3.2, "Condense").
+
+TEST INFRASTRUCTURE ONLY: imported by tests, the smoke check and the benchmark's
+CPU-baseline leg, never by the product path.
+
+Steps, in the paper's order:
+  feature preview  T_i, l2-normalised per patch             (Section 3.2, "Shallow Feature Preview")
+  global density   phi = mean over all N^2 pairs of cos(T_i, T_j)   (Eq. 1); rho_g = 1 - phi (Eq. 2)
+  background       c = mean_i T_i, c_hat = c / ||c||          (Section 3.2, "Local Detail Contrast")
+  detail distance  d_i = ||T_i - c_hat||
+  tail mean        mean of the top 10% of d_i; rho_d = min(d_top / gamma, 1)
+  retention        rho = alpha * rho_g + (1 - alpha) * rho_d   ("Adaptive Condensation")
+  resize           width and height each scaled by sqrt(r), r = rho under the budget, bicubic
+                   (Appendix, "Detailed Implementation Specifics")
+
+Readings where the paper is silent (listed in the design notes):
+  * The preview network's weights are not available, so the per-patch feature is
+    the patch's pixels mapped to x/127.5 - 1 (a 3*P*P vector), one of the
+    pixel-statistic previews of the preview ablation.  Values of rho therefore
+    differ from the paper's: parity with the paper's own rho is unpinned.
+  * "top 10%" keeps ceil(0.10 * N) distances, at least one.
+  * When ||c|| = 0 the baseline direction is the zero vector, so every d_i = ||T_i||.
+    A norm at or below C_ZERO = 1e-5 (phi <= 1e-10) counts as zero: an exactly cancelling
+    mean leaves only rounding noise, whose direction is meaningless.
+  * The hard budget is a clamp of the area ratio r between a floor and a cap, and
+    output sides are snapped to a multiple of ``snap``.
+  * Bicubic: Keys' cubic convolution with a = -0.5, filter stretched by the
+    shrink factor (antialiasing), pixel-centre alignment, taps outside the image
+    dropped and the remaining weights renormalised, one rounding (half up) at
+    the end.
+"""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+
+# Hyperparameters from Section 4.1 (Implementation Details) and the tail-percentile study.
+ALPHA = 0.6
+GAMMA = 1.5
+TAIL_FRAC = 0.10
+C_ZERO = 1e-5
+
+
+def count_for_fraction(frac: float, n: int, at_least_one: bool = False) -> int:
+    """ceil(frac * n) with a 1e-9 guard against float products such as 0.1*30 = 3.0000000000000004."""
+    k = int(math.ceil(frac * n - 1e-9))
+    k = max(0, min(n, k))
+    if at_least_one and n > 0:
+        k = max(1, k)
+    return k
+
+
+def patch_features(img: np.ndarray, patch: int = 14) -> np.ndarray:
+    """Per-patch feature vectors, patches in raster order (row-major over the patch grid).
+
+    Each patch's pixels (patch x patch x 3) are mapped to x/127.5 - 1 and flattened."""
+    H, W, C = img.shape
+    gh, gw = H // patch, W // patch
+    x = img[: gh * patch, : gw * patch, :].astype(np.float64) / 127.5 - 1.0
+    x = x.reshape(gh, patch, gw, patch, C).transpose(0, 2, 1, 3, 4)
+    return x.reshape(gh * gw, patch * patch * C)
+
+
+def l2_normalise(f: np.ndarray) -> np.ndarray:
+    """T_i = f_i / ||f_i||  (Section 3.2: preview embeddings are l2-normalised)."""
+    n = np.linalg.norm(f, axis=1, keepdims=True)
+    return f / n
+
+
+def global_density(T: np.ndarray, chunk: int = 1024) -> float:
+    """Eq. 1: phi = (1/N^2) sum_i sum_j T_i.T_j / (||T_i|| ||T_j||), as a double sum over
+    all ordered pairs (rows taken in chunks so the N x N matrix is never held)."""
+    N = T.shape[0]
+    norms = np.linalg.norm(T, axis=1)
+    total = 0.0
+    for a in range(0, N, chunk):
+        b = min(N, a + chunk)
+        cos = (T[a:b] @ T.T) / (norms[a:b, None] * norms[None, :])
+        total += float(cos.sum())
+    return total / (N * N)
+
+
+def background_direction(T: np.ndarray) -> np.ndarray:
+    """c = (1/N) sum_i T_i, c_hat = c / ||c|| (zero vector when ||c|| <= C_ZERO)."""
+    c = T.mean(axis=0)
+    nc = float(np.linalg.norm(c))
+    if nc <= C_ZERO:
+        return np.zeros_like(c)
+    return c / nc
+
+
+def detail_distances(T: np.ndarray, c_hat: np.ndarray) -> np.ndarray:
+    """d_i = ||T_i - c_hat||_2."""
+    return np.linalg.norm(T - c_hat[None, :], axis=1)
+
+
+def tail_mean(d: np.ndarray, tail_frac: float = TAIL_FRAC) -> float:
+    """Mean of the ceil(tail_frac * N) largest distances (at least one)."""
+    n_tail = count_for_fraction(tail_frac, d.shape[0], at_least_one=True)
+    top = np.sort(d)[::-1][:n_tail]
+    return float(top.mean())
+
+
+def density_from_features(T: np.ndarray, tail_frac: float = TAIL_FRAC, alpha: float = ALPHA,
+                          gamma: float = GAMMA) -> dict:
+    """The APC scores for l2-normalised preview embeddings T [N, D]."""
+    phi = global_density(T)
+    rho_g = 1.0 - phi                                   # Eq. 2
+    c_hat = background_direction(T)
+    d = detail_distances(T, c_hat)
+    d_top = tail_mean(d, tail_frac)
+    rho_d = min(d_top / gamma, 1.0)
+    rho = alpha * rho_g + (1.0 - alpha) * rho_d
+    return {"phi": phi, "rho_g": rho_g, "rho_d": rho_d, "rho": rho, "d": d,
+            "d_top": d_top, "c_hat": c_hat}
+
+
+def apc_density(img: np.ndarray, patch: int = 14, tail_frac: float = TAIL_FRAC,
+                alpha: float = ALPHA, gamma: float = GAMMA) -> dict:
+    """APC density of a uint8 HWC image, with the pixel stand-in feature."""
+    T = l2_normalise(patch_features(img, patch))
+    return density_from_features(T, tail_frac, alpha, gamma)
+
+
+# ---------------------------------------------------------------- resize
+def target_size(rho: float, H: int, W: int, min_pixels: float, max_pixels: float,
+                snap: int) -> tuple:
+    """Output size after APC's resize: area ratio r = rho clamped to [r_floor, r_cap], with
+    r_cap = min(1, max_pixels/(H W)) and r_floor = min(r_cap, min_pixels/(H W)); each side is
+    scaled by sqrt(r), rounded half up to a multiple of ``snap`` and kept within
+    [min(snap, X), floor(X/snap)*snap]."""
+    area = float(H) * float(W)
+    r_cap = min(1.0, max_pixels / area)
+    r_floor = min(r_cap, min_pixels / area)
+    r = min(max(float(rho), r_floor), r_cap)
+    s = math.sqrt(r)
+
+    def side(X):
+        o = int(math.floor(X * s / snap + 0.5)) * snap
+        o = min(o, (X // snap) * snap)
+        return max(o, min(snap, X))
+    return side(H), side(W)
+
+
+def keys_cubic(x: np.ndarray, a: float = -0.5) -> np.ndarray:
+    """Keys' cubic convolution kernel."""
+    x = np.abs(np.asarray(x, dtype=np.float64))
+    w = np.zeros_like(x)
+    m1 = x <= 1.0
+    m2 = (x > 1.0) & (x < 2.0)
+    w[m1] = (a + 2.0) * x[m1] ** 3 - (a + 3.0) * x[m1] ** 2 + 1.0
+    w[m2] = a * x[m2] ** 3 - 5.0 * a * x[m2] ** 2 + 8.0 * a * x[m2] - 4.0 * a
+    return w
+
+
+def resize_weights(n_in: int, n_out: int) -> np.ndarray:
+    """Dense [n_out, n_in] matrix of 1-D bicubic weights (rows sum to 1).
+
+    Output pixel o has centre (o + 0.5) * n_in / n_out in input coordinates; input pixel i
+    has centre i + 0.5.  The kernel is stretched by f = max(1, n_in / n_out)."""
+    scale = n_in / n_out
+    f = max(1.0, scale)
+    Wm = np.zeros((n_out, n_in), dtype=np.float64)
+    centres_in = np.arange(n_in, dtype=np.float64) + 0.5
+    for o in range(n_out):
+        c = (o + 0.5) * scale
+        dist = (centres_in - c) / f
+        w = keys_cubic(dist)
+        w[np.abs(dist) >= 2.0] = 0.0
+        Wm[o] = w / w.sum()
+    return Wm
+
+
+def resize_bicubic_exact(img: np.ndarray, oH: int, oW: int) -> np.ndarray:
+    """Separable resize in float64 with no intermediate rounding -> float64 [oH, oW, 3]."""
+    Wy = resize_weights(img.shape[0], oH)
+    Wx = resize_weights(img.shape[1], oW)
+    x = img.astype(np.float64)
+    out = np.empty((oH, oW, img.shape[2]), dtype=np.float64)
+    for c in range(img.shape[2]):
+        out[:, :, c] = Wy @ x[:, :, c] @ Wx.T
+    return out
+
+
+def round_u8(v: np.ndarray) -> np.ndarray:
+    return np.clip(np.floor(v + 0.5), 0, 255).astype(np.uint8)
+
+
+def resize_bicubic(img: np.ndarray, oH: int, oW: int) -> np.ndarray:
+    return round_u8(resize_bicubic_exact(img, oH, oW))

@@ -1,0 +1,163 @@
+"""Pins for the APC oracle (Section 3.2): closed forms, brute force and bounds.
+
+None of these recompute the oracle's own formulas: expected values come from hand
+derivations (tests/golden), colour-level closed forms in 3 dimensions, pure-Python
+brute force over small inputs, or library routines."""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+
+from oracle import apc
+
+GOLD = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _gold(name):
+    with open(os.path.join(GOLD, name)) as f:
+        return json.load(f)
+
+
+def test_defaults_match_paper_constants():
+    hp = _gold("paper_hyperparameters.json")
+    assert apc.ALPHA == hp["alpha"]["value"]
+    assert apc.GAMMA == hp["gamma"]["value"]
+    assert apc.TAIL_FRAC == hp["tail_frac"]["value"]
+
+
+def _uniform(H, W, rgb):
+    img = np.empty((H, W, 3), np.uint8)
+    img[:] = np.asarray(rgb, np.uint8)
+    return img
+
+
+def test_uniform_image_closed_form():
+    g = _gold("apc_closed_forms.json")["uniform_image"]
+    r = apc.apc_density(_uniform(56, 84, (200, 31, 77)))
+    assert r["phi"] == pytest.approx(g["phi"], abs=1e-12)
+    assert r["rho_g"] == pytest.approx(g["rho_g"], abs=1e-12)
+    assert np.max(np.abs(r["d"])) < 1e-7
+    assert r["rho_d"] == pytest.approx(g["rho_d"], abs=1e-7)
+    assert r["rho"] == pytest.approx(g["rho"], abs=1e-7)
+
+
+def test_mirrored_image_closed_form():
+    g = _gold("apc_closed_forms.json")["mirrored_image"]
+    rs = np.random.default_rng(5)
+    left = rs.integers(0, 256, size=(42, 56, 3), dtype=np.uint8)   # 3 x 4 patches
+    img = np.concatenate([left, 255 - left], axis=1)               # 3 x 8 patches
+    r = apc.apc_density(img)
+    assert r["phi"] == pytest.approx(g["phi"], abs=1e-12)
+    assert r["rho_g"] == pytest.approx(g["rho_g"], abs=1e-12)
+    np.testing.assert_allclose(r["d"], 1.0, atol=1e-12)
+    assert r["rho_d"] == pytest.approx(g["rho_d"], abs=1e-12)
+    assert r["rho"] == pytest.approx(g["rho"], abs=1e-12)
+
+
+def _unit3(rgb):
+    f = np.asarray(rgb, np.float64) / 127.5 - 1.0
+    return f / np.linalg.norm(f)
+
+
+@pytest.mark.parametrize("n_a,n_b", [(1, 15), (3, 13), (5, 11), (8, 8)])
+def test_two_colour_closed_form(n_a, n_b):
+    """Patches of two flat colours a, b.  A flat patch's feature repeats its colour's 3-vector,
+    so T = u_colour (repeated, /sqrt(196)) and cos(T_a, T_b) = u_a . u_b in 3-D.  With
+    p = n_a / N: phi = p^2 + q^2 + 2 p q cos; c = p T_a + q T_b;
+    d_a^2 = 2 - 2 (p + q cos) / |c|, d_b^2 = 2 - 2 (q + p cos) / |c|, |c|^2 = phi."""
+    ca, cb = (250, 10, 40), (20, 60, 230)
+    N = n_a + n_b
+    patches = [ca] * n_a + [cb] * n_b
+    img = np.empty((14, 14 * N, 3), np.uint8)
+    for i, c in enumerate(patches):
+        img[:, 14 * i:14 * (i + 1), :] = c
+    cos = float(_unit3(ca) @ _unit3(cb))
+    p, q = n_a / N, n_b / N
+    phi = p * p + q * q + 2 * p * q * cos
+    nc = math.sqrt(phi)
+    da = math.sqrt(max(0.0, 2 - 2 * (p + q * cos) / nc))
+    db = math.sqrt(max(0.0, 2 - 2 * (q + p * cos) / nc))
+    n_tail = math.ceil(0.1 * N - 1e-9)
+    ds = sorted([da] * n_a + [db] * n_b, reverse=True)[:n_tail]
+    d_top = sum(ds) / n_tail
+    rho_d = min(d_top / 1.5, 1.0)
+    rho = 0.6 * (1 - phi) + 0.4 * rho_d
+    r = apc.apc_density(img)
+    assert r["phi"] == pytest.approx(phi, abs=1e-12)
+    assert r["rho_g"] == pytest.approx(1 - phi, abs=1e-12)
+    np.testing.assert_allclose(np.sort(r["d"]), np.sort([da] * n_a + [db] * n_b), atol=1e-7)
+    assert r["d_top"] == pytest.approx(d_top, abs=1e-7)
+    assert r["rho"] == pytest.approx(rho, abs=1e-7)
+
+
+def test_patch_order_is_raster_over_patch_grid():
+    """Feature row py*gw + px holds patch (py, px); its first entries are that patch's pixel
+    (0, 0) channels.  Catches a transposed patch grid."""
+    gh, gw = 3, 5
+    img = np.zeros((14 * gh, 14 * gw, 3), np.uint8)
+    for py in range(gh):
+        for px in range(gw):
+            img[14 * py:14 * (py + 1), 14 * px:14 * (px + 1), 0] = 10 * py + px
+    f = apc.patch_features(img)
+    assert f.shape == (gh * gw, 588)
+    for py in range(gh):
+        for px in range(gw):
+            assert f[py * gw + px, 0] == pytest.approx((10 * py + px) / 127.5 - 1.0)
+
+
+def test_phi_pairwise_brute_force():
+    """Eq. 1 by explicit Python double loop over pairs on a tiny image."""
+    rs = np.random.default_rng(1)
+    img = rs.integers(0, 256, size=(28, 42, 3), dtype=np.uint8)      # 6 patches
+    f = apc.patch_features(img)
+    T = f / np.linalg.norm(f, axis=1, keepdims=True)
+    N = T.shape[0]
+    tot = 0.0
+    for i in range(N):
+        for j in range(N):
+            a, b = T[i], T[j]
+            tot += sum(x * y for x, y in zip(a, b)) / (math.sqrt(sum(x * x for x in a)) *
+                                                       math.sqrt(sum(y * y for y in b)))
+    assert apc.global_density(T) == pytest.approx(tot / (N * N), abs=1e-12)
+    # identity: sum_ij T_i.T_j = |sum_i T_i|^2 (check of the chunked evaluation)
+    assert apc.global_density(T, chunk=2) == pytest.approx(float(np.sum(T, 0) @ np.sum(T, 0)) / N ** 2,
+                                                           abs=1e-12)
+
+
+@pytest.mark.parametrize("n,frac", [(10, 0.1), (11, 0.1), (1024, 0.1), (196, 0.05), (30, 0.2), (1, 0.1)])
+def test_tail_mean_brute_force(n, frac):
+    rs = np.random.default_rng(n)
+    d = rs.random(n)
+    k = max(1, math.ceil(frac * n - 1e-9))
+    # exact ceil for decimal fractions
+    from fractions import Fraction
+    kk = max(1, -(-Fraction(str(frac)) * n // 1))
+    assert k == kk
+    expect = sum(sorted(d.tolist(), reverse=True)[:k]) / k
+    assert apc.tail_mean(d, frac) == pytest.approx(expect, abs=1e-12)
+
+
+def test_bounds_random_images():
+    rs = np.random.default_rng(7)
+    for _ in range(3):
+        img = rs.integers(0, 256, size=(56, 70, 3), dtype=np.uint8)
+        r = apc.apc_density(img)
+        assert 0 <= r["rho_g"] <= 1 + 1e-12
+        assert np.all(r["d"] >= 0) and np.all(r["d"] <= 2 + 1e-12)
+        assert 0 <= r["rho_d"] <= 1 and 0 <= r["rho"] <= 1 + 1e-12
+
+
+def test_target_size_rules():
+    # rho inside the budget: area ratio rho, sides * sqrt(rho), snapped to 28
+    assert apc.target_size(0.25, 1120, 1680, 0, 1e12, 28) == (560, 840)
+    # hard cap binds: max_pixels / area
+    oh, ow = apc.target_size(0.9, 2000, 2000, 0, 1000 * 1000, 1)
+    assert (oh, ow) == (1000, 1000)
+    # floor binds for rho = 0
+    oh, ow = apc.target_size(0.0, 1000, 1000, 250000, 1e12, 1)
+    assert (oh, ow) == (500, 500)
+    # never larger than the input, never below one snap
+    assert apc.target_size(1.0, 50, 50, 0, 1e12, 28) == (28, 28)
+    assert apc.target_size(0.0, 3000, 3000, 0, 1e12, 28) == (28, 28)

@@ -1,0 +1,118 @@
+"""Pins for the DDAE oracle (Section 3.3): fusion closed forms, top-K brute force, keep count."""
+import json
+import math
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+from oracle import ddae
+
+GOLD = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def test_tau_default_matches_paper():
+    with open(os.path.join(GOLD, "paper_hyperparameters.json")) as f:
+        assert ddae.TAU == json.load(f)["tau"]["value"]
+
+
+def test_minmax_endpoints_and_affine_invariance():
+    rs = np.random.default_rng(0)
+    x = rs.random(50)
+    s = ddae.minmax(x)
+    assert s[np.argmin(x)] == 0.0 and s[np.argmax(x)] == 1.0
+    np.testing.assert_allclose(ddae.minmax(3.5 * x + 7), s, atol=1e-13)
+    assert np.all(ddae.minmax(np.full(5, 2.0)) == 0)
+
+
+def test_equal_confidence_gives_half_half():
+    rs = np.random.default_rng(1)
+    l = rs.random((3, 40))
+    v = l[:, ::-1].copy()            # same distribution of values -> same sigma
+    S, (sl, sv, wl, wv) = ddae.fuse(v, l, merge=1, mode=0)
+    assert sl == pytest.approx(sv, abs=1e-14)
+    assert wl == pytest.approx(0.5) and wv == pytest.approx(0.5)
+
+
+def test_confidence_softmax_three_to_one():
+    """S_llm half zeros / half ones has population sigma 1/2; a constant S_vis has sigma 0.
+    With tau = 1/(2 ln 3): softmax([1/2, 0]/tau) = (3/4, 1/4), so S = 3/4 * S_llm."""
+    n = 20
+    llm = np.zeros((1, n))
+    llm[0, ::2] = 1.0
+    vis = np.ones((1, n))
+    tau = 0.5 / math.log(3.0)
+    S, (sl, sv, wl, wv) = ddae.fuse(vis, llm, merge=1, mode=0, tau=tau)
+    assert sl == pytest.approx(0.5, abs=1e-15)      # population, not sample, std
+    assert sv == 0.0
+    assert wl == pytest.approx(0.75, abs=1e-14) and wv == pytest.approx(0.25, abs=1e-14)
+    np.testing.assert_allclose(S, 0.75 * llm[0], atol=1e-14)
+    # roles swapped: the sharper vision map takes 3/4
+    S2, (_, _, wl2, wv2) = ddae.fuse(llm, vis, merge=1, mode=0, tau=tau)
+    assert wl2 == pytest.approx(0.25) and wv2 == pytest.approx(0.75)
+
+
+def test_fixed_mode_is_weighted_average():
+    rs = np.random.default_rng(2)
+    vis = rs.random((2, 30))
+    llm = rs.random((4, 30))
+    S, (_, _, wl, wv) = ddae.fuse(vis, llm, merge=1, mode=1, w_llm_fixed=0.5)
+    sv = vis.sum(0)
+    sl = llm.sum(0)
+    sv = (sv - sv.min()) / (sv.max() - sv.min())
+    sl = (sl - sl.min()) / (sl.max() - sl.min())
+    np.testing.assert_allclose(S, 0.5 * sv + 0.5 * sl, atol=1e-14)
+    assert (wl, wv) == (0.5, 0.5)
+
+
+def test_merge_and_permutation():
+    """Mass only on patch 4*j + t of head 0 lands on merged token j; LLM token i reads merged
+    token vis_perm[i]."""
+    nv = 6
+    vis = np.zeros((2, 4 * nv))
+    vis[0, 4 * 3 + 2] = 5.0       # merged token 3
+    vis[1, 4 * 1 + 0] = 1.0       # merged token 1
+    perm = np.array([3, 0, 1, 2, 5, 4])
+    m = ddae.vis_token_map(vis, 4, perm)
+    np.testing.assert_allclose(m, [5.0, 0, 1.0, 0, 0, 0])
+
+
+def _brute_topk(S, K):
+    order = sorted(range(len(S)), key=lambda i: (-S[i], i))
+    return sorted(order[:K])
+
+
+@pytest.mark.parametrize("n,K,levels", [(50, 5, None), (200, 20, 7), (13, 13, 3), (9, 0, None),
+                                        (1000, 100, 2), (64, 1, 1)])
+def test_topk_brute_force(n, K, levels):
+    rs = np.random.default_rng(n + K)
+    S = rs.random(n) if levels is None else rs.integers(0, levels, n).astype(np.float64)
+    idx = ddae.topk_indices(S, K)
+    assert idx.tolist() == _brute_topk(S.tolist(), K)
+    assert len(idx) == K and np.all(np.diff(idx) > 0)
+    if 0 < K < n:
+        kept = np.zeros(n, bool)
+        kept[idx] = True
+        assert S[kept].min() >= S[~kept].max()
+        thr = S[kept].min()
+        # at the threshold, every kept index is below every dropped index
+        tk = np.where(kept & (S == thr))[0]
+        td = np.where(~kept & (S == thr))[0]
+        if len(tk) and len(td):
+            assert tk.max() < td.min()
+
+
+def test_keep_count_exact_ceiling():
+    for ratio in ("0.05", "0.1", "0.2", "0.25", "0.5"):
+        fr = Fraction(ratio)
+        for n in list(range(0, 2000)) + [10549, 42196, 20000]:
+            exact = -(-fr * n // 1)
+            assert ddae.keep_count(float(ratio), n) == exact
+
+
+def test_gather_rows():
+    hidden = np.arange(40, dtype=np.uint16).reshape(10, 4)
+    out = ddae.gather(hidden, np.array([1, 4, 9]))
+    np.testing.assert_array_equal(out, hidden[[1, 4, 9]])
+    assert out[2, 3] == 39
