@@ -1,0 +1,229 @@
+/*
+ * pace.h - C ABI of libpace.so, the MI355X (gfx950) hot path of PACE
+ * (Pixel-Adaptive Condense and Extract, arXiv 2608.27206).
+ *
+ * The library implements the data-parallel steps of the method:
+ *   APC  (Section 3.2, "Condense"): per-patch information density of an image
+ *        (Eq. 1-2, the background baseline, the detail distances, the tail mean,
+ *        rho_d and rho) and the bicubic resize by sqrt(r) per side
+ *        (Appendix, "Detailed Implementation Specifics").
+ *   Attention read-outs (Section 3.3 and the implementation details): vision-
+ *        encoder self-attention (window and full) and causal grouped-query LLM
+ *        prefill attention, each also returning the attention mass every key
+ *        receives, with no attention matrix ever stored.
+ *   DDAE (Section 3.3, "Extract"): min-max maps, std confidences, softmax(sigma/tau)
+ *        fusion, top-K ranking and the gather of the kept token rows.
+ *
+ * Conventions for every call:
+ *   - Tensor pointers are DEVICE pointers owned by the caller, contiguous, and
+ *     16-byte aligned unless stated otherwise.  The library never allocates or
+ *     frees memory; calls that need scratch take a caller-owned workspace whose
+ *     size the matching *_workspace_size() function returns.
+ *   - Every device call is asynchronous on `stream` and never synchronises.
+ *   - bf16 tensors are passed as uint16_t bit patterns.  Mass and LSE are fp32;
+ *     LSE is the natural log of the softmax denominator (log-sum-exp of the
+ *     scaled logits).
+ *   - On bad arguments a call returns an error status WITHOUT launching
+ *     anything; pace_last_error() then returns a message (thread-local).
+ *   - Device-side metadata (cu_seqlens and the like) is trusted: it must be
+ *     monotone and consistent with the host-side maxima passed alongside it.
+ *   - The library keeps no global mutable state other than the thread-local
+ *     error message, so independent calls may run concurrently on different
+ *     streams.
+ */
+#ifndef PACE_H_
+#define PACE_H_
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum pace_status {
+  PACE_OK = 0,
+  PACE_ERR_INVALID_ARG = 1,   /* bad shape, count, pointer or alignment; nothing launched */
+  PACE_ERR_UNSUPPORTED = 2,   /* valid but not implemented, e.g. head dim not in {80, 128} */
+  PACE_ERR_WORKSPACE = 3,     /* workspace missing or smaller than *_workspace_size() */
+  PACE_ERR_HIP = 4            /* a HIP launch or runtime call failed */
+} pace_status_t;
+
+/* Message describing the last error returned on this thread ("" if none). */
+const char* pace_last_error(void);
+
+/* Library ABI version (major * 100 + minor). */
+int pace_version(void);
+
+/* ---------------------------------------------------------------- host-only helpers */
+
+/*
+ * Number of tokens kept for a retention ratio: ceil(ratio * n - 1e-9), clamped
+ * to [0, n].  The 1e-9 guard absorbs float products such as 0.1 * 30.
+ * Used for DDAE's K (Section 3.3: keep the top-K tokens) and APC's tail count.
+ * Returns -1 if n < 0 or ratio is not finite.
+ */
+int pace_keep_count(double ratio, int n);
+
+/*
+ * Output size of APC's resize (Section 3.2, "Adaptive Condensation"; Appendix
+ * implementation details: area ratio r = rho, each side scaled by sqrt(r), and a
+ * hard budget overrides rho when it allows less).
+ *   r_cap = min(1, max_pixels / (H*W)), r_floor = min(r_cap, min_pixels / (H*W)),
+ *   r = clamp(rho, r_floor, r_cap); each side X -> floor(X*sqrt(r)/snap + 0.5)*snap,
+ *   kept within [min(snap, X), floor(X/snap)*snap].
+ * Writes *oH, *oW.  INVALID_ARG on non-positive sizes or snap, or null outputs.
+ */
+pace_status_t pace_apc_target_size(double rho, int H, int W, double min_pixels,
+                                   double max_pixels, int snap, int* oH, int* oW);
+
+/* ---------------------------------------------------------------- APC */
+
+/* Workspace bytes for pace_apc_density on an H x W image with square patches. */
+size_t pace_apc_density_workspace_size(int H, int W, int patch);
+
+/*
+ * APC information density (Section 3.2).
+ *   img       uint8 [H, W, 3], HWC, row-major.  H and W must be multiples of patch.
+ *   patch     patch side in pixels, 1..16 (14 for Qwen2.5-VL); patches in raster order.
+ *   tail_frac fraction of largest distances averaged for d_top (0.10 in the paper);
+ *             n_tail = max(1, pace_keep_count(tail_frac, N)).
+ *   alpha, gamma   rho = alpha*rho_g + (1-alpha)*min(d_top/gamma, 1)  (0.6 and 1.5).
+ *   d_out     fp32 [N] per-patch distance d_i = ||T_i - c_hat||, or NULL.
+ *   rho_out   fp32 [4]: rho_g, rho_d, rho, phi.
+ * Per-patch feature: the patch's 3*patch*patch pixels mapped to x/127.5 - 1 and
+ * l2-normalised (a pixel preview; the paper's ViT-block preview needs weights).
+ * phi (Eq. 1) is evaluated as ||mean_i T_i||^2, which equals the mean pairwise
+ * cosine exactly; c_hat is zero when ||c|| <= 1e-5.
+ * N = (H/patch)*(W/patch) must be >= 1.
+ */
+pace_status_t pace_apc_density(const uint8_t* img, int H, int W, int patch, double tail_frac,
+                               float alpha, float gamma, float* d_out, float* rho_out,
+                               void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * APC resize (Appendix implementation details: bicubic resize of both sides).
+ *   src uint8 [H, W, 3] -> dst uint8 [oH, oW, 3], with 1 <= oH <= H and 1 <= oW <= W.
+ * Separable Keys cubic (a = -0.5); when shrinking, the kernel is stretched by the
+ * shrink factor (antialiasing); output pixel o samples input coordinate
+ * (o + 0.5) * X / oX; taps outside the image are dropped and the remaining
+ * weights renormalised; accumulation in fp32 without intermediate rounding;
+ * result rounded half up and clamped to [0, 255].  Pointers need no alignment.
+ * UNSUPPORTED when a side shrinks by more than 32x.
+ */
+pace_status_t pace_apc_downsample(const uint8_t* src, int H, int W, uint8_t* dst, int oH, int oW,
+                                  hipStream_t stream);
+
+/* ---------------------------------------------------------------- attention */
+
+/* Workspace bytes for pace_vit_attention (LSE scratch when lse == NULL and mass != NULL). */
+size_t pace_vit_attention_workspace_size(int N, int H);
+
+/*
+ * Vision-encoder self-attention with per-key mass (window attention and the
+ * full-attention block whose mass is S_vis, Section 3.3 / implementation details).
+ *   q, k, v   bf16 [N, H, d] token-major; d in {80, 128}.
+ *   cu_seqlens int32 [nseg+1] on the device: segment s is rows [cu[s], cu[s+1]);
+ *             segments (windows or whole images) never attend to each other.
+ *   max_seglen host-side upper bound of the segment lengths.
+ *   scale     logit scale (1/sqrt(d) for the encoder).
+ *   o         bf16 [N, H, d] = softmax(q k^T * scale) v, no mask inside a segment.
+ *   lse       fp32 [H, N] natural-log LSE of each row, or NULL.
+ *   mass      fp32 [H, N]: mass[h, j] = sum over every query row i of j's segment
+ *             of P_h[i, j] (column sums of the normalised probabilities), or NULL.
+ * The mass pass needs the LSE: when lse is NULL and mass is not, the workspace
+ * holds it.  Requires N >= 1, H >= 1, nseg >= 1.
+ */
+pace_status_t pace_vit_attention(const uint16_t* q, const uint16_t* k, const uint16_t* v, int N,
+                                 int H, int d, const int32_t* cu_seqlens, int nseg, int max_seglen,
+                                 float scale, uint16_t* o, float* lse, float* mass,
+                                 void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* Workspace bytes for pace_prefill_attention_with_mass (LSE scratch when lse == NULL). */
+size_t pace_prefill_attention_workspace_size(int Ntot, int Hq);
+
+/*
+ * Causal grouped-query prefill attention with visual-key mass (S_llm, Section 3.3).
+ *   q         bf16 [Ntot, Hq, d]; k, v bf16 [Ntot, Hkv, d]; d in {80, 128}; Hq % Hkv == 0;
+ *             query head h uses KV head h / (Hq / Hkv).
+ *   cu_seqlens int32 [B+1] (device): packed sequences, causal inside each (key <= query).
+ *   vis_len   int32 [B] (device): the first vis_len[b] tokens of sequence b are visual.
+ *   cu_vis    int32 [B+1] (device): offset of sequence b's visual keys in mass;
+ *             nvis_total (host) = cu_vis[B], the row length of mass.
+ *   mq_start, mq_len int32 [B] (device): mass sums P over query rows
+ *             [mq_start[b], mq_start[b] + mq_len[b]) of sequence b (relative positions).
+ *             Text rows (mq_start = vis_len) give the paper's "Text" source; all rows
+ *             give "Vision + Text"; the last row gives "Last".
+ *   max_seqlen, max_vis_len, max_mq_len  host-side upper bounds.
+ *   o         bf16 [Ntot, Hq, d]; lse fp32 [Hq, Ntot] or NULL (then the workspace holds it);
+ *   mass      fp32 [Hq, nvis_total]: mass[h, cu_vis[b] + j] = sum_{i in rows_b} P_h[i, j],
+ *             or NULL to skip the mass pass (vis_len, cu_vis, mq_* are then unused).
+ */
+pace_status_t pace_prefill_attention_with_mass(
+    const uint16_t* q, const uint16_t* k, const uint16_t* v, int Ntot, int Hq, int Hkv, int d,
+    const int32_t* cu_seqlens, int B, int max_seqlen, const int32_t* vis_len,
+    const int32_t* cu_vis, int nvis_total, int max_vis_len, const int32_t* mq_start,
+    const int32_t* mq_len,
+    int max_mq_len, float scale, uint16_t* o, float* lse, float* mass, void* workspace,
+    size_t workspace_bytes, hipStream_t stream);
+
+/* ---------------------------------------------------------------- DDAE */
+
+#define PACE_MAX_SEGMENTS 64
+
+/* Workspace bytes for pace_ddae_select / pace_ddae_select_varlen / pace_topk_gather. */
+size_t pace_ddae_select_workspace_size(int nv_total, int nseg);
+
+/*
+ * DDAE selection over B images packed in one batch (Section 3.3).
+ *   vis_mass  fp32 [Hv, nv_total*merge]: vision mass per encoder patch, images
+ *             concatenated (image b owns patches [cu_nv[b]*merge, cu_nv[b+1]*merge)).
+ *             S_vis of LLM token i of image b = sum_h sum_{t<merge}
+ *             vis_mass[h, (cu_nv[b] + p)*merge + t] with p = vis_perm[cu_nv[b] + i]
+ *             (p = i when vis_perm is NULL), then min-max normalised per image.
+ *   vis_perm  int32 [nv_total] (device) or NULL: per image, merged encoder index of each
+ *             LLM-order visual token.
+ *   llm_mass  fp32 [Hl, nv_total]: S_llm of token i = sum_h llm_mass[h, i], min-max per image.
+ *   nv_host   int [B] (HOST): visual tokens per image; keep_host int [B] (HOST): K_b,
+ *             0 <= K_b <= nv_host[b].  B <= PACE_MAX_SEGMENTS.
+ *   mode      0: (w_llm, w_vis) = softmax([sigma_llm, sigma_vis] / tau), sigma = population
+ *             std of each normalised map; 1: fixed (w_llm_fixed, 1 - w_llm_fixed).
+ *   S_final = w_llm * S_llm + w_vis * S_vis.  Top-K per image: highest scores, ties to
+ *             the lower index, kept indices ascending.
+ *   idx_out   int32 [sum K_b]: kept GLOBAL token indices (image b's block starts at
+ *             sum_{c<b} K_c).
+ *   score_out fp32 [nv_total] S_final, or NULL.   fuse_out fp32 [4*B]
+ *             (sigma_llm, sigma_vis, w_llm, w_vis) per image, or NULL.
+ *   hidden    [nv_total, row_bytes] device rows to gather, or NULL to skip the gather;
+ *   out       [sum K_b, row_bytes]: out[r] = hidden[idx_out[r]] bit for bit.
+ *             row_bytes must be a positive multiple of 16.
+ */
+pace_status_t pace_ddae_select_varlen(const float* vis_mass, int Hv, int merge,
+                                      const int32_t* vis_perm, const float* llm_mass, int Hl,
+                                      int B, const int* nv_host, const int* keep_host, int mode,
+                                      float tau, float w_llm_fixed, const void* hidden,
+                                      size_t row_bytes, int32_t* idx_out, float* score_out,
+                                      float* fuse_out, void* out, void* workspace,
+                                      size_t workspace_bytes, hipStream_t stream);
+
+/* Single-image form of pace_ddae_select_varlen (B = 1, nv_host = {Nv}, keep_host = {K}). */
+pace_status_t pace_ddae_select(const float* vis_mass, int Hv, int merge, const int32_t* vis_perm,
+                               const float* llm_mass, int Hl, int Nv, int mode, float tau,
+                               float w_llm_fixed, int K, const void* hidden, size_t row_bytes,
+                               int32_t* idx_out, float* score_out, float* fuse_out, void* out,
+                               void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * The ranking and pruning steps alone (end of Section 3.3): top-K of given fp32
+ * scores [N] (ties to the lower index, ascending output) and the gather of the
+ * kept rows.  hidden may be NULL to skip the gather.  NaN scores are not allowed.
+ */
+pace_status_t pace_topk_gather(const float* scores, int N, int K, const void* hidden,
+                               size_t row_bytes, int32_t* idx_out, void* out, void* workspace,
+                               size_t workspace_bytes, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* PACE_H_ */

@@ -1,0 +1,595 @@
+// Attention with per-key mass for the two read-outs DDAE fuses (Section 3.3): the
+// vision encoder's self-attention (window and full segments; S_vis from the full
+// block) and the LLM's causal grouped-query prefill attention (S_llm from the text
+// query rows).  No attention matrix is ever stored.
+//
+// Two kernels, both on bf16 MFMA (v_mfma_f32_32x32x16_bf16, fp32 accumulation):
+//
+//  attn_fwd   query-stationary.  A workgroup = 4 waves x 32 query rows of one
+//             (segment, head).  K and V tiles of 64 keys are staged through LDS
+//             (double buffered, next tile prefetched into registers).  Each wave
+//             computes S^T = K Q^T so that every lane owns one query row (the MFMA
+//             accumulator column) and 16 keys of it: the row max and row sum are
+//             in-lane, plus one exchange between the two half-waves.  Online softmax
+//             in the log2 domain, P^T feeds O^T = V^T P^T straight from registers
+//             (no LDS round trip).  V is written to LDS transposed, with the keys of
+//             each 16-key chunk permuted to match the accumulator layout of P^T.
+//             For head dim 80 the PV product is padded to 96 rows and row 80 of V^T
+//             holds ones, so the MFMA also produces the softmax denominator.
+//             Writes O (bf16) and the natural-log LSE (fp32).
+//
+//  attn_mass  key-stationary.  A workgroup = 4 waves x 64 keys of one (segment,
+//             head); K stays in registers, query tiles of 32 rows stream through LDS
+//             (double buffered).  P = exp2(S * scale * log2 e - LSE * log2 e) is the
+//             exact normalised probability; each lane accumulates column sums for
+//             its 16 keys in fp32, and one butterfly over the half-wave finishes the
+//             sum.  Writes mass[h, key] once (no atomics, deterministic).
+//
+// Operand layouts of v_mfma_f32_32x32x16_bf16 (wave64, lane l, g = l / 32):
+//   A (32 x 16): lane l holds A[l % 32][8g .. 8g+7]
+//   B (16 x 32): lane l holds B[8g .. 8g+7][l % 32]
+//   C (32 x 32): lane l holds C[8j + 4g + i][l % 32] in register 4j + i (j, i < 4)
+// The k index within a chunk is only ever contracted, so both operands may use any
+// common permutation of it.
+#include <math.h>
+
+#include "pace_internal.h"
+
+namespace pace {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+
+__device__ __forceinline__ bf16x8 as_bf16x8(uint4 u) {
+  bf16x8 r;
+  __builtin_memcpy(&r, &u, 16);
+  return r;
+}
+
+__device__ __forceinline__ f32x16 mfma(bf16x8 a, bf16x8 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
+  f32x2 v = {a, b};
+  bf16x2 r = __builtin_convertvector(v, bf16x2);
+  uint32_t u;
+  __builtin_memcpy(&u, &r, 4);
+  return u;
+}
+
+__device__ __forceinline__ bf16x8 pack_bf16x8(const float* x) {
+  uint4 u;
+  u.x = pack_bf16x2(x[0], x[1]);
+  u.y = pack_bf16x2(x[2], x[3]);
+  u.z = pack_bf16x2(x[4], x[5]);
+  u.w = pack_bf16x2(x[6], x[7]);
+  return as_bf16x8(u);
+}
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// ---------------------------------------------------------------- forward
+struct FwdParams {
+  const uint16_t* q;
+  const uint16_t* k;
+  const uint16_t* v;
+  uint16_t* o;
+  float* lse;              // [Hq, Ntot] or null
+  const int32_t* cu;       // [nseg + 1]
+  int Ntot, Hq, Hkv, group;
+  int nseg, nqt;           // q tiles per segment in the grid
+  float scale_log2;        // scale * log2(e)
+};
+
+constexpr int kBM = 128;   // query rows per workgroup
+constexpr int kBN = 64;    // keys per tile
+constexpr int kThreads = 256;
+
+template <int D>
+struct FwdCfg {
+  static constexpr int DV = (D == 80) ? 96 : D;   // PV rows incl. padding
+  static constexpr int NT = DV / 32;              // O^T accumulator tiles
+  static constexpr int KC = D / 16;               // QK^T k-chunks
+  static constexpr int KS = D + 8;                // LDS row stride of K (elements)
+  static constexpr int VS = kBN + 8;              // LDS row stride of V^T (elements)
+  static constexpr bool ONES = (D == 80);         // row D of V^T is ones -> row sums
+  static constexpr int KCHUNKS = kBN * D / 8;     // 16-byte chunks of a K tile
+  static constexpr int KLOADS = (KCHUNKS + kThreads - 1) / kThreads;
+  static constexpr int VTHREADS = 16 * (D / 8);   // (key quad, 8 dv) work items of a V tile
+};
+
+// position of key quad kq (0..15) of a 64-key tile in the permuted V^T row
+__device__ __forceinline__ int vt_pos(int kq) {
+  const int qd = kq & 3;
+  const int pq = (qd == 1) ? 2 : (qd == 2) ? 1 : qd;
+  return 16 * (kq >> 2) + 4 * pq;
+}
+
+template <int D, bool CAUSAL>
+__global__ __launch_bounds__(kThreads) void attn_fwd(const FwdParams p) {
+  using C = FwdCfg<D>;
+  __shared__ __align__(16) uint16_t Ks[2][kBN * C::KS];
+  __shared__ __align__(16) uint16_t Vt[2][C::DV * C::VS];
+
+  const int lb = remap_block_id(blockIdx.x, gridDim.x);
+  const int per_head = p.nseg * p.nqt;
+  const int h = lb / per_head;
+  const int rem = lb - h * per_head;
+  const int seg = rem / p.nqt;
+  int qt = rem - seg * p.nqt;
+  if (CAUSAL) qt = p.nqt - 1 - qt;   // longest causal rows first
+  const int s0 = p.cu[seg];
+  const int L = p.cu[seg + 1] - s0;
+  const int q0 = qt * kBM;
+  if (q0 >= L) return;
+  const int kvh = h / p.group;
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, g = lane >> 5, c32 = lane & 31;
+  const int qrow = q0 + w * 32 + c32;
+  const long long qstride = static_cast<long long>(p.Hq) * D;
+  const long long kvstride = static_cast<long long>(p.Hkv) * D;
+  const uint16_t* kbase = p.k + static_cast<long long>(s0) * kvstride + kvh * D;
+  const uint16_t* vbase = p.v + static_cast<long long>(s0) * kvstride + kvh * D;
+
+  bf16x8 qf[C::KC];
+  {
+    const uint16_t* qp = p.q + static_cast<long long>(s0 + qrow) * qstride + h * D + g * 8;
+#pragma unroll
+    for (int c = 0; c < C::KC; ++c) {
+      uint4 u = make_uint4(0, 0, 0, 0);
+      if (qrow < L) u = *reinterpret_cast<const uint4*>(qp + c * 16);
+      qf[c] = as_bf16x8(u);
+    }
+  }
+  if constexpr (C::ONES) {
+    // rows D..DV-1 of both V^T buffers: row D = 1.0 (bf16 0x3F80), the rest 0
+    for (int e = tid; e < 2 * (C::DV - D) * kBN; e += kThreads) {
+      const int buf = e / ((C::DV - D) * kBN);
+      const int r = (e / kBN) % (C::DV - D);
+      const int col = e % kBN;
+      Vt[buf][(D + r) * C::VS + col] = (r == 0) ? 0x3F80 : 0;
+    }
+  }
+
+  // register staging of one K/V tile
+  uint4 kreg[C::KLOADS];
+  uint4 vreg[4];
+  auto load_tile = [&](int kt) {
+#pragma unroll
+    for (int i = 0; i < C::KLOADS; ++i) {
+      const int id = tid + i * kThreads;
+      const int r = id / (D / 8), cc = id % (D / 8);
+      uint4 u = make_uint4(0, 0, 0, 0);
+      if (id < C::KCHUNKS && kt + r < L)
+        u = *reinterpret_cast<const uint4*>(kbase + static_cast<long long>(kt + r) * kvstride + cc * 8);
+      kreg[i] = u;
+    }
+    if (tid < C::VTHREADS) {
+      const int kq = tid & 15, dc = tid >> 4;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int key = kt + 4 * kq + i;
+        uint4 u = make_uint4(0, 0, 0, 0);
+        if (key < L)
+          u = *reinterpret_cast<const uint4*>(vbase + static_cast<long long>(key) * kvstride + dc * 8);
+        vreg[i] = u;
+      }
+    }
+  };
+  auto store_tile = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < C::KLOADS; ++i) {
+      const int id = tid + i * kThreads;
+      if (id < C::KCHUNKS) {
+        const int r = id / (D / 8), cc = id % (D / 8);
+        *reinterpret_cast<uint4*>(&Ks[buf][r * C::KS + cc * 8]) = kreg[i];
+      }
+    }
+    if (tid < C::VTHREADS) {
+      const int kq = tid & 15, dc = tid >> 4;
+      const int pos = vt_pos(kq);
+      const uint32_t* a = reinterpret_cast<const uint32_t*>(&vreg[0]);
+      const uint32_t* b = reinterpret_cast<const uint32_t*>(&vreg[1]);
+      const uint32_t* c = reinterpret_cast<const uint32_t*>(&vreg[2]);
+      const uint32_t* d = reinterpret_cast<const uint32_t*>(&vreg[3]);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int wd = e >> 1, sh = (e & 1) * 16;
+        const uint32_t x0 = (a[wd] >> sh) & 0xFFFFu, x1 = (b[wd] >> sh) & 0xFFFFu;
+        const uint32_t x2 = (c[wd] >> sh) & 0xFFFFu, x3 = (d[wd] >> sh) & 0xFFFFu;
+        uint2 pk;
+        pk.x = x0 | (x1 << 16);
+        pk.y = x2 | (x3 << 16);
+        *reinterpret_cast<uint2*>(&Vt[buf][(dc * 8 + e) * C::VS + pos]) = pk;
+      }
+    }
+  };
+
+  f32x16 oacc[C::NT];
+#pragma unroll
+  for (int t = 0; t < C::NT; ++t) oacc[t] = f32x16{};
+  float m_run = -INFINITY;
+  float l_part = 0.f;
+  const int kend = CAUSAL ? min(L, q0 + kBM) : L;
+
+  load_tile(0);
+  int it = 0;
+  for (int kt = 0; kt < kend; kt += kBN, ++it) {
+    const int buf = it & 1;
+    store_tile(buf);
+    __syncthreads();
+    if (kt + kBN < kend) load_tile(kt + kBN);
+
+    // S^T = K Q^T for two sub-tiles of 32 keys
+    f32x16 s[2];
+#pragma unroll
+    for (int st = 0; st < 2; ++st) {
+      s[st] = f32x16{};
+      const uint16_t* kp = &Ks[buf][(st * 32 + c32) * C::KS + g * 8];
+#pragma unroll
+      for (int c = 0; c < C::KC; ++c)
+        s[st] = mfma(*reinterpret_cast<const bf16x8*>(kp + c * 16), qf[c], s[st]);
+    }
+    // mask and row max (in-lane over 32 keys, then across the half-waves)
+    float mx = -INFINITY;
+    const bool need_mask = (kt + kBN > L) || (CAUSAL && kt + kBN - 1 > q0 + w * 32);
+#pragma unroll
+    for (int st = 0; st < 2; ++st) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        if (need_mask) {
+          const int key = kt + st * 32 + g * 4 + 8 * (r >> 2) + (r & 3);
+          const bool ok = (key < L) && (!CAUSAL || key <= qrow);
+          if (!ok) s[st][r] = -INFINITY;
+        }
+        mx = fmaxf(mx, s[st][r]);
+      }
+    }
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    const float m_new = fmaxf(m_run, mx * p.scale_log2);
+    const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
+    const float alpha = fast_exp2(m_run - m_use);
+    m_run = m_new;
+#pragma unroll
+    for (int t = 0; t < C::NT; ++t)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) oacc[t][r] *= alpha;
+    if (!C::ONES) l_part *= alpha;
+#pragma unroll
+    for (int st = 0; st < 2; ++st)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const float pr = fast_exp2(s[st][r] * p.scale_log2 - m_use);
+        s[st][r] = pr;
+        if (!C::ONES) l_part += pr;
+      }
+    // O^T += V^T P^T, 16 keys per MFMA
+#pragma unroll
+    for (int st = 0; st < 2; ++st) {
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh) {
+        float pv[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) pv[e] = s[st][8 * hh + e];
+        const bf16x8 pb = pack_bf16x8(pv);
+        const uint16_t* vp = &Vt[buf][c32 * C::VS + st * 32 + hh * 16 + g * 8];
+#pragma unroll
+        for (int t = 0; t < C::NT; ++t)
+          oacc[t] = mfma(*reinterpret_cast<const bf16x8*>(vp + t * 32 * C::VS), pb, oacc[t]);
+      }
+    }
+  }
+
+  // epilogue: normalise, store O (bf16) and LSE
+  float l;
+  if (C::ONES) {
+    // row D = 80 of O^T sits in tile 2, register 8 of the lanes with g = 0
+    l = __shfl(oacc[2][8], c32, 64);
+  } else {
+    l = l_part + __shfl_xor(l_part, 32, 64);
+  }
+  const float inv_l = 1.f / l;
+  if (qrow < L) {
+    uint16_t* op = p.o + static_cast<long long>(s0 + qrow) * qstride + h * D;
+#pragma unroll
+    for (int t = 0; t < C::NT; ++t) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int dv = t * 32 + g * 4 + 8 * j;
+        if (dv < D) {
+          uint2 pk;
+          pk.x = pack_bf16x2(oacc[t][4 * j + 0] * inv_l, oacc[t][4 * j + 1] * inv_l);
+          pk.y = pack_bf16x2(oacc[t][4 * j + 2] * inv_l, oacc[t][4 * j + 3] * inv_l);
+          *reinterpret_cast<uint2*>(op + dv) = pk;
+        }
+      }
+    }
+    if (g == 0 && p.lse)
+      p.lse[static_cast<long long>(h) * p.Ntot + s0 + qrow] = (m_run + __builtin_amdgcn_logf(l)) * kLn2;
+  }
+}
+
+// ---------------------------------------------------------------- mass
+struct MassParams {
+  const uint16_t* q;
+  const uint16_t* k;
+  const float* lse;          // [Hq, Ntot]
+  float* mass;               // [Hq, mass_stride]
+  const int32_t* cu;         // [nseg + 1]
+  const int32_t* key_len;    // [nseg] keys receiving mass (prefix of the segment), or null = all
+  const int32_t* q_start;    // [nseg] first querying row (relative), or null = 0
+  const int32_t* q_len;      // [nseg] querying rows, or null = whole segment
+  const int32_t* mass_off;   // [nseg] column offset of the segment's keys in mass, or null = cu[s]
+  long long mass_stride;
+  int Ntot, Hq, Hkv, group;
+  int nseg, nkt;             // key tiles per segment in the grid
+  float scale_log2;
+};
+
+constexpr int kMassKeys = 256;   // keys per workgroup (4 waves x 64)
+constexpr int kMassQ = 32;       // query rows per tile
+
+template <int D, bool CAUSAL>
+__global__ __launch_bounds__(kThreads) void attn_mass(const MassParams p) {
+  constexpr int KC = D / 16;
+  constexpr int QS = D + 8;
+  constexpr int QCHUNKS = kMassQ * D / 8;
+  constexpr int QLOADS = (QCHUNKS + kThreads - 1) / kThreads;
+  __shared__ __align__(16) uint16_t Qs[2][kMassQ * QS];
+  __shared__ float L2s[2][kMassQ];
+
+  const int lb = remap_block_id(blockIdx.x, gridDim.x);
+  const int per_head = p.nseg * p.nkt;
+  const int h = lb / per_head;
+  const int rem = lb - h * per_head;
+  const int seg = rem / p.nkt;
+  const int kt = rem - seg * p.nkt;
+  const int s0 = p.cu[seg];
+  const int L = p.cu[seg + 1] - s0;
+  const int klen = p.key_len ? p.key_len[seg] : L;
+  const int k0 = kt * kMassKeys;
+  if (k0 >= klen) return;
+  const int qs = p.q_start ? p.q_start[seg] : 0;
+  const int ql = p.q_len ? p.q_len[seg] : L;
+  const long long moff = p.mass_off ? p.mass_off[seg] : s0;
+  const int kvh = h / p.group;
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, g = lane >> 5, c32 = lane & 31;
+  const long long qstride = static_cast<long long>(p.Hq) * D;
+  const long long kvstride = static_cast<long long>(p.Hkv) * D;
+
+  // K fragments (A operand of S^T = K Q^T) for this wave's two 32-key sets
+  bf16x8 kf[2][KC];
+#pragma unroll
+  for (int ks = 0; ks < 2; ++ks) {
+    const int key = k0 + w * 64 + ks * 32 + c32;
+    const uint16_t* kp = p.k + static_cast<long long>(s0 + key) * kvstride + kvh * D + g * 8;
+#pragma unroll
+    for (int c = 0; c < KC; ++c) {
+      uint4 u = make_uint4(0, 0, 0, 0);
+      if (key < klen) u = *reinterpret_cast<const uint4*>(kp + c * 16);
+      kf[ks][c] = as_bf16x8(u);
+    }
+  }
+
+  const uint16_t* qbase = p.q + static_cast<long long>(s0 + qs) * qstride + h * D;
+  const float* lbase = p.lse + static_cast<long long>(h) * p.Ntot + s0 + qs;
+  uint4 qreg[QLOADS];
+  float lreg = INFINITY;
+  auto load_q = [&](int qt) {
+#pragma unroll
+    for (int i = 0; i < QLOADS; ++i) {
+      const int id = tid + i * kThreads;
+      const int r = id / (D / 8), cc = id % (D / 8);
+      uint4 u = make_uint4(0, 0, 0, 0);
+      if (id < QCHUNKS && qt + r < ql)
+        u = *reinterpret_cast<const uint4*>(qbase + static_cast<long long>(qt + r) * qstride + cc * 8);
+      qreg[i] = u;
+    }
+    if (tid < kMassQ) lreg = (qt + tid < ql) ? lbase[qt + tid] * kLog2e : INFINITY;
+  };
+  auto store_q = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < QLOADS; ++i) {
+      const int id = tid + i * kThreads;
+      if (id < QCHUNKS) {
+        const int r = id / (D / 8), cc = id % (D / 8);
+        *reinterpret_cast<uint4*>(&Qs[buf][r * QS + cc * 8]) = qreg[i];
+      }
+    }
+    if (tid < kMassQ) L2s[buf][tid] = lreg;
+  };
+
+  float macc[2][16];
+#pragma unroll
+  for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) macc[ks][r] = 0.f;
+
+  if (ql > 0) load_q(0);
+  int it = 0;
+  for (int qt = 0; qt < ql; qt += kMassQ, ++it) {
+    const int buf = it & 1;
+    store_q(buf);
+    __syncthreads();
+    if (qt + kMassQ < ql) load_q(qt + kMassQ);
+    bf16x8 qb[KC];
+#pragma unroll
+    for (int c = 0; c < KC; ++c)
+      qb[c] = *reinterpret_cast<const bf16x8*>(&Qs[buf][c32 * QS + c * 16 + g * 8]);
+    const float l2 = L2s[buf][c32];
+    const int qrow = qs + qt + c32;
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      f32x16 acc = f32x16{};
+#pragma unroll
+      for (int c = 0; c < KC; ++c) acc = mfma(kf[ks][c], qb[c], acc);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        float pr = fast_exp2(acc[r] * p.scale_log2 - l2);
+        if (CAUSAL) {
+          const int key = k0 + w * 64 + ks * 32 + g * 4 + 8 * (r >> 2) + (r & 3);
+          if (key > qrow) pr = 0.f;
+        }
+        macc[ks][r] += pr;
+      }
+    }
+  }
+  // column sums over the 32 query lanes of each half-wave
+#pragma unroll
+  for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      float x = macc[ks][r];
+#pragma unroll
+      for (int o = 16; o >= 1; o >>= 1) x += __shfl_xor(x, o, 64);
+      macc[ks][r] = x;
+    }
+  float* mrow = p.mass + static_cast<long long>(h) * p.mass_stride + moff;
+#pragma unroll
+  for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      if (c32 == r) {
+        const int key = k0 + w * 64 + ks * 32 + g * 4 + 8 * (r >> 2) + (r & 3);
+        if (key < klen) mrow[key] = macc[ks][r];
+      }
+    }
+}
+
+template <int D>
+pace_status_t launch_attention(const FwdParams& fp, bool causal, const MassParams* mp, int nfwd,
+                               int nmass, hipStream_t stream) {
+  if (causal)
+    hipLaunchKernelGGL((attn_fwd<D, true>), dim3(nfwd), dim3(kThreads), 0, stream, fp);
+  else
+    hipLaunchKernelGGL((attn_fwd<D, false>), dim3(nfwd), dim3(kThreads), 0, stream, fp);
+  pace_status_t st = check_launch("attn_fwd");
+  if (st != PACE_OK || mp == nullptr || nmass == 0) return st;
+  if (causal)
+    hipLaunchKernelGGL((attn_mass<D, true>), dim3(nmass), dim3(kThreads), 0, stream, *mp);
+  else
+    hipLaunchKernelGGL((attn_mass<D, false>), dim3(nmass), dim3(kThreads), 0, stream, *mp);
+  return check_launch("attn_mass");
+}
+
+}  // namespace
+}  // namespace pace
+
+using namespace pace;
+
+extern "C" {
+
+size_t pace_vit_attention_workspace_size(int N, int H) {
+  if (N < 0 || H < 0) return 0;
+  return static_cast<size_t>(N) * H * sizeof(float);
+}
+
+size_t pace_prefill_attention_workspace_size(int Ntot, int Hq) {
+  if (Ntot < 0 || Hq < 0) return 0;
+  return static_cast<size_t>(Ntot) * Hq * sizeof(float);
+}
+
+pace_status_t pace_vit_attention(const uint16_t* q, const uint16_t* k, const uint16_t* v, int N,
+                                 int H, int d, const int32_t* cu_seqlens, int nseg, int max_seglen,
+                                 float scale, uint16_t* o, float* lse, float* mass,
+                                 void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  PACE_REQUIRE(q && k && v && o && cu_seqlens, "pace_vit_attention: null device pointer");
+  PACE_REQUIRE(aligned16(q) && aligned16(k) && aligned16(v) && aligned16(o),
+               "pace_vit_attention: q/k/v/o must be 16-byte aligned");
+  PACE_REQUIRE(N >= 1 && H >= 1 && nseg >= 1 && max_seglen >= 1 && max_seglen <= N,
+               "pace_vit_attention: N=%d H=%d nseg=%d max_seglen=%d", N, H, nseg, max_seglen);
+  PACE_REQUIRE(isfinite(scale) && scale > 0.f, "pace_vit_attention: scale must be positive");
+  if (d != 80 && d != 128)
+    return set_error(PACE_ERR_UNSUPPORTED, "pace_vit_attention: head dim %d not in {80, 128}", d);
+  const long long nqt = (max_seglen + kBM - 1) / kBM;
+  const long long nkt = (max_seglen + kMassKeys - 1) / kMassKeys;
+  PACE_REQUIRE(nqt * nseg * H < (1ll << 31) && static_cast<long long>(N) * H * d < (1ll << 40),
+               "pace_vit_attention: problem too large");
+  float* lse_buf = lse;
+  if (mass != nullptr && lse == nullptr) {
+    const size_t need = pace_vit_attention_workspace_size(N, H);
+    if (workspace == nullptr || workspace_bytes < need)
+      return set_error(PACE_ERR_WORKSPACE, "pace_vit_attention: workspace %zu < %zu bytes",
+                       workspace_bytes, need);
+    lse_buf = static_cast<float*>(workspace);
+  }
+  FwdParams fp{};
+  fp.q = q; fp.k = k; fp.v = v; fp.o = o; fp.lse = lse_buf; fp.cu = cu_seqlens;
+  fp.Ntot = N; fp.Hq = H; fp.Hkv = H; fp.group = 1;
+  fp.nseg = nseg; fp.nqt = static_cast<int>(nqt);
+  fp.scale_log2 = scale * kLog2e;
+  MassParams mp{};
+  mp.q = q; mp.k = k; mp.lse = lse_buf; mp.mass = mass; mp.cu = cu_seqlens;
+  mp.mass_stride = N;
+  mp.Ntot = N; mp.Hq = H; mp.Hkv = H; mp.group = 1;
+  mp.nseg = nseg; mp.nkt = static_cast<int>(nkt);
+  mp.scale_log2 = fp.scale_log2;
+  const int nfwd = static_cast<int>(nqt * nseg * H);
+  const int nmass = mass ? static_cast<int>(nkt * nseg * H) : 0;
+  if (d == 80) return launch_attention<80>(fp, false, mass ? &mp : nullptr, nfwd, nmass, stream);
+  return launch_attention<128>(fp, false, mass ? &mp : nullptr, nfwd, nmass, stream);
+}
+
+pace_status_t pace_prefill_attention_with_mass(
+    const uint16_t* q, const uint16_t* k, const uint16_t* v, int Ntot, int Hq, int Hkv, int d,
+    const int32_t* cu_seqlens, int B, int max_seqlen, const int32_t* vis_len,
+    const int32_t* cu_vis, int nvis_total, int max_vis_len, const int32_t* mq_start,
+    const int32_t* mq_len, int max_mq_len, float scale, uint16_t* o, float* lse, float* mass,
+    void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  PACE_REQUIRE(q && k && v && o && cu_seqlens, "pace_prefill_attention_with_mass: null device pointer");
+  PACE_REQUIRE(aligned16(q) && aligned16(k) && aligned16(v) && aligned16(o),
+               "pace_prefill_attention_with_mass: q/k/v/o must be 16-byte aligned");
+  PACE_REQUIRE(Ntot >= 1 && Hq >= 1 && Hkv >= 1 && Hq % Hkv == 0,
+               "pace_prefill_attention_with_mass: Ntot=%d Hq=%d Hkv=%d (Hq %% Hkv must be 0)", Ntot,
+               Hq, Hkv);
+  PACE_REQUIRE(B >= 1 && max_seqlen >= 1 && max_seqlen <= Ntot,
+               "pace_prefill_attention_with_mass: B=%d max_seqlen=%d", B, max_seqlen);
+  PACE_REQUIRE(isfinite(scale) && scale > 0.f, "pace_prefill_attention_with_mass: scale must be positive");
+  if (d != 80 && d != 128)
+    return set_error(PACE_ERR_UNSUPPORTED, "pace_prefill_attention_with_mass: head dim %d not in {80, 128}", d);
+  const bool want_mass = mass != nullptr;
+  if (want_mass) {
+    PACE_REQUIRE(vis_len && cu_vis && mq_start && mq_len,
+                 "pace_prefill_attention_with_mass: mass needs vis_len, cu_vis, mq_start, mq_len");
+    PACE_REQUIRE(nvis_total >= 0 && max_vis_len >= 0 && max_vis_len <= max_seqlen && max_mq_len >= 0 &&
+                     max_mq_len <= max_seqlen,
+                 "pace_prefill_attention_with_mass: nvis_total=%d max_vis_len=%d max_mq_len=%d",
+                 nvis_total, max_vis_len, max_mq_len);
+  }
+  const long long nqt = (max_seqlen + kBM - 1) / kBM;
+  const long long nkt = (max_vis_len + kMassKeys - 1) / kMassKeys;
+  PACE_REQUIRE(nqt * B * Hq < (1ll << 31), "pace_prefill_attention_with_mass: problem too large");
+  float* lse_buf = lse;
+  if (lse == nullptr) {
+    const size_t need = pace_prefill_attention_workspace_size(Ntot, Hq);
+    if (workspace == nullptr || workspace_bytes < need)
+      return set_error(PACE_ERR_WORKSPACE, "pace_prefill_attention_with_mass: workspace %zu < %zu bytes",
+                       workspace_bytes, need);
+    lse_buf = static_cast<float*>(workspace);
+  }
+  FwdParams fp{};
+  fp.q = q; fp.k = k; fp.v = v; fp.o = o; fp.lse = lse_buf; fp.cu = cu_seqlens;
+  fp.Ntot = Ntot; fp.Hq = Hq; fp.Hkv = Hkv; fp.group = Hq / Hkv;
+  fp.nseg = B; fp.nqt = static_cast<int>(nqt);
+  fp.scale_log2 = scale * kLog2e;
+  MassParams mp{};
+  mp.q = q; mp.k = k; mp.lse = lse_buf; mp.mass = mass; mp.cu = cu_seqlens;
+  mp.key_len = vis_len; mp.q_start = mq_start; mp.q_len = mq_len; mp.mass_off = cu_vis;
+  mp.mass_stride = nvis_total;
+  mp.Ntot = Ntot; mp.Hq = Hq; mp.Hkv = Hkv; mp.group = Hq / Hkv;
+  mp.nseg = B; mp.nkt = static_cast<int>(nkt);
+  mp.scale_log2 = fp.scale_log2;
+  const int nfwd = static_cast<int>(nqt * B * Hq);
+  // the mass kernel also runs when no row queries (it then writes zeros)
+  const int nmass = (want_mass && nkt > 0) ? static_cast<int>(nkt * B * Hq) : 0;
+  if (d == 80) return launch_attention<80>(fp, true, want_mass ? &mp : nullptr, nfwd, nmass, stream);
+  return launch_attention<128>(fp, true, want_mass ? &mp : nullptr, nfwd, nmass, stream);
+}
+
+}  // extern "C"

@@ -259,6 +259,11 @@ def _vit(config_id: int, layouts: List[VitLayout]) -> VitInputs:
                      cu_vis=np.asarray(cu_vis, dtype=np.int32))
 
 
+def random_bf16(seed: int, shape, scale: float = 1.0) -> np.ndarray:
+    """bf16 bits of N(0, scale^2) draws from rng([1000 + seed, 0]) (test shapes)."""
+    return f32_to_bf16_bits(_normal_bf16(1000 + seed, 0, shape, scale))
+
+
 def _hidden(config_id: int, nv: int) -> np.ndarray:
     return f32_to_bf16_bits(_normal_bf16(config_id, S_HIDDEN, (nv, HIDDEN)))
 

@@ -27,3 +27,11 @@ def pytest_collection_modifyitems(config, items):
     for it in items:
         if "gpu" in it.keywords:
             it.add_marker(skip)
+
+
+@pytest.fixture(autouse=True)
+def _announce_gpu_case(request):
+    # name the case (and flush) before any GPU work, so a crash log says where it stopped
+    if "gpu" in request.keywords:
+        print(f"\n[gpu-case] {request.node.nodeid}", flush=True)
+    yield

@@ -1,0 +1,68 @@
+"""Helpers for the GPU parity tests: moving seeded inputs to the device and back."""
+import sys
+
+import numpy as np
+
+from paper_2608_27206_amd import workloads as wl
+
+
+def torch():
+    import torch as _t
+    return _t
+
+
+def say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def dev_bf16(bits: np.ndarray):
+    t = torch()
+    return t.from_numpy(np.ascontiguousarray(bits).view(np.int16).copy()).view(t.bfloat16).cuda()
+
+
+def dev_i32(a):
+    t = torch()
+    return t.from_numpy(np.ascontiguousarray(np.asarray(a, dtype=np.int32))).cuda()
+
+
+def dev_f32(a):
+    t = torch()
+    return t.from_numpy(np.ascontiguousarray(np.asarray(a, dtype=np.float32))).cuda()
+
+
+def dev_u8(a):
+    t = torch()
+    return t.from_numpy(np.ascontiguousarray(a, dtype=np.uint8)).cuda()
+
+
+def host_bf16_to_f64(x) -> np.ndarray:
+    t = torch()
+    return wl.bf16_bits_to_f64(x.detach().view(t.int16).cpu().numpy().view(np.uint16))
+
+
+def host(x) -> np.ndarray:
+    return x.detach().cpu().numpy()
+
+
+def mass_ok(gpu, ref, nq, rel=1e-3):
+    """Per-key mass parity: |m_gpu - m_ref| <= rel * m_ref + 1e-12 * |Q_set|."""
+    gpu = np.asarray(gpu, np.float64)
+    ref = np.asarray(ref, np.float64)
+    err = np.abs(gpu - ref) - (rel * np.abs(ref) + 1e-12 * nq)
+    return float(err.max()), float((np.abs(gpu - ref) / np.maximum(np.abs(ref), 1e-30)).max())
+
+
+def kept_sets_agree(idx_gpu, idx_ref, S_ref, band=1e-3):
+    """Kept sets may differ only by swapping tokens whose oracle scores lie within `band`."""
+    a = set(int(i) for i in idx_gpu)
+    b = set(int(i) for i in idx_ref)
+    only_gpu = sorted(a - b)
+    only_ref = sorted(b - a)
+    if len(only_gpu) != len(only_ref):
+        return False, f"sizes differ {len(a)} vs {len(b)}"
+    if not only_gpu:
+        return True, "identical"
+    lo = min(S_ref[i] for i in only_gpu)
+    hi = max(S_ref[i] for i in only_ref)
+    return (hi - lo) <= band, f"{len(only_gpu)} swaps, spread {hi - lo:.3g}"

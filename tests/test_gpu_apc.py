@@ -1,0 +1,73 @@
+"""GPU parity of APC density and resize against the float64 oracle.
+
+Density: d_i within 1e-4, rho_g / rho_d / rho / phi within 1e-4 (fp32 accumulation).
+Resize: the rounded output equals the oracle's wherever the oracle's exact value is more
+than 1e-3 from a rounding boundary, and is within one level everywhere."""
+import numpy as np
+import pytest
+
+from oracle import apc as oapc
+from paper_2608_27206_amd import workloads as wl
+from tests.gpu_util import dev_u8, host, say
+
+pytestmark = pytest.mark.gpu
+
+
+def _density(img, tail=0.1):
+    from paper_2608_27206_amd import pace
+    import torch
+    rho, d = pace.apc_density(dev_u8(img), 14, tail, 0.6, 1.5)
+    torch.cuda.synchronize()
+    return host(rho), host(d)
+
+
+def _check_density(img, tail=0.1):
+    say(f"apc density {img.shape}")
+    rho, d = _density(img, tail)
+    ref = oapc.apc_density(img, 14, tail)
+    np.testing.assert_allclose(d, ref["d"], atol=1e-4)
+    np.testing.assert_allclose(rho, [ref["rho_g"], ref["rho_d"], ref["rho"], ref["phi"]], atol=1e-4)
+    return rho
+
+
+def test_density_img448():
+    _check_density(wl.make_image(1, 448, 448))
+
+
+def test_density_ragged_tiles_and_tails():
+    img = wl.make_image(5, 14 * 7, 14 * 37)        # 37 patches per row: 2 full tiles + 5
+    _check_density(img, 0.05)
+    _check_density(img, 0.2)
+
+
+def test_density_uniform_and_mirrored():
+    u = np.full((56, 84, 3), 77, np.uint8)
+    rho = _check_density(u)
+    assert abs(rho[2]) < 1e-5
+    left = np.random.default_rng(5).integers(0, 256, size=(42, 56, 3), dtype=np.uint8)
+    rho = _check_density(np.concatenate([left, 255 - left], axis=1))
+    assert abs(rho[2] - 13 / 15) < 1e-4
+
+
+def _check_resize(img, oh, ow):
+    from paper_2608_27206_amd import pace
+    import torch
+    say(f"resize {img.shape} -> {oh}x{ow}")
+    out = pace.apc_downsample(dev_u8(img), oh, ow)
+    torch.cuda.synchronize()
+    got = host(out).astype(np.int64)
+    exact = oapc.resize_bicubic_exact(img, oh, ow)
+    ref = oapc.round_u8(exact).astype(np.int64)
+    frac = exact - np.floor(exact)
+    near = np.abs(frac - 0.5) < 1e-3
+    assert np.max(np.abs(got - ref)) <= 1
+    assert np.all(got[~near] == ref[~near])
+    return got
+
+
+@pytest.mark.parametrize("shape,out", [((448, 448), (224, 224)), ((448, 448), (308, 308)),
+                                       ((150, 333), (149, 100)), ((96, 128), (96, 128)),
+                                       ((300, 200), (37, 23)), ((64, 64), (1, 1))])
+def test_resize_parity(shape, out):
+    img = wl.make_image(3, *shape)
+    _check_resize(img, *out)

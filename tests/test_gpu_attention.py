@@ -1,0 +1,159 @@
+"""GPU parity of the attention kernels against the float64 oracle.
+
+Bars: O max-abs error <= 2e-2, LSE abs error <= 1e-3, per-key mass relative error <= 1e-3
+(|m_gpu - m_ref| <= 1e-3 m_ref + 1e-12 |Q_set|); keys no querying row can see get exactly 0."""
+import math
+
+import numpy as np
+import pytest
+
+from oracle import attention as oatt
+from paper_2608_27206_amd import workloads as wl
+from tests.gpu_util import (dev_bf16, dev_i32, host, host_bf16_to_f64, mass_ok, say)
+
+pytestmark = pytest.mark.gpu
+
+O_TOL = 2e-2
+LSE_TOL = 1e-3
+
+
+def _vit_case(seed, cu, H, d):
+    N = cu[-1]
+    q = wl.random_bf16(seed, (N, H, d))
+    k = wl.random_bf16(seed + 1, (N, H, d))
+    v = wl.random_bf16(seed + 2, (N, H, d))
+    return q, k, v
+
+
+def _run_vit(q, k, v, cu, maxlen):
+    from paper_2608_27206_amd import pace
+    import torch
+    o, lse, mass = pace.vit_attention(dev_bf16(q), dev_bf16(k), dev_bf16(v), dev_i32(cu), maxlen)
+    torch.cuda.synchronize()
+    return host_bf16_to_f64(o), host(lse), host(mass)
+
+
+def _check_vit(q, k, v, cu, d):
+    N = cu[-1]
+    maxlen = int(np.max(np.diff(cu)))
+    say(f"vit case N={N} H={q.shape[1]} d={d} nseg={len(cu) - 1} maxlen={maxlen}")
+    o, lse, mass = _run_vit(q, k, v, cu, maxlen)
+    Or, Lr, Mr = oatt.vit_attention(wl.bf16_bits_to_f64(q), wl.bf16_bits_to_f64(k),
+                                    wl.bf16_bits_to_f64(v), cu, 1 / math.sqrt(d))
+    assert np.max(np.abs(o - Or)) <= O_TOL
+    assert np.max(np.abs(lse - Lr)) <= LSE_TOL
+    err, rel = mass_ok(mass, Mr, maxlen)
+    assert err <= 0, f"mass rel err {rel}"
+    for a, b in zip(cu[:-1], cu[1:]):   # rows of a segment sum to 1
+        np.testing.assert_allclose(mass[:, a:b].sum(1), b - a, rtol=1e-4)
+
+
+@pytest.mark.parametrize("d", [80, 128])
+def test_vit_full_ragged(d):
+    cu = [0, 1000]
+    q, k, v = _vit_case(1, cu, 4, d)
+    _check_vit(q, k, v, cu, d)
+
+
+@pytest.mark.parametrize("d", [80, 128])
+def test_vit_windows_and_ragged_segments(d):
+    sizes = [64, 64, 16, 4, 64, 1, 33, 130, 64, 257]
+    cu = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int32)
+    q, k, v = _vit_case(5, cu, 3, d)
+    _check_vit(q, k, v, cu, d)
+
+
+def test_vit_large_logits():
+    """Logits with std ~ 6 stress the online max and the rescaling."""
+    cu = [0, 700]
+    N, H, d = 700, 2, 80
+    q = wl.random_bf16(11, (N, H, d), 2.5)
+    k = wl.random_bf16(12, (N, H, d), 2.5)
+    v = wl.random_bf16(13, (N, H, d))
+    _check_vit(q, k, v, cu, d)
+
+
+def _run_prefill(p, d_override=None):
+    from paper_2608_27206_amd import pace
+    import torch
+    cu = p.cu_seqlens
+    seqlens = np.diff(cu)
+    o, lse, mass = pace.prefill_attention_with_mass(
+        dev_bf16(p.q), dev_bf16(p.k), dev_bf16(p.v), dev_i32(cu), int(seqlens.max()),
+        dev_i32(p.vis_len), dev_i32(p.cu_vis), int(p.cu_vis[-1]), int(p.vis_len.max()),
+        dev_i32(p.mq_start), dev_i32(p.mq_len), int(p.mq_len.max()))
+    torch.cuda.synchronize()
+    return host_bf16_to_f64(o), host(lse), host(mass)
+
+
+def _check_prefill(p):
+    d = p.q.shape[2]
+    say(f"prefill case Ntot={p.q.shape[0]} Hq={p.q.shape[1]} Hkv={p.k.shape[1]} d={d} "
+        f"B={len(p.vis_len)}")
+    o, lse, mass = _run_prefill(p)
+    Or, Lr, Mr = oatt.prefill_attention(wl.bf16_bits_to_f64(p.q), wl.bf16_bits_to_f64(p.k),
+                                        wl.bf16_bits_to_f64(p.v), p.cu_seqlens, p.vis_len,
+                                        p.mq_start, p.mq_len, 1 / math.sqrt(d))
+    assert np.max(np.abs(o - Or)) <= O_TOL
+    assert np.max(np.abs(lse - Lr)) <= LSE_TOL
+    err, rel = mass_ok(mass[:, :Mr.shape[1]], Mr, int(p.mq_len.max()))
+    assert err <= 0, f"mass rel err {rel}"
+    return mass, Mr
+
+
+def test_prefill_tiny_config():
+    w = wl.make_workload(0)
+    mass, Mr = _check_prefill(w.prefill)
+    # every visual key is seen by every text row: per head the mass sums to the text length
+    np.testing.assert_allclose(mass.sum(1), Mr.sum(1), rtol=1e-4)
+
+
+def _packed(seed, vis, text, hq, hkv, d):
+    seqlens = [a + b for a, b in zip(vis, text)]
+    n = sum(seqlens)
+    cu = np.concatenate([[0], np.cumsum(seqlens)]).astype(np.int32)
+    cuv = np.concatenate([[0], np.cumsum(vis)]).astype(np.int32)
+    return wl.PrefillInputs(q=wl.random_bf16(seed, (n, hq, d)), k=wl.random_bf16(seed + 1, (n, hkv, d)),
+                            v=wl.random_bf16(seed + 2, (n, hkv, d)), cu_seqlens=cu,
+                            vis_len=np.asarray(vis, np.int32), text_len=np.asarray(text, np.int32),
+                            cu_vis=cuv, salient=[])
+
+
+def test_prefill_varlen_gqa_d128():
+    _check_prefill(_packed(21, [100, 300, 7], [40, 64, 5], 28, 4, 128))
+
+
+def test_prefill_varlen_d80():
+    _check_prefill(_packed(31, [130, 9], [70, 200], 8, 2, 80))
+
+
+def test_prefill_all_rows_mass():
+    """'Vision + Text' source: every row of the sequence queries; causal keys see fewer rows."""
+    p = _packed(41, [150, 40], [50, 9], 14, 2, 128)
+    p.text_len = p.text_len.copy()
+    seqlens = np.diff(p.cu_seqlens)
+    p2 = wl.PrefillInputs(q=p.q, k=p.k, v=p.v, cu_seqlens=p.cu_seqlens, vis_len=p.vis_len,
+                          text_len=p.text_len, cu_vis=p.cu_vis, salient=[])
+    from paper_2608_27206_amd import pace
+    import torch
+    o, lse, mass = pace.prefill_attention_with_mass(
+        dev_bf16(p2.q), dev_bf16(p2.k), dev_bf16(p2.v), dev_i32(p2.cu_seqlens), int(seqlens.max()),
+        dev_i32(p2.vis_len), dev_i32(p2.cu_vis), int(p2.cu_vis[-1]), int(p2.vis_len.max()),
+        dev_i32([0, 0]), dev_i32(seqlens), int(seqlens.max()))
+    torch.cuda.synchronize()
+    _, _, Mr = oatt.prefill_attention(wl.bf16_bits_to_f64(p2.q), wl.bf16_bits_to_f64(p2.k),
+                                      wl.bf16_bits_to_f64(p2.v), p2.cu_seqlens, p2.vis_len,
+                                      [0, 0], seqlens, 1 / math.sqrt(128))
+    err, rel = mass_ok(host(mass), Mr, int(seqlens.max()))
+    assert err <= 0, f"mass rel err {rel}"
+
+
+def test_prefill_no_querying_rows_gives_zero_mass():
+    p = _packed(51, [64], [16], 4, 1, 128)
+    from paper_2608_27206_amd import pace
+    import torch
+    o, lse, mass = pace.prefill_attention_with_mass(
+        dev_bf16(p.q), dev_bf16(p.k), dev_bf16(p.v), dev_i32(p.cu_seqlens), 80, dev_i32(p.vis_len),
+        dev_i32(p.cu_vis), 64, 64, dev_i32([64]), dev_i32([0]), 0)
+    torch.cuda.synchronize()
+    assert np.all(host(mass) == 0)

@@ -1,0 +1,148 @@
+"""GPU parity of DDAE selection (fusion, top-K, gather) against the float64 oracle.
+
+Top-K and gather fed the oracle's scores (as fp32) must be bit-exact; fused scores agree to
+1e-5; end to end, kept sets may differ only on pairs whose oracle scores lie within 1e-3."""
+import numpy as np
+import pytest
+
+from oracle import ddae as oddae
+from paper_2608_27206_amd import workloads as wl
+from tests.gpu_util import dev_bf16, dev_f32, dev_i32, host, kept_sets_agree, say
+
+pytestmark = pytest.mark.gpu
+
+
+def _topk_case(S32, K, hidden_bits):
+    from paper_2608_27206_amd import pace
+    import torch
+    idx, out = pace.topk_gather(dev_f32(S32), K, dev_bf16(hidden_bits))
+    torch.cuda.synchronize()
+    ref = oddae.topk_indices(S32.astype(np.float32), K)
+    got = host(idx).astype(np.int64)
+    np.testing.assert_array_equal(got, ref)
+    import torch as t
+    out_bits = out.view(t.int16).cpu().numpy().view(np.uint16)
+    np.testing.assert_array_equal(out_bits, hidden_bits[ref])
+
+
+@pytest.mark.parametrize("n,K,levels", [(196, 20, None), (10549, 1055, None), (5000, 500, 3),
+                                        (1000, 1, None), (1000, 999, None), (777, 77, 1),
+                                        (4096, 1024, 50)])
+def test_topk_gather_bit_exact_on_oracle_scores(n, K, levels):
+    say(f"topk n={n} K={K} levels={levels}")
+    rs = np.random.default_rng(n * 7 + K)
+    if levels is None:
+        S = rs.random(n).astype(np.float32)
+    else:
+        S = (rs.integers(0, levels, n) / max(1, levels)).astype(np.float32)
+    S[::97] = 0.0
+    hidden = wl.random_bf16(n, (n, 256))
+    _topk_case(S, K, hidden)
+
+
+def test_topk_negative_and_signed_zero():
+    S = np.array([-1.0, -0.0, 0.0, 2.0, -3.5, 1e-30, -1e-30, 0.5] * 30, np.float32)
+    hidden = wl.random_bf16(99, (S.size, 64))
+    _topk_case(S, 37, hidden)
+
+
+def test_topk_edge_counts():
+    from paper_2608_27206_amd import pace
+    import torch
+    S = np.random.default_rng(3).random(300).astype(np.float32)
+    for K in (0, 300):
+        idx, _ = pace.topk_gather(dev_f32(S), K, None)
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(host(idx), np.arange(K))
+
+
+def _fuse_case(vis, llm, merge, perm, mode, K, hidden=None):
+    from paper_2608_27206_amd import pace
+    import torch
+    nv = llm.shape[1]
+    idx, sc, fz, out = pace.ddae_select(dev_f32(vis), merge, None if perm is None else dev_i32(perm),
+                                        dev_f32(llm), [nv], [K], mode=mode, tau=0.5,
+                                        w_llm_fixed=0.5,
+                                        hidden=None if hidden is None else dev_bf16(hidden))
+    torch.cuda.synchronize()
+    S_ref, st = oddae.fuse(vis.astype(np.float64), llm.astype(np.float64), merge, perm, mode, 0.5, 0.5)
+    np.testing.assert_allclose(host(sc), S_ref, atol=1e-5)
+    np.testing.assert_allclose(host(fz)[0], st, atol=1e-5)
+    idx_ref = oddae.topk_indices(S_ref, K)
+    ok, msg = kept_sets_agree(host(idx), idx_ref, S_ref)
+    assert ok, msg
+    # given the GPU's own fp32 scores, the selection is exactly the oracle's rule
+    np.testing.assert_array_equal(host(idx), oddae.topk_indices(host(sc), K))
+    if hidden is not None:
+        import torch as t
+        got = out.view(t.int16).cpu().numpy().view(np.uint16)
+        np.testing.assert_array_equal(got, hidden[host(idx)])
+    return host(idx)
+
+
+def test_fuse_dynamic_with_merge_and_perm():
+    rs = np.random.default_rng(7)
+    nv = 2304
+    vis = rs.gamma(0.5, size=(16, 4 * nv)).astype(np.float32)
+    llm = rs.gamma(0.3, size=(28, nv)).astype(np.float32)
+    perm = rs.permutation(nv).astype(np.int32)
+    _fuse_case(vis, llm, 4, perm, 0, 231, wl.random_bf16(7, (nv, 3584)))
+
+
+def test_fuse_fixed_tiny_config_end_to_end_inputs():
+    w = wl.make_workload(0)
+    rs = np.random.default_rng(8)
+    llm = rs.gamma(0.5, size=(8, 196)).astype(np.float32)
+    _fuse_case(w.vit_mass.astype(np.float32), llm, 1, None, 1, 20, w.hidden)
+
+
+def test_fuse_constant_map():
+    rs = np.random.default_rng(9)
+    vis = np.ones((2, 400), np.float32)
+    llm = rs.random((3, 400)).astype(np.float32)
+    _fuse_case(vis, llm, 1, None, 0, 40)
+
+
+def test_varlen_segments():
+    from paper_2608_27206_amd import pace
+    import torch
+    rs = np.random.default_rng(10)
+    nvs = [256, 1000, 37, 2304]
+    keeps = [oddae.keep_count(r, n) for r, n in zip([0.05, 0.25, 0.1, 0.17], nvs)]
+    nt = sum(nvs)
+    vis = rs.gamma(0.5, size=(16, 4 * nt)).astype(np.float32)
+    llm = rs.gamma(0.3, size=(28, nt)).astype(np.float32)
+    perm = np.concatenate([rs.permutation(n) for n in nvs]).astype(np.int32)
+    hidden = wl.random_bf16(10, (nt, 512))
+    idx, sc, fz, out = pace.ddae_select(dev_f32(vis), 4, dev_i32(perm), dev_f32(llm), nvs, keeps,
+                                        mode=0, hidden=dev_bf16(hidden))
+    torch.cuda.synchronize()
+    idx = host(idx)
+    off = 0
+    koff = 0
+    for b, (n, K) in enumerate(zip(nvs, keeps)):
+        S_ref, st = oddae.fuse(vis[:, 4 * off:4 * (off + n)].astype(np.float64),
+                               llm[:, off:off + n].astype(np.float64), 4, perm[off:off + n], 0)
+        np.testing.assert_allclose(host(sc)[off:off + n], S_ref, atol=1e-5)
+        np.testing.assert_allclose(host(fz)[b], st, atol=1e-5)
+        got = idx[koff:koff + K] - off
+        ok, msg = kept_sets_agree(got, oddae.topk_indices(S_ref, K), S_ref)
+        assert ok, msg
+        np.testing.assert_array_equal(got, oddae.topk_indices(host(sc)[off:off + n], K))
+        off += n
+        koff += K
+    import torch as t
+    np.testing.assert_array_equal(out.view(t.int16).cpu().numpy().view(np.uint16), hidden[idx])
+
+
+def test_determinism():
+    from paper_2608_27206_amd import pace
+    import torch
+    rs = np.random.default_rng(11)
+    vis = rs.gamma(0.5, size=(16, 4 * 3000)).astype(np.float32)
+    llm = rs.gamma(0.3, size=(28, 3000)).astype(np.float32)
+    r1 = pace.ddae_select(dev_f32(vis), 4, None, dev_f32(llm), [3000], [300])
+    r2 = pace.ddae_select(dev_f32(vis), 4, None, dev_f32(llm), [3000], [300])
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(host(r1[0]), host(r2[0]))
+    np.testing.assert_array_equal(host(r1[1]), host(r2[1]))
