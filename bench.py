@@ -1,0 +1,255 @@
+"""PACE hot-path benchmark on one MI355X.
+
+A step is one pass of every hot-path kernel over the 4K-frame workload
+(3836x2156 RGB image, Qwen2.5-VL-7B shapes): APC density and 2x downsample of the
+image, vision-encoder window attention (700 windows of <= 64 patches, 16 heads,
+d = 80) and full attention over 42,196 patches with the per-key mass, causal GQA
+prefill over 10,549 visual + 128 text tokens (28/4 heads, d = 128) with the
+text-query mass of every visual key, and DDAE fusion + top-K (10%) + gather of the
+kept rows of a 10,549 x 3584 bf16 hidden-state matrix.  Inputs are synthetic and
+seeded, already resident in HBM when the timed region starts.
+
+Prints one JSON line.  `value` is the step's algorithmic attention FLOP rate
+(all three attention passes' 4*d*(visible pairs)*heads, over the whole step time).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2516.6     # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", type=int, default=3, help="workload id (3 = 4K frame)")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+                    help="wall-clock budget of the oracle CPU baseline sample (0 = skip)")
+    return ap.parse_args()
+
+
+def main():
+    a = parse()
+    if a.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1 "
+                          "(multi-GPU sharding is described in the design notes, not built)"}))
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    from paper_2608_27206_amd import pace
+    from paper_2608_27206_amd import workloads as wl
+
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda:0")
+    w = wl.make_workload(a.config)
+    L = w.layouts[0]
+    img_np = w.images[0]
+    H, W, _ = img_np.shape
+    vit, pre = w.vit, w.prefill
+
+    def bf(x):
+        return torch.from_numpy(np.ascontiguousarray(x).view(np.int16)).view(torch.bfloat16).to(dev)
+
+    def i32(x):
+        return torch.from_numpy(np.asarray(x, np.int32)).to(dev)
+
+    img = torch.from_numpy(img_np).to(dev)
+    vq, vk, vv = bf(vit.q), bf(vit.k), bf(vit.v)
+    cu_win, cu_full = i32(vit.cu_windows), i32(vit.cu_full)
+    max_win = int(np.diff(vit.cu_windows).max())
+    Np, Hv, dv = vit.q.shape
+    pq, pk, pv = bf(pre.q), bf(pre.k), bf(pre.v)
+    p_cu, p_vis, p_cuv = i32(pre.cu_seqlens), i32(pre.vis_len), i32(pre.cu_vis)
+    p_mqs, p_mql = i32(pre.mq_start), i32(pre.mq_len)
+    S = int(pre.cu_seqlens[-1])
+    Nv = int(pre.vis_len[0])
+    T = int(pre.text_len[0])
+    Hq, Hkv, dq = pre.q.shape[1], pre.k.shape[1], pre.q.shape[2]
+    hidden = bf(w.hidden)
+    perm = i32(vit.vis_perm)
+    K = pace.keep_count(w.keep_ratio, Nv)
+    oH, oW = (int(round(H * w.downsample_scale)), int(round(W * w.downsample_scale))) \
+        if w.downsample_scale else pace.apc_target_size(0.5, H, W, 0, 1e18, 28)
+
+    # outputs and workspaces, allocated once
+    f32 = dict(dtype=torch.float32, device=dev)
+    rho = torch.empty(4, **f32)
+    dpatch = torch.empty(L.n_patches, **f32)
+    ws_apc = torch.empty(pace.lib().pace_apc_density_workspace_size(H, W, 14), dtype=torch.uint8, device=dev)
+    small = torch.empty((oH, oW, 3), dtype=torch.uint8, device=dev)
+    o_win = torch.empty_like(vq)
+    lse_win = torch.empty((Hv, Np), **f32)
+    mass_win = torch.empty((Hv, Np), **f32)
+    o_full = torch.empty_like(vq)
+    lse_full = torch.empty((Hv, Np), **f32)
+    mass_vis = torch.empty((Hv, Np), **f32)
+    o_pre = torch.empty_like(pq)
+    lse_pre = torch.empty((Hq, S), **f32)
+    mass_llm = torch.empty((Hq, Nv), **f32)
+    idx = torch.empty(K, dtype=torch.int32, device=dev)
+    scores = torch.empty(Nv, **f32)
+    fuse = torch.empty((1, 4), **f32)
+    kept = torch.empty((K, hidden.shape[1]), dtype=hidden.dtype, device=dev)
+    ws_sel = torch.empty(pace.lib().pace_ddae_select_workspace_size(Nv, 1), dtype=torch.uint8, device=dev)
+
+    stream = torch.cuda.current_stream()
+    names = ("apc", "resize", "vit_win", "vit_fwd", "vit_mass", "prefill", "select")
+
+    def new_events():
+        return {n: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                for n in names}
+
+    def run(name, fn, ev):
+        if ev is not None:
+            ev[name][0].record(stream)
+        fn()
+        if ev is not None:
+            ev[name][1].record(stream)
+
+    def step(ev):
+        run("apc", lambda: pace.apc_density(img, 14, 0.10, 0.6, 1.5, d_out=dpatch, rho_out=rho,
+                                            workspace=ws_apc), ev)
+        run("resize", lambda: pace.apc_downsample(img, oH, oW, dst=small), ev)
+        run("vit_win", lambda: pace.vit_attention(vq, vk, vv, cu_win, max_win, o=o_win, lse=lse_win,
+                                                  mass=mass_win), ev)
+        run("vit_fwd", lambda: pace.vit_attention(vq, vk, vv, cu_full, Np, o=o_full, lse=lse_full,
+                                                  want_mass=False), ev)
+        run("vit_mass", lambda: pace.vit_attention_mass(vq, vk, cu_full, Np, lse_full, mass=mass_vis),
+            ev)
+        run("prefill", lambda: pace.prefill_attention_with_mass(
+            pq, pk, pv, p_cu, S, p_vis, p_cuv, Nv, Nv, p_mqs, p_mql, T, o=o_pre, lse=lse_pre,
+            mass=mass_llm), ev)
+        run("select", lambda: pace.ddae_select(mass_vis, 4, perm, mass_llm, [Nv], [K], mode=w.fusion_mode,
+                                               tau=w.tau, hidden=hidden, idx_out=idx, score_out=scores,
+                                               fuse_out=fuse, out=kept, workspace=ws_sel), ev)
+
+    for _ in range(a.warmup):
+        step(None)
+    torch.cuda.synchronize()
+    step_events = [new_events() for _ in range(a.steps)]
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    t_start.record(stream)
+    for i in range(a.steps):
+        step(step_events[i])
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    ms_per_step = t_start.elapsed_time(t_end) / a.steps
+    # per-part averages over the timed steps (HIP events on the launch stream)
+    per = {n: 0.0 for n in names}
+    for ev in step_events:
+        for n in names:
+            per[n] += ev[n][0].elapsed_time(ev[n][1])
+    per = {n: v / a.steps for n, v in per.items()}
+
+    # algorithmic work
+    win_sizes = np.diff(vit.cu_windows).astype(np.float64)
+    flop_win = 4.0 * dv * Hv * float(np.sum(win_sizes ** 2))
+    flop_full = 4.0 * dv * Hv * float(Np) ** 2
+    flop_pre = 4.0 * dq * Hq * (S * (S + 1) / 2.0)
+    flop_attn = flop_win + flop_full + flop_pre
+    bytes_win = 4.0 * Np * Hv * dv * 2 + 2.0 * Hv * Np * 4
+    bytes_sel = Hv * Np * 4 + Hq * Nv * 4 + 4 * K + 2.0 * K * hidden.shape[1] * 2
+    bytes_apc = H * W * 3 + 4.0 * L.n_patches
+    bytes_resize = H * W * 3 + oH * oW * 3
+    t_fwd = per["vit_fwd"] * 1e-3
+    achieved = flop_full / t_fwd / 1e12 if t_fwd > 0 else 0.0
+    value = flop_attn / (ms_per_step * 1e-3) / 1e12
+
+    result = {
+        "metric": "attn TFLOP/s (% bf16 MFMA peak) + DDAE select tokens/s (% HBM BW), 1 GPU",
+        "value": round(value, 3),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": a.steps,
+        "warmup": a.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded Qwen2.5-VL-7B-shaped inputs)",
+        "config": {"workload": wl.CONFIG_NAMES[a.config], "image": f"{W}x{H}",
+                   "vit_patches": int(Np), "vit_heads": int(Hv), "vit_head_dim": int(dv),
+                   "windows": int(len(win_sizes)), "prefill_tokens": S, "visual_tokens": Nv,
+                   "text_tokens": T, "llm_heads": f"{Hq}/{Hkv}", "llm_head_dim": int(dq),
+                   "keep": K, "hidden": int(hidden.shape[1]), "resize_to": f"{oW}x{oH}"},
+        "roofline": {"kernel": "attn_fwd<80> (vision full attention, 42,196 patches x 16 heads)",
+                     "bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+                     "traffic": None},
+        "breakdown_ms": {n: round(v, 4) for n, v in per.items()},
+        "attention": {
+            "vit_full_fwd_tflops": round(achieved, 2),
+            "vit_full_fwd_plus_mass_tflops": round(flop_full / ((per["vit_fwd"] + per["vit_mass"]) * 1e-3) / 1e12, 2)
+            if per["vit_fwd"] + per["vit_mass"] > 0 else None,
+            "prefill_fwd_plus_mass_tflops": round(flop_pre / (per["prefill"] * 1e-3) / 1e12, 2)
+            if per["prefill"] > 0 else None,
+            "vit_window_gbs": round(bytes_win / (per["vit_win"] * 1e-3) / 1e9, 1) if per["vit_win"] > 0 else None,
+        },
+        "select": {
+            "tokens_per_s": round(Nv / (per["select"] * 1e-3), 1) if per["select"] > 0 else None,
+            "gbs": round(bytes_sel / (per["select"] * 1e-3) / 1e9, 1) if per["select"] > 0 else None,
+            "hbm_frac": round(bytes_sel / (per["select"] * 1e-3) / 1e9 / PEAK_HBM_GBS, 4) if per["select"] > 0 else None,
+        },
+        "apc": {
+            "density_gbs": round(bytes_apc / (per["apc"] * 1e-3) / 1e9, 1) if per["apc"] > 0 else None,
+            "resize_gbs": round(bytes_resize / (per["resize"] * 1e-3) / 1e9, 1) if per["resize"] > 0 else None,
+        },
+    }
+    if a.cpu_seconds > 0:
+        result["cpu_baseline"] = cpu_baseline(vit, a.cpu_seconds)
+    print(json.dumps(result), flush=True)
+
+
+def cpu_baseline(vit, budget_s: float):
+    """The float64 oracle (unchanged) on the host cores: O and LSE of query rows of the 4K
+    full attention, all 16 heads, over all 42,196 keys, in chunks of 256 rows until the time
+    budget is spent.  Reported in the metric's unit (algorithmic attention TFLOP/s)."""
+    import numpy as np
+
+    from oracle import attention as oatt
+    from paper_2608_27206_amd import workloads as wl
+
+    cores = None
+    try:
+        from threadpoolctl import threadpool_info
+        blas = [p for p in threadpool_info() if p.get("user_api") == "blas"]
+        if blas:
+            cores = int(max(p["num_threads"] for p in blas))
+    except Exception:  # pragma: no cover
+        pass
+    if cores is None:
+        cores = len(os.sched_getaffinity(0))
+    q = wl.bf16_bits_to_f64(vit.q)
+    k = wl.bf16_bits_to_f64(vit.k)
+    v = wl.bf16_bits_to_f64(vit.v)
+    N, H, d = q.shape
+    rows_done = 0
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < budget_s and rows_done < N:
+        rows = np.arange(rows_done, min(N, rows_done + 256))
+        oatt.attention_rows(q, k, v, 0, N, rows, False, 1 / math.sqrt(d))
+        rows_done += rows.size
+    dt = time.perf_counter() - t0
+    flops = 4.0 * d * H * rows_done * N
+    return {"value": round(flops / dt / 1e12, 5), "unit": "TFLOP/s", "cores": cores, "kind": "oracle",
+            "sample": f"float64 oracle attention (O, LSE) for the first {rows_done} of {N} query rows "
+                      f"x {H} heads of the 4K full attention over all {N} keys, {dt:.1f} s wall"}
+
+
+if __name__ == "__main__":
+    main()

@@ -140,6 +140,19 @@ pace_status_t pace_vit_attention(const uint16_t* q, const uint16_t* k, const uin
                                  float scale, uint16_t* o, float* lse, float* mass,
                                  void* workspace, size_t workspace_bytes, hipStream_t stream);
 
+/*
+ * The mass pass of pace_vit_attention alone, from a caller-provided LSE (for
+ * callers that ran the forward pass earlier, or want to time it separately).
+ *   q, k bf16 [N, H, d]; cu_seqlens, nseg, max_seglen, scale as in pace_vit_attention;
+ *   lse  fp32 [H, N] natural-log LSE of every row (as pace_vit_attention writes it);
+ *   mass fp32 [H, N]: mass[h, j] = sum over the rows i of j's segment of
+ *        exp(q_i . k_j * scale - lse[h, i]).
+ */
+pace_status_t pace_vit_attention_mass(const uint16_t* q, const uint16_t* k, int N, int H, int d,
+                                      const int32_t* cu_seqlens, int nseg, int max_seglen,
+                                      float scale, const float* lse, float* mass,
+                                      hipStream_t stream);
+
 /* Workspace bytes for pace_prefill_attention_with_mass (LSE scratch when lse == NULL). */
 size_t pace_prefill_attention_workspace_size(int Ntot, int Hq);
 

@@ -184,6 +184,7 @@ struct ResizeParams {
   uint8_t* dst;
   int H, W, oH, oW;
   int ty;                 // output rows per workgroup
+  int tx;                 // output columns per workgroup (<= kRsTX)
   int rows_cap;           // input rows staged per workgroup
   float sx, sy;           // input pixels per output pixel
   float fx, fy;           // kernel stretch (max(1, s))
@@ -196,66 +197,78 @@ __device__ __forceinline__ float keys_cubic(float x) {
   return 0.f;
 }
 
-// Tap range and weight normaliser of output coordinate o along an axis of n inputs.
-__device__ __forceinline__ void taps(int o, float s, float f, int n, int* lo, int* hi, float* c,
-                                     float* inv_sum) {
-  const float centre = (static_cast<float>(o) + 0.5f) * s;
-  const float support = 2.f * f;
-  int a = static_cast<int>(floorf(centre - support - 0.5f));
-  int b = static_cast<int>(ceilf(centre + support - 0.5f));
-  a = max(a, 0);
-  b = min(b, n - 1);
+// Taps of output coordinate o along an axis of n inputs resized to m outputs.  Input
+// pixel i's distance to o's sample point, in kernel units, is
+//   ((2i + 1) m - (2o + 1) n) / (2 max(n, m)),
+// whose numerator is an exact integer, so the weights carry a single rounding.
+struct Taps {
+  int lo, hi;        // inclusive tap range (extra taps at |dist| >= 2 weigh 0)
+  long long num0;    // numerator at i = lo
+  long long step;    // numerator increment per tap (2m)
+  float inv_den;     // 1 / (2 max(n, m))
+  float inv_sum;     // 1 / sum of the weights
+};
+
+__device__ __forceinline__ Taps make_taps(int o, int n, int m) {
+  Taps t;
+  const long long den = 2ll * (n > m ? n : m);
+  // support in input pixels: 2 * max(1, n/m); centre (o + 0.5) n / m
+  const float centre = (static_cast<float>(o) + 0.5f) * static_cast<float>(n) / static_cast<float>(m);
+  const float support = 2.f * fmaxf(1.f, static_cast<float>(n) / static_cast<float>(m));
+  t.lo = max(static_cast<int>(floorf(centre - support - 0.5f)) - 1, 0);
+  t.hi = min(static_cast<int>(ceilf(centre + support - 0.5f)) + 1, n - 1);
+  t.step = 2ll * m;
+  t.num0 = (2ll * t.lo + 1) * m - (2ll * o + 1) * n;
+  t.inv_den = 1.f / static_cast<float>(den);
   float sum = 0.f;
-  for (int i = a; i <= b; ++i) sum += keys_cubic((static_cast<float>(i) + 0.5f - centre) / f);
-  *lo = a;
-  *hi = b;
-  *c = centre;
-  *inv_sum = 1.f / sum;
+  long long num = t.num0;
+  for (int i = t.lo; i <= t.hi; ++i, num += t.step) sum += keys_cubic(static_cast<float>(num) * t.inv_den);
+  t.inv_sum = 1.f / sum;
+  return t;
 }
 
 __global__ __launch_bounds__(kRsThreads) void apc_resize(const ResizeParams p) {
-  extern __shared__ float hbuf[];   // [rows_cap][kRsTX][3] horizontally filtered rows
-  const int ox0 = blockIdx.x * kRsTX;
+  extern __shared__ float hbuf[];   // [rows_cap][tx][3] horizontally filtered rows
+  const int ox0 = blockIdx.x * p.tx;
   const int oy0 = blockIdx.y * p.ty;
   const int oy1 = min(p.oH, oy0 + p.ty);
   // input rows needed by this tile's output rows
-  int ylo, yhi, tmp_lo, tmp_hi;
-  float cdummy, sdummy;
-  taps(oy0, p.sy, p.fy, p.H, &ylo, &tmp_hi, &cdummy, &sdummy);
-  taps(oy1 - 1, p.sy, p.fy, p.H, &tmp_lo, &yhi, &cdummy, &sdummy);
-  const int nrows = min(yhi - ylo + 1, p.rows_cap);   // the host sizes rows_cap to fit
-  const int ncols = min(kRsTX, p.oW - ox0);
+  const Taps tfirst = make_taps(oy0, p.H, p.oH);
+  const Taps tlast = make_taps(oy1 - 1, p.H, p.oH);
+  const int ylo = tfirst.lo;
+  const int nrows = min(tlast.hi - ylo + 1, p.rows_cap);   // the host sizes rows_cap to fit
+  const int ncols = min(p.tx, p.oW - ox0);
   // horizontal pass into LDS
   for (int e = threadIdx.x; e < nrows * ncols; e += kRsThreads) {
     const int r = e / ncols, x = e - r * ncols;
-    int lo, hi;
-    float c, is;
-    taps(ox0 + x, p.sx, p.fx, p.W, &lo, &hi, &c, &is);
+    const Taps t = make_taps(ox0 + x, p.W, p.oW);
     const uint8_t* row = p.src + static_cast<long long>(ylo + r) * p.W * 3;
     float a0 = 0.f, a1 = 0.f, a2 = 0.f;
-    for (int i = lo; i <= hi; ++i) {
-      const float w = keys_cubic((static_cast<float>(i) + 0.5f - c) / p.fx);
+    long long num = t.num0;
+    for (int i = t.lo; i <= t.hi; ++i, num += t.step) {
+      const float w = keys_cubic(static_cast<float>(num) * t.inv_den);
       a0 += w * static_cast<float>(row[3 * i + 0]);
       a1 += w * static_cast<float>(row[3 * i + 1]);
       a2 += w * static_cast<float>(row[3 * i + 2]);
     }
-    float* h = hbuf + (r * kRsTX + x) * 3;
-    h[0] = a0 * is; h[1] = a1 * is; h[2] = a2 * is;
+    float* h = hbuf + (r * p.tx + x) * 3;
+    h[0] = a0 * t.inv_sum; h[1] = a1 * t.inv_sum; h[2] = a2 * t.inv_sum;
   }
   __syncthreads();
   // vertical pass and store
   for (int e = threadIdx.x; e < (oy1 - oy0) * ncols * 3; e += kRsThreads) {
     const int yy = e / (ncols * 3), rem = e - yy * ncols * 3;
     const int x = rem / 3, ch = rem - x * 3;
-    int lo, hi;
-    float c, is;
-    taps(oy0 + yy, p.sy, p.fy, p.H, &lo, &hi, &c, &is);
+    const Taps t = make_taps(oy0 + yy, p.H, p.oH);
     float acc = 0.f;
-    for (int i = lo; i <= hi; ++i) {
-      const float w = keys_cubic((static_cast<float>(i) + 0.5f - c) / p.fy);
-      acc += w * hbuf[((i - ylo) * kRsTX + x) * 3 + ch];
+    long long num = t.num0;
+    for (int i = t.lo; i <= t.hi; ++i, num += t.step) {
+      const int r = i - ylo;
+      if (r < 0 || r >= nrows) continue;
+      const float w = keys_cubic(static_cast<float>(num) * t.inv_den);
+      acc += w * hbuf[(r * p.tx + x) * 3 + ch];
     }
-    const float v = floorf(acc * is + 0.5f);
+    const float v = floorf(acc * t.inv_sum + 0.5f);
     const int u = static_cast<int>(fminf(fmaxf(v, 0.f), 255.f));
     p.dst[(static_cast<long long>(oy0 + yy) * p.oW + ox0 + x) * 3 + ch] = static_cast<uint8_t>(u);
   }
@@ -350,17 +363,21 @@ pace_status_t pace_apc_downsample(const uint8_t* src, int H, int W, uint8_t* dst
   p.fy = p.sy > 1.f ? p.sy : 1.f;
   if (p.fx > 32.f || p.fy > 32.f)
     return set_error(PACE_ERR_UNSUPPORTED, "pace_apc_downsample: shrink factor above 32");
-  // rows of input per tile of ty output rows: ty*sy + 4*fy + 3 (generous bound)
-  int ty = 16;
-  auto rows_for = [&](int t) { return static_cast<int>(ceilf(t * p.sy + 4.f * p.fy)) + 3; };
-  while (ty > 1 && static_cast<size_t>(rows_for(ty)) * kRsTX * 3 * sizeof(float) > kRsMaxLds) ty >>= 1;
-  const int rows = rows_for(ty);
-  const size_t lds = static_cast<size_t>(rows) * kRsTX * 3 * sizeof(float);
-  if (lds > kRsMaxLds)
-    return set_error(PACE_ERR_UNSUPPORTED, "pace_apc_downsample: shrink factor too large");
+  // rows of input per tile of ty output rows: ty*sy + 4*fy + 5 (generous bound, taps
+  // include one extra zero-weight pixel on each side)
+  int ty = 16, tx = kRsTX;
+  auto rows_for = [&](int t) { return static_cast<int>(ceilf(t * p.sy + 4.f * p.fy)) + 5; };
+  auto lds_for = [&](int t, int x) { return static_cast<size_t>(rows_for(t)) * x * 3 * sizeof(float); };
+  while (lds_for(ty, tx) > kRsMaxLds) {
+    if (ty > 1) ty >>= 1;
+    else if (tx > 8) tx >>= 1;
+    else return set_error(PACE_ERR_UNSUPPORTED, "pace_apc_downsample: shrink factor too large");
+  }
+  const size_t lds = lds_for(ty, tx);
   p.ty = ty;
-  p.rows_cap = rows;
-  dim3 grid((oW + kRsTX - 1) / kRsTX, (oH + ty - 1) / ty);
+  p.tx = tx;
+  p.rows_cap = rows_for(ty);
+  dim3 grid((oW + tx - 1) / tx, (oH + ty - 1) / ty);
   hipLaunchKernelGGL(apc_resize, grid, dim3(kRsThreads), lds, stream, p);
   return check_launch("apc_resize");
 }

@@ -14,8 +14,7 @@
 //             in the log2 domain, P^T feeds O^T = V^T P^T straight from registers
 //             (no LDS round trip).  V is written to LDS transposed, with the keys of
 //             each 16-key chunk permuted to match the accumulator layout of P^T.
-//             For head dim 80 the PV product is padded to 96 rows and row 80 of V^T
-//             holds ones, so the MFMA also produces the softmax denominator.
+//             For head dim 80 the PV product is padded to 96 rows (zero rows).
 //             Writes O (bf16) and the natural-log LSE (fp32).
 //
 //  attn_mass  key-stationary.  A workgroup = 4 waves x 64 keys of one (segment,
@@ -99,7 +98,6 @@ struct FwdCfg {
   static constexpr int KC = D / 16;               // QK^T k-chunks
   static constexpr int KS = D + 8;                // LDS row stride of K (elements)
   static constexpr int VS = kBN + 8;              // LDS row stride of V^T (elements)
-  static constexpr bool ONES = (D == 80);         // row D of V^T is ones -> row sums
   static constexpr int KCHUNKS = kBN * D / 8;     // 16-byte chunks of a K tile
   static constexpr int KLOADS = (KCHUNKS + kThreads - 1) / kThreads;
   static constexpr int VTHREADS = 16 * (D / 8);   // (key quad, 8 dv) work items of a V tile
@@ -147,13 +145,13 @@ __global__ __launch_bounds__(kThreads) void attn_fwd(const FwdParams p) {
       qf[c] = as_bf16x8(u);
     }
   }
-  if constexpr (C::ONES) {
-    // rows D..DV-1 of both V^T buffers: row D = 1.0 (bf16 0x3F80), the rest 0
+  if constexpr (C::DV > D) {
+    // padding rows D..DV-1 of both V^T buffers are zero
     for (int e = tid; e < 2 * (C::DV - D) * kBN; e += kThreads) {
       const int buf = e / ((C::DV - D) * kBN);
       const int r = (e / kBN) % (C::DV - D);
       const int col = e % kBN;
-      Vt[buf][(D + r) * C::VS + col] = (r == 0) ? 0x3F80 : 0;
+      Vt[buf][(D + r) * C::VS + col] = 0;
     }
   }
 
@@ -260,14 +258,14 @@ __global__ __launch_bounds__(kThreads) void attn_fwd(const FwdParams p) {
     for (int t = 0; t < C::NT; ++t)
 #pragma unroll
       for (int r = 0; r < 16; ++r) oacc[t][r] *= alpha;
-    if (!C::ONES) l_part *= alpha;
+    l_part *= alpha;
 #pragma unroll
     for (int st = 0; st < 2; ++st)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const float pr = fast_exp2(s[st][r] * p.scale_log2 - m_use);
         s[st][r] = pr;
-        if (!C::ONES) l_part += pr;
+        l_part += pr;
       }
     // O^T += V^T P^T, 16 keys per MFMA
 #pragma unroll
@@ -287,13 +285,8 @@ __global__ __launch_bounds__(kThreads) void attn_fwd(const FwdParams p) {
   }
 
   // epilogue: normalise, store O (bf16) and LSE
-  float l;
-  if (C::ONES) {
-    // row D = 80 of O^T sits in tile 2, register 8 of the lanes with g = 0
-    l = __shfl(oacc[2][8], c32, 64);
-  } else {
-    l = l_part + __shfl_xor(l_part, 32, 64);
-  }
+  // fp32 row sum of the unrounded probabilities (the LSE feeds the mass pass)
+  const float l = l_part + __shfl_xor(l_part, 32, 64);
   const float inv_l = 1.f / l;
   if (qrow < L) {
     uint16_t* op = p.o + static_cast<long long>(s0 + qrow) * qstride + h * D;
@@ -534,6 +527,33 @@ pace_status_t pace_vit_attention(const uint16_t* q, const uint16_t* k, const uin
   const int nmass = mass ? static_cast<int>(nkt * nseg * H) : 0;
   if (d == 80) return launch_attention<80>(fp, false, mass ? &mp : nullptr, nfwd, nmass, stream);
   return launch_attention<128>(fp, false, mass ? &mp : nullptr, nfwd, nmass, stream);
+}
+
+pace_status_t pace_vit_attention_mass(const uint16_t* q, const uint16_t* k, int N, int H, int d,
+                                      const int32_t* cu_seqlens, int nseg, int max_seglen,
+                                      float scale, const float* lse, float* mass,
+                                      hipStream_t stream) {
+  PACE_REQUIRE(q && k && cu_seqlens && lse && mass, "pace_vit_attention_mass: null device pointer");
+  PACE_REQUIRE(aligned16(q) && aligned16(k), "pace_vit_attention_mass: q/k must be 16-byte aligned");
+  PACE_REQUIRE(N >= 1 && H >= 1 && nseg >= 1 && max_seglen >= 1 && max_seglen <= N,
+               "pace_vit_attention_mass: N=%d H=%d nseg=%d max_seglen=%d", N, H, nseg, max_seglen);
+  PACE_REQUIRE(isfinite(scale) && scale > 0.f, "pace_vit_attention_mass: scale must be positive");
+  if (d != 80 && d != 128)
+    return set_error(PACE_ERR_UNSUPPORTED, "pace_vit_attention_mass: head dim %d not in {80, 128}", d);
+  const long long nkt = (max_seglen + kMassKeys - 1) / kMassKeys;
+  PACE_REQUIRE(nkt * nseg * H < (1ll << 31), "pace_vit_attention_mass: problem too large");
+  MassParams mp{};
+  mp.q = q; mp.k = k; mp.lse = lse; mp.mass = mass; mp.cu = cu_seqlens;
+  mp.mass_stride = N;
+  mp.Ntot = N; mp.Hq = H; mp.Hkv = H; mp.group = 1;
+  mp.nseg = nseg; mp.nkt = static_cast<int>(nkt);
+  mp.scale_log2 = scale * kLog2e;
+  const int nmass = static_cast<int>(nkt * nseg * H);
+  if (d == 80)
+    hipLaunchKernelGGL((attn_mass<80, false>), dim3(nmass), dim3(kThreads), 0, stream, mp);
+  else
+    hipLaunchKernelGGL((attn_mass<128, false>), dim3(nmass), dim3(kThreads), 0, stream, mp);
+  return check_launch("attn_mass");
 }
 
 pace_status_t pace_prefill_attention_with_mass(

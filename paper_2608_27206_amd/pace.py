@@ -38,6 +38,8 @@ _PROTOS = {
     "pace_vit_attention_workspace_size": (c_size, [c_int, c_int]),
     "pace_vit_attention": (c_int, [c_void, c_void, c_void, c_int, c_int, c_int, c_void, c_int, c_int,
                                    c_float, c_void, c_void, c_void, c_void, c_size, c_void]),
+    "pace_vit_attention_mass": (c_int, [c_void, c_void, c_int, c_int, c_int, c_void, c_int, c_int,
+                                        c_float, c_void, c_void, c_void]),
     "pace_prefill_attention_workspace_size": (c_size, [c_int, c_int]),
     "pace_prefill_attention_with_mass": (c_int, [c_void, c_void, c_void, c_int, c_int, c_int, c_int,
                                                  c_void, c_int, c_int, c_void, c_void, c_int, c_int,
@@ -170,6 +172,20 @@ def vit_attention(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, cu_seqlens:
                                     0 if workspace is None else workspace.numel(), _stream()),
            "pace_vit_attention")
     return o, lse, mass
+
+
+def vit_attention_mass(q: torch.Tensor, k: torch.Tensor, cu_seqlens: torch.Tensor, max_seglen: int,
+                       lse: torch.Tensor, scale: Optional[float] = None,
+                       mass: Optional[torch.Tensor] = None):
+    """Mass pass alone from a given LSE [H, N].  Returns mass fp32 [H, N]."""
+    N, H, d = q.shape
+    scale = 1.0 / math.sqrt(d) if scale is None else scale
+    if mass is None:
+        mass = torch.empty((H, N), dtype=torch.float32, device=q.device)
+    _check(lib().pace_vit_attention_mass(_ptr(q), _ptr(k), N, H, d, _ptr(cu_seqlens),
+                                         cu_seqlens.numel() - 1, int(max_seglen), float(scale),
+                                         _ptr(lse), _ptr(mass), _stream()), "pace_vit_attention_mass")
+    return mass
 
 
 def prefill_attention_with_mass(q, k, v, cu_seqlens, max_seqlen: int, vis_len, cu_vis,

@@ -67,7 +67,15 @@ def _check_resize(img, oh, ow):
 
 @pytest.mark.parametrize("shape,out", [((448, 448), (224, 224)), ((448, 448), (308, 308)),
                                        ((150, 333), (149, 100)), ((96, 128), (96, 128)),
-                                       ((300, 200), (37, 23)), ((64, 64), (1, 1))])
+                                       ((300, 200), (37, 23)), ((64, 64), (2, 2)),
+                                       ((2156, 3836), (1078, 1918))])
 def test_resize_parity(shape, out):
     img = wl.make_image(3, *shape)
     _check_resize(img, *out)
+
+
+def test_resize_rejects_shrink_beyond_32x():
+    from paper_2608_27206_amd import pace
+    img = wl.make_image(3, 64, 64)
+    with pytest.raises(pace.PaceError, match="shrink factor"):
+        pace.apc_downsample(dev_u8(img), 1, 1)

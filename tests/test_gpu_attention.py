@@ -157,3 +157,17 @@ def test_prefill_no_querying_rows_gives_zero_mass():
         dev_i32(p.cu_vis), 64, 64, dev_i32([64]), dev_i32([0]), 0)
     torch.cuda.synchronize()
     assert np.all(host(mass) == 0)
+
+
+def test_mass_only_entry_matches_fused_call():
+    from paper_2608_27206_amd import pace
+    import torch
+    cu = np.array([0, 64, 128, 500], np.int32)
+    q, k, v = _vit_case(61, cu, 2, 80)
+    Q, K, V, CU = dev_bf16(q), dev_bf16(k), dev_bf16(v), dev_i32(cu)
+    o, lse, mass = pace.vit_attention(Q, K, V, CU, 372)
+    o2, lse2, _ = pace.vit_attention(Q, K, V, CU, 372, want_mass=False)
+    m2 = pace.vit_attention_mass(Q, K, CU, 372, lse2)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(host(mass), host(m2))
+    np.testing.assert_array_equal(host(lse), host(lse2))
