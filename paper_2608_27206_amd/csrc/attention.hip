@@ -12,9 +12,8 @@
 //             accumulator column) and 16 keys of it: the row max and row sum are
 //             in-lane, plus one exchange between the two half-waves.  Online softmax
 //             in the log2 domain, P^T feeds O^T = V^T P^T straight from registers
-//             (no LDS round trip).  V is written to LDS transposed, with the keys of
-//             each 16-key chunk permuted to match the accumulator layout of P^T.
-//             For head dim 80 the PV product is padded to 96 rows (zero rows).
+//             (no LDS round trip); V^T comes from transposing LDS reads of the
+//             row-major V tile.  For head dim 80 the PV product is padded to 96 rows.
 //             Writes O (bf16) and the natural-log LSE (fp32).
 //
 //  attn_mass  key-stationary.  A workgroup = 4 waves x 64 keys of one (segment,
@@ -31,6 +30,8 @@
 // The k index within a chunk is only ever contracted, so both operands may use any
 // common permutation of it.
 #include <math.h>
+
+#include <type_traits>
 
 #include "pace_internal.h"
 
@@ -74,6 +75,27 @@ __device__ __forceinline__ bf16x8 pack_bf16x8(const float* x) {
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// Buffer resource over `bytes` bytes from `base`: loads at offsets past the end return 0
+// (the hardware range check), so tile loads need neither branches nor clamps.  The whole
+// offset always goes in the VGPR operand, which the range check covers.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, unsigned bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+__device__ __forceinline__ uint4 buf_load16(__amdgpu_buffer_rsrc_t r, unsigned voff, unsigned soff) {
+  return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
+}
+constexpr unsigned kOutOfRange = 0x7FFFFFF0u;
+
+// Compile-time loop: f(integral_constant<int, I>) for I in [B, E), so register arrays
+// are only ever indexed by constants.
+template <int B, int E, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (B < E) {
+    f(std::integral_constant<int, B>{});
+    static_for<B + 1, E>(f);
+  }
+}
+
 // ---------------------------------------------------------------- forward
 struct FwdParams {
   const uint16_t* q;
@@ -97,24 +119,41 @@ struct FwdCfg {
   static constexpr int NT = DV / 32;              // O^T accumulator tiles
   static constexpr int KC = D / 16;               // QK^T k-chunks
   static constexpr int KS = D + 8;                // LDS row stride of K (elements)
-  static constexpr int VS = kBN + 8;              // LDS row stride of V^T (elements)
-  static constexpr int KCHUNKS = kBN * D / 8;     // 16-byte chunks of a K tile
-  static constexpr int KLOADS = (KCHUNKS + kThreads - 1) / kThreads;
-  static constexpr int VTHREADS = 16 * (D / 8);   // (key quad, 8 dv) work items of a V tile
+  static constexpr int VS = D + 16;               // LDS row stride of V (elements)
+  static constexpr int CHUNKS = kBN * D / 8;      // 16-byte chunks of a K or V tile
+  static constexpr int LOADS = (CHUNKS + kThreads - 1) / kThreads;
 };
 
-// position of key quad kq (0..15) of a 64-key tile in the permuted V^T row
-__device__ __forceinline__ int vt_pos(int kq) {
-  const int qd = kq & 3;
-  const int pq = (qd == 1) ? 2 : (qd == 2) ? 1 : qd;
-  return 16 * (kq >> 2) + 4 * pq;
+typedef short v4s __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) v4s lds_v4s;
+
+// ds_read_b64_tr_b16: within each 16-lane group, destination lane i, slot j receives
+// element (i % 4) of the 8 bytes addressed by source lane 4j + i/4.
+__device__ __forceinline__ uint2 lds_read_tr16(const uint16_t* p) {
+  v4s r = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s*)(p));
+  uint2 u;
+  __builtin_memcpy(&u, &r, 8);
+  return u;
 }
 
+// Rows whose running max grows by less than this (log2 units) keep their old max:
+// probabilities then stay below 2^8, harmless in fp32 accumulators and bf16 operands,
+// and the O accumulators are rescaled only when some row's max really moves.
+constexpr float kRescaleSlack = 8.0f;
+
+// The forward kernel.  Per 64-key tile t, every wave:
+//   - issues S^T(t+1) = K(t+1) Q^T on the MFMA pipe (K runs one tile ahead in LDS),
+//   - runs the online softmax of S^T(t) on the VALU while those MFMAs execute,
+//   - accumulates O^T += V(t)^T P^T(t).
+// K and V tiles are row-major in LDS.  The A operand V^T of the PV product is read with
+// transposing LDS reads whose source addresses also apply the key permutation that
+// matches the accumulator layout of P^T: A slot (g, 4*rd + j) holds key 8*rd + 4*g + j of
+// each 16-key chunk.
 template <int D, bool CAUSAL>
-__global__ __launch_bounds__(kThreads) void attn_fwd(const FwdParams p) {
+__global__ __launch_bounds__(kThreads, 2) void attn_fwd(const FwdParams p) {
   using C = FwdCfg<D>;
   __shared__ __align__(16) uint16_t Ks[2][kBN * C::KS];
-  __shared__ __align__(16) uint16_t Vt[2][C::DV * C::VS];
+  __shared__ __align__(16) uint16_t Vs[2][kBN * C::VS];
 
   const int lb = remap_block_id(blockIdx.x, gridDim.x);
   const int per_head = p.nseg * p.nqt;
@@ -130,181 +169,186 @@ __global__ __launch_bounds__(kThreads) void attn_fwd(const FwdParams p) {
   const int kvh = h / p.group;
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, g = lane >> 5, c32 = lane & 31;
   const int qrow = q0 + w * 32 + c32;
-  const long long qstride = static_cast<long long>(p.Hq) * D;
-  const long long kvstride = static_cast<long long>(p.Hkv) * D;
+  const int qstride = p.Hq * D;
+  const int kvstride = p.Hkv * D;
   const uint16_t* kbase = p.k + static_cast<long long>(s0) * kvstride + kvh * D;
   const uint16_t* vbase = p.v + static_cast<long long>(s0) * kvstride + kvh * D;
 
+  // Q, K and V of this (segment, head) as buffer resources: rows past the segment end fall
+  // outside the range and load as zeros.
+  const unsigned seg_bytes_q = static_cast<unsigned>((L - 1) * qstride + D) * 2u;
+  const unsigned seg_bytes_kv = static_cast<unsigned>((L - 1) * kvstride + D) * 2u;
+  const auto rq = make_rsrc(p.q + static_cast<long long>(s0) * qstride + h * D, seg_bytes_q);
+  const auto rk = make_rsrc(kbase, seg_bytes_kv);
+  const auto rv = make_rsrc(vbase, seg_bytes_kv);
+
   bf16x8 qf[C::KC];
   {
-    const uint16_t* qp = p.q + static_cast<long long>(s0 + qrow) * qstride + h * D + g * 8;
+    const unsigned qoff = static_cast<unsigned>(qrow * qstride + g * 8) * 2u;
 #pragma unroll
-    for (int c = 0; c < C::KC; ++c) {
-      uint4 u = make_uint4(0, 0, 0, 0);
-      if (qrow < L) u = *reinterpret_cast<const uint4*>(qp + c * 16);
-      qf[c] = as_bf16x8(u);
-    }
-  }
-  if constexpr (C::DV > D) {
-    // padding rows D..DV-1 of both V^T buffers are zero
-    for (int e = tid; e < 2 * (C::DV - D) * kBN; e += kThreads) {
-      const int buf = e / ((C::DV - D) * kBN);
-      const int r = (e / kBN) % (C::DV - D);
-      const int col = e % kBN;
-      Vt[buf][(D + r) * C::VS + col] = 0;
-    }
+    for (int c = 0; c < C::KC; ++c) qf[c] = as_bf16x8(buf_load16(rq, qoff + c * 32, 0));
   }
 
-  // register staging of one K/V tile
-  uint4 kreg[C::KLOADS];
-  uint4 vreg[4];
-  auto load_tile = [&](int kt) {
-#pragma unroll
-    for (int i = 0; i < C::KLOADS; ++i) {
-      const int id = tid + i * kThreads;
-      const int r = id / (D / 8), cc = id % (D / 8);
-      uint4 u = make_uint4(0, 0, 0, 0);
-      if (id < C::KCHUNKS && kt + r < L)
-        u = *reinterpret_cast<const uint4*>(kbase + static_cast<long long>(kt + r) * kvstride + cc * 8);
-      kreg[i] = u;
-    }
-    if (tid < C::VTHREADS) {
-      const int kq = tid & 15, dc = tid >> 4;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int key = kt + 4 * kq + i;
-        uint4 u = make_uint4(0, 0, 0, 0);
-        if (key < L)
-          u = *reinterpret_cast<const uint4*>(vbase + static_cast<long long>(key) * kvstride + dc * 8);
-        vreg[i] = u;
-      }
-    }
+  // Tile loads: 16-byte chunk id = tid + i*256 -> (row, column chunk); chunks past the tile
+  // get an offset beyond any range (they load zeros and are not stored).
+  unsigned ld_off[C::LOADS];
+  int ld_lds_k[C::LOADS], ld_lds_v[C::LOADS];
+  static_for<0, C::LOADS>([&](auto I) __attribute__((always_inline)) {
+    const int id = tid + I * kThreads;
+    const int r = min(id, C::CHUNKS - 1) / (D / 8), cc = min(id, C::CHUNKS - 1) % (D / 8);
+    ld_off[I] = (id < C::CHUNKS) ? static_cast<unsigned>(r * kvstride + cc * 8) * 2u : kOutOfRange;
+    ld_lds_k[I] = r * C::KS + cc * 8;
+    ld_lds_v[I] = r * C::VS + cc * 8;
+  });
+  const bool last_ok = (C::CHUNKS % kThreads == 0) || (tid + (C::LOADS - 1) * kThreads < C::CHUNKS);
+  uint4 kreg[C::LOADS], vreg[C::LOADS];
+  const unsigned tile_bytes = static_cast<unsigned>(kBN * kvstride) * 2u;
+  auto load_k = [&](int t) __attribute__((always_inline)) {
+    static_for<0, C::LOADS>([&](auto I) __attribute__((always_inline)) {
+      kreg[I] = buf_load16(rk, ld_off[I] + t * tile_bytes, 0);
+    });
   };
-  auto store_tile = [&](int buf) {
+  auto load_v = [&](int t) __attribute__((always_inline)) {
+    static_for<0, C::LOADS>([&](auto I) __attribute__((always_inline)) {
+      vreg[I] = buf_load16(rv, ld_off[I] + t * tile_bytes, 0);
+    });
+  };
+  auto store_k = [&](int buf) __attribute__((always_inline)) {
+    static_for<0, C::LOADS>([&](auto I) __attribute__((always_inline)) {
+      if (I + 1 < C::LOADS || last_ok) *reinterpret_cast<uint4*>(&Ks[buf][ld_lds_k[I]]) = kreg[I];
+    });
+  };
+  auto store_v = [&](int buf) __attribute__((always_inline)) {
+    static_for<0, C::LOADS>([&](auto I) __attribute__((always_inline)) {
+      if (I + 1 < C::LOADS || last_ok) *reinterpret_cast<uint4*>(&Vs[buf][ld_lds_v[I]]) = vreg[I];
+    });
+  };
+
+  // transposed-read source addresses (elements, within a V tile) for this lane
+  const int grp = lane >> 4, li = lane & 15;
+  const int tr_row = 4 * (grp >> 1) + (li >> 2);          // + 8*rd + 16*chunk
+  const int tr_col = 16 * (grp & 1) + 4 * (li & 3);       // + 32*t (dv)
+  const int tr_base = tr_row * C::VS + tr_col;
+
+  auto qk = [&](int buf, f32x16* s) __attribute__((always_inline)) {
 #pragma unroll
-    for (int i = 0; i < C::KLOADS; ++i) {
-      const int id = tid + i * kThreads;
-      if (id < C::KCHUNKS) {
-        const int r = id / (D / 8), cc = id % (D / 8);
-        *reinterpret_cast<uint4*>(&Ks[buf][r * C::KS + cc * 8]) = kreg[i];
-      }
-    }
-    if (tid < C::VTHREADS) {
-      const int kq = tid & 15, dc = tid >> 4;
-      const int pos = vt_pos(kq);
-      const uint32_t* a = reinterpret_cast<const uint32_t*>(&vreg[0]);
-      const uint32_t* b = reinterpret_cast<const uint32_t*>(&vreg[1]);
-      const uint32_t* c = reinterpret_cast<const uint32_t*>(&vreg[2]);
-      const uint32_t* d = reinterpret_cast<const uint32_t*>(&vreg[3]);
+    for (int st = 0; st < 2; ++st) {
+      const uint16_t* kp = &Ks[buf][(st * 32 + c32) * C::KS + g * 8];
+      s[st] = mfma(*reinterpret_cast<const bf16x8*>(kp), qf[0], f32x16{});
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const int wd = e >> 1, sh = (e & 1) * 16;
-        const uint32_t x0 = (a[wd] >> sh) & 0xFFFFu, x1 = (b[wd] >> sh) & 0xFFFFu;
-        const uint32_t x2 = (c[wd] >> sh) & 0xFFFFu, x3 = (d[wd] >> sh) & 0xFFFFu;
-        uint2 pk;
-        pk.x = x0 | (x1 << 16);
-        pk.y = x2 | (x3 << 16);
-        *reinterpret_cast<uint2*>(&Vt[buf][(dc * 8 + e) * C::VS + pos]) = pk;
-      }
+      for (int c = 1; c < C::KC; ++c)
+        s[st] = mfma(*reinterpret_cast<const bf16x8*>(kp + c * 16), qf[c], s[st]);
     }
   };
 
   f32x16 oacc[C::NT];
 #pragma unroll
   for (int t = 0; t < C::NT; ++t) oacc[t] = f32x16{};
-  float m_run = -INFINITY;
-  float l_part = 0.f;
-  const int kend = CAUSAL ? min(L, q0 + kBM) : L;
+  float m_used = -INFINITY;   // max used in the exponentials (log2 domain), per query row
+  float l_part = 0.f;         // this lane's share of the row sum
 
-  load_tile(0);
-  int it = 0;
-  for (int kt = 0; kt < kend; kt += kBN, ++it) {
-    const int buf = it & 1;
-    store_tile(buf);
-    __syncthreads();
-    if (kt + kBN < kend) load_tile(kt + kBN);
-
-    // S^T = K Q^T for two sub-tiles of 32 keys
-    f32x16 s[2];
-#pragma unroll
-    for (int st = 0; st < 2; ++st) {
-      s[st] = f32x16{};
-      const uint16_t* kp = &Ks[buf][(st * 32 + c32) * C::KS + g * 8];
-#pragma unroll
-      for (int c = 0; c < C::KC; ++c)
-        s[st] = mfma(*reinterpret_cast<const bf16x8*>(kp + c * 16), qf[c], s[st]);
-    }
-    // mask and row max (in-lane over 32 keys, then across the half-waves)
-    float mx = -INFINITY;
+  auto softmax_pv = [&](f32x16* s, int kt, int buf) __attribute__((always_inline)) {
     const bool need_mask = (kt + kBN > L) || (CAUSAL && kt + kBN - 1 > q0 + w * 32);
 #pragma unroll
     for (int st = 0; st < 2; ++st) {
+      if (need_mask) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        if (need_mask) {
+        for (int r = 0; r < 16; ++r) {
           const int key = kt + st * 32 + g * 4 + 8 * (r >> 2) + (r & 3);
           const bool ok = (key < L) && (!CAUSAL || key <= qrow);
           if (!ok) s[st][r] = -INFINITY;
         }
-        mx = fmaxf(mx, s[st][r]);
       }
-    }
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    const float m_new = fmaxf(m_run, mx * p.scale_log2);
-    const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
-    const float alpha = fast_exp2(m_run - m_use);
-    m_run = m_new;
+      float mx = fmaxf(fmaxf(s[st][0], s[st][1]), s[st][2]);
 #pragma unroll
-    for (int t = 0; t < C::NT; ++t)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) oacc[t][r] *= alpha;
-    l_part *= alpha;
-#pragma unroll
-    for (int st = 0; st < 2; ++st)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const float pr = fast_exp2(s[st][r] * p.scale_log2 - m_use);
-        s[st][r] = pr;
-        l_part += pr;
-      }
-    // O^T += V^T P^T, 16 keys per MFMA
-#pragma unroll
-    for (int st = 0; st < 2; ++st) {
-#pragma unroll
-      for (int hh = 0; hh < 2; ++hh) {
-        float pv[8];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) pv[e] = s[st][8 * hh + e];
-        const bf16x8 pb = pack_bf16x8(pv);
-        const uint16_t* vp = &Vt[buf][c32 * C::VS + st * 32 + hh * 16 + g * 8];
+      for (int r = 3; r < 15; r += 2) mx = fmaxf(fmaxf(mx, s[st][r]), s[st][r + 1]);
+      mx = fmaxf(mx, s[st][15]);
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * p.scale_log2;
+      if (__builtin_amdgcn_ballot_w64(mx > m_used + kRescaleSlack) != 0ull) {
+        const float m_new = fmaxf(m_used, mx);
+        const float alpha = fast_exp2(m_used - m_new);
+        m_used = m_new;
 #pragma unroll
         for (int t = 0; t < C::NT; ++t)
-          oacc[t] = mfma(*reinterpret_cast<const bf16x8*>(vp + t * 32 * C::VS), pb, oacc[t]);
+#pragma unroll
+          for (int r = 0; r < 16; ++r) oacc[t][r] *= alpha;
+        l_part *= alpha;
+      }
+      const float m_off = (m_used == -INFINITY) ? 0.f : m_used;
+      float pv[16];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        pv[r] = fast_exp2(s[st][r] * p.scale_log2 - m_off);
+        l_part += pv[r];
+      }
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh) {
+        const bf16x8 pb = pack_bf16x8(&pv[8 * hh]);
+        const uint16_t* vp = &Vs[buf][(st * 32 + hh * 16) * C::VS + tr_base];
+#pragma unroll
+        for (int t = 0; t < C::NT; ++t) {
+          if (t * 32 >= D) {
+            // padding rows of O^T (head dim 80): zero A operand
+            oacc[t] = mfma(as_bf16x8(make_uint4(0, 0, 0, 0)), pb, oacc[t]);
+          } else {
+            const uint2 lo = lds_read_tr16(vp + t * 32);
+            const uint2 hi = lds_read_tr16(vp + 8 * C::VS + t * 32);
+            oacc[t] = mfma(as_bf16x8(make_uint4(lo.x, lo.y, hi.x, hi.y)), pb, oacc[t]);
+          }
+        }
       }
     }
+  };
+
+  const int kend = CAUSAL ? min(L, q0 + kBM) : L;
+  const int ntiles = (kend + kBN - 1) / kBN;
+  load_k(0);
+  store_k(0);
+  if (ntiles > 1) load_k(1);
+  load_v(0);
+  __syncthreads();
+  f32x16 sa[2], sb[2];
+  qk(0, sa);
+
+  auto iteration = [&](int t, f32x16* s_cur, f32x16* s_next) __attribute__((always_inline)) {
+    const int kt = t * kBN;
+    if (t + 1 < ntiles) store_k((t + 1) & 1);
+    store_v(t & 1);
+    __syncthreads();
+    if (t + 2 < ntiles) load_k(t + 2);
+    if (t + 1 < ntiles) {
+      load_v(t + 1);
+      qk((t + 1) & 1, s_next);
+    }
+    softmax_pv(s_cur, kt, t & 1);
+  };
+  int t = 0;
+  for (; t + 1 < ntiles; t += 2) {
+    iteration(t, sa, sb);
+    iteration(t + 1, sb, sa);
   }
+  if (t < ntiles) iteration(t, sa, sb);
 
   // epilogue: normalise, store O (bf16) and LSE
-  // fp32 row sum of the unrounded probabilities (the LSE feeds the mass pass)
   const float l = l_part + __shfl_xor(l_part, 32, 64);
   const float inv_l = 1.f / l;
   if (qrow < L) {
     uint16_t* op = p.o + static_cast<long long>(s0 + qrow) * qstride + h * D;
 #pragma unroll
-    for (int t = 0; t < C::NT; ++t) {
+    for (int t2 = 0; t2 < C::NT; ++t2) {
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const int dv = t * 32 + g * 4 + 8 * j;
+        const int dv = t2 * 32 + g * 4 + 8 * j;
         if (dv < D) {
           uint2 pk;
-          pk.x = pack_bf16x2(oacc[t][4 * j + 0] * inv_l, oacc[t][4 * j + 1] * inv_l);
-          pk.y = pack_bf16x2(oacc[t][4 * j + 2] * inv_l, oacc[t][4 * j + 3] * inv_l);
+          pk.x = pack_bf16x2(oacc[t2][4 * j + 0] * inv_l, oacc[t2][4 * j + 1] * inv_l);
+          pk.y = pack_bf16x2(oacc[t2][4 * j + 2] * inv_l, oacc[t2][4 * j + 3] * inv_l);
           *reinterpret_cast<uint2*>(op + dv) = pk;
         }
       }
     }
     if (g == 0 && p.lse)
-      p.lse[static_cast<long long>(h) * p.Ntot + s0 + qrow] = (m_run + __builtin_amdgcn_logf(l)) * kLn2;
+      p.lse[static_cast<long long>(h) * p.Ntot + s0 + qrow] = (m_used + __builtin_amdgcn_logf(l)) * kLn2;
   }
 }
 
@@ -502,8 +546,8 @@ pace_status_t pace_vit_attention(const uint16_t* q, const uint16_t* k, const uin
     return set_error(PACE_ERR_UNSUPPORTED, "pace_vit_attention: head dim %d not in {80, 128}", d);
   const long long nqt = (max_seglen + kBM - 1) / kBM;
   const long long nkt = (max_seglen + kMassKeys - 1) / kMassKeys;
-  PACE_REQUIRE(nqt * nseg * H < (1ll << 31) && static_cast<long long>(N) * H * d < (1ll << 40),
-               "pace_vit_attention: problem too large");
+  PACE_REQUIRE(nqt * nseg * H < (1ll << 31) && 2ll * max_seglen * H * d < (1ll << 31),
+               "pace_vit_attention: a segment must span less than 2 GiB of q/k/v");
   float* lse_buf = lse;
   if (mass != nullptr && lse == nullptr) {
     const size_t need = pace_vit_attention_workspace_size(N, H);
@@ -541,7 +585,8 @@ pace_status_t pace_vit_attention_mass(const uint16_t* q, const uint16_t* k, int 
   if (d != 80 && d != 128)
     return set_error(PACE_ERR_UNSUPPORTED, "pace_vit_attention_mass: head dim %d not in {80, 128}", d);
   const long long nkt = (max_seglen + kMassKeys - 1) / kMassKeys;
-  PACE_REQUIRE(nkt * nseg * H < (1ll << 31), "pace_vit_attention_mass: problem too large");
+  PACE_REQUIRE(nkt * nseg * H < (1ll << 31) && 2ll * max_seglen * H * d < (1ll << 31),
+               "pace_vit_attention_mass: a segment must span less than 2 GiB of q/k");
   MassParams mp{};
   mp.q = q; mp.k = k; mp.lse = lse; mp.mass = mass; mp.cu = cu_seqlens;
   mp.mass_stride = N;
@@ -584,7 +629,8 @@ pace_status_t pace_prefill_attention_with_mass(
   }
   const long long nqt = (max_seqlen + kBM - 1) / kBM;
   const long long nkt = (max_vis_len + kMassKeys - 1) / kMassKeys;
-  PACE_REQUIRE(nqt * B * Hq < (1ll << 31), "pace_prefill_attention_with_mass: problem too large");
+  PACE_REQUIRE(nqt * B * Hq < (1ll << 31) && 2ll * max_seqlen * Hq * d < (1ll << 31),
+               "pace_prefill_attention_with_mass: a sequence must span less than 2 GiB of q");
   float* lse_buf = lse;
   if (lse == nullptr) {
     const size_t need = pace_prefill_attention_workspace_size(Ntot, Hq);
