@@ -86,6 +86,15 @@ __device__ __forceinline__ uint4 buf_load16(__amdgpu_buffer_rsrc_t r, unsigned v
 }
 constexpr unsigned kOutOfRange = 0x7FFFFFF0u;
 
+typedef __attribute__((address_space(3))) void lds_void;
+
+// Buffer-to-LDS DMA: every lane's 16 bytes land at lds + 16 * lane (lds is wave-uniform);
+// lanes whose offset is out of range write zeros.
+__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, void* lds, unsigned voff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)lds, 16, voff, 0, 0, 0);
+}
+__device__ __forceinline__ void wait_vmem() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
 // Compile-time loop: f(integral_constant<int, I>) for I in [B, E), so register arrays
 // are only ever indexed by constants.
 template <int B, int E, typename F>
@@ -120,8 +129,12 @@ struct FwdCfg {
   static constexpr int KC = D / 16;               // QK^T k-chunks
   static constexpr int KS = D + 8;                // LDS row stride of K (elements)
   static constexpr int VS = D + 16;               // LDS row stride of V (elements)
-  static constexpr int CHUNKS = kBN * D / 8;      // 16-byte chunks of a K or V tile
-  static constexpr int LOADS = (CHUNKS + kThreads - 1) / kThreads;
+  static constexpr int KROW = KS / 8;             // 16-byte chunks per K row (incl. padding)
+  static constexpr int VROW = VS / 8;             // 16-byte chunks per V row (incl. padding)
+  static constexpr int KINST = kBN * KROW / 64;   // wave-wide DMA loads per K tile
+  static constexpr int VINST = kBN * VROW / 64;   // wave-wide DMA loads per V tile
+  static constexpr int KPW = (KINST + 3) / 4;     // per wave (4 waves)
+  static constexpr int VPW = (VINST + 3) / 4;
 };
 
 typedef short v4s __attribute__((ext_vector_type(4)));
@@ -167,7 +180,9 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd(const FwdParams p) {
   const int q0 = qt * kBM;
   if (q0 >= L) return;
   const int kvh = h / p.group;
-  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, g = lane >> 5, c32 = lane & 31;
+  // the wave index is wave-uniform: keep it in an SGPR (DMA destinations must be uniform)
+  const int tid = threadIdx.x, w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int lane = tid & 63, g = lane >> 5, c32 = lane & 31;
   const int qrow = q0 + w * 32 + c32;
   const int qstride = p.Hq * D;
   const int kvstride = p.Hkv * D;
@@ -189,38 +204,31 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd(const FwdParams p) {
     for (int c = 0; c < C::KC; ++c) qf[c] = as_bf16x8(buf_load16(rq, qoff + c * 32, 0));
   }
 
-  // Tile loads: 16-byte chunk id = tid + i*256 -> (row, column chunk); chunks past the tile
-  // get an offset beyond any range (they load zeros and are not stored).
-  unsigned ld_off[C::LOADS];
-  int ld_lds_k[C::LOADS], ld_lds_v[C::LOADS];
-  static_for<0, C::LOADS>([&](auto I) __attribute__((always_inline)) {
-    const int id = tid + I * kThreads;
-    const int r = min(id, C::CHUNKS - 1) / (D / 8), cc = min(id, C::CHUNKS - 1) % (D / 8);
-    ld_off[I] = (id < C::CHUNKS) ? static_cast<unsigned>(r * kvstride + cc * 8) * 2u : kOutOfRange;
-    ld_lds_k[I] = r * C::KS + cc * 8;
-    ld_lds_v[I] = r * C::VS + cc * 8;
+  // Tile loads go straight from the buffers to LDS (DMA), 64 16-byte chunks per wave-wide
+  // load, chunks in LDS order: chunk c of a tile is row c / ROW, column chunk c % ROW; the
+  // padding column of each row reads out of range (zeros).  Wave w issues loads w, w+4, ...
+  unsigned koff[C::KPW], voff[C::VPW];
+  static_for<0, C::KPW>([&](auto I) __attribute__((always_inline)) {
+    const int c = (w + 4 * I) * 64 + lane;
+    const int r = c / C::KROW, cc = c % C::KROW;
+    koff[I] = (cc < D / 8 && w + 4 * I < C::KINST) ? static_cast<unsigned>(r * kvstride + cc * 8) * 2u
+                                                    : kOutOfRange;
   });
-  const bool last_ok = (C::CHUNKS % kThreads == 0) || (tid + (C::LOADS - 1) * kThreads < C::CHUNKS);
-  uint4 kreg[C::LOADS], vreg[C::LOADS];
+  static_for<0, C::VPW>([&](auto I) __attribute__((always_inline)) {
+    const int c = (w + 4 * I) * 64 + lane;
+    const int r = c / C::VROW, cc = c % C::VROW;
+    voff[I] = (cc < D / 8 && w + 4 * I < C::VINST) ? static_cast<unsigned>(r * kvstride + cc * 8) * 2u
+                                                    : kOutOfRange;
+  });
   const unsigned tile_bytes = static_cast<unsigned>(kBN * kvstride) * 2u;
-  auto load_k = [&](int t) __attribute__((always_inline)) {
-    static_for<0, C::LOADS>([&](auto I) __attribute__((always_inline)) {
-      kreg[I] = buf_load16(rk, ld_off[I] + t * tile_bytes, 0);
+  auto load_k = [&](int t, int buf) __attribute__((always_inline)) {
+    static_for<0, C::KPW>([&](auto I) __attribute__((always_inline)) {
+      if (w + 4 * I < C::KINST) dma16(rk, &Ks[buf][(w + 4 * I) * 512], koff[I] + t * tile_bytes);
     });
   };
-  auto load_v = [&](int t) __attribute__((always_inline)) {
-    static_for<0, C::LOADS>([&](auto I) __attribute__((always_inline)) {
-      vreg[I] = buf_load16(rv, ld_off[I] + t * tile_bytes, 0);
-    });
-  };
-  auto store_k = [&](int buf) __attribute__((always_inline)) {
-    static_for<0, C::LOADS>([&](auto I) __attribute__((always_inline)) {
-      if (I + 1 < C::LOADS || last_ok) *reinterpret_cast<uint4*>(&Ks[buf][ld_lds_k[I]]) = kreg[I];
-    });
-  };
-  auto store_v = [&](int buf) __attribute__((always_inline)) {
-    static_for<0, C::LOADS>([&](auto I) __attribute__((always_inline)) {
-      if (I + 1 < C::LOADS || last_ok) *reinterpret_cast<uint4*>(&Vs[buf][ld_lds_v[I]]) = vreg[I];
+  auto load_v = [&](int t, int buf) __attribute__((always_inline)) {
+    static_for<0, C::VPW>([&](auto I) __attribute__((always_inline)) {
+      if (w + 4 * I < C::VINST) dma16(rv, &Vs[buf][(w + 4 * I) * 512], voff[I] + t * tile_bytes);
     });
   };
 
@@ -234,10 +242,12 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd(const FwdParams p) {
 #pragma unroll
     for (int st = 0; st < 2; ++st) {
       const uint16_t* kp = &Ks[buf][(st * 32 + c32) * C::KS + g * 8];
-      s[st] = mfma(*reinterpret_cast<const bf16x8*>(kp), qf[0], f32x16{});
+      bf16x8 kf[C::KC];
 #pragma unroll
-      for (int c = 1; c < C::KC; ++c)
-        s[st] = mfma(*reinterpret_cast<const bf16x8*>(kp + c * 16), qf[c], s[st]);
+      for (int c = 0; c < C::KC; ++c) kf[c] = *reinterpret_cast<const bf16x8*>(kp + c * 16);
+      s[st] = mfma(kf[0], qf[0], f32x16{});
+#pragma unroll
+      for (int c = 1; c < C::KC; ++c) s[st] = mfma(kf[c], qf[c], s[st]);
     }
   };
 
@@ -247,87 +257,128 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd(const FwdParams p) {
   float m_used = -INFINITY;   // max used in the exponentials (log2 domain), per query row
   float l_part = 0.f;         // this lane's share of the row sum
 
-  auto softmax_pv = [&](f32x16* s, int kt, int buf) __attribute__((always_inline)) {
+  // Masks, tile max and the (rare) rescale of the accumulators for the tile in s.
+  auto tile_max = [&](f32x16* s, int kt) __attribute__((always_inline)) {
     const bool need_mask = (kt + kBN > L) || (CAUSAL && kt + kBN - 1 > q0 + w * 32);
+    if (need_mask) {
 #pragma unroll
-    for (int st = 0; st < 2; ++st) {
-      if (need_mask) {
+      for (int st = 0; st < 2; ++st)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int key = kt + st * 32 + g * 4 + 8 * (r >> 2) + (r & 3);
           const bool ok = (key < L) && (!CAUSAL || key <= qrow);
           if (!ok) s[st][r] = -INFINITY;
         }
-      }
-      float mx = fmaxf(fmaxf(s[st][0], s[st][1]), s[st][2]);
+    }
+    // max over the 32 in-lane values (three-input max chain), then across the half-waves
+    float mx = fmaxf(fmaxf(s[0][0], s[0][1]), s[0][2]);
 #pragma unroll
-      for (int r = 3; r < 15; r += 2) mx = fmaxf(fmaxf(mx, s[st][r]), s[st][r + 1]);
-      mx = fmaxf(mx, s[st][15]);
-      mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * p.scale_log2;
-      if (__builtin_amdgcn_ballot_w64(mx > m_used + kRescaleSlack) != 0ull) {
-        const float m_new = fmaxf(m_used, mx);
-        const float alpha = fast_exp2(m_used - m_new);
-        m_used = m_new;
+    for (int r = 3; r < 15; r += 2) mx = fmaxf(fmaxf(mx, s[0][r]), s[0][r + 1]);
+    mx = fmaxf(fmaxf(mx, s[0][15]), s[1][0]);
 #pragma unroll
-        for (int t = 0; t < C::NT; ++t)
+    for (int r = 1; r < 15; r += 2) mx = fmaxf(fmaxf(mx, s[1][r]), s[1][r + 1]);
+    mx = fmaxf(mx, s[1][15]);
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * p.scale_log2;
+    // lazy rescale: only when some row's max moved up by more than the slack
+    if (__builtin_amdgcn_ballot_w64(mx > m_used + kRescaleSlack) != 0ull) {
+      const float m_new = fmaxf(m_used, mx);
+      const float alpha = fast_exp2(m_used - m_new);
+      m_used = m_new;
 #pragma unroll
-          for (int r = 0; r < 16; ++r) oacc[t][r] *= alpha;
-        l_part *= alpha;
-      }
-      const float m_off = (m_used == -INFINITY) ? 0.f : m_used;
+      for (int t2 = 0; t2 < C::NT; ++t2)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) oacc[t2][r] *= alpha;
+      l_part *= alpha;
+    }
+  };
+
+  // exp, row sum and bf16 packing of the tile in s, then O^T += V^T P^T (buffer BUF)
+  auto exp_pv = [&](f32x16* s, int buf) __attribute__((always_inline)) {
+    const float m_off = (m_used == -INFINITY) ? 0.f : m_used;
+    bf16x8 pb[2][2];
+#pragma unroll
+    for (int st = 0; st < 2; ++st) {
       float pv[16];
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         pv[r] = fast_exp2(s[st][r] * p.scale_log2 - m_off);
         l_part += pv[r];
       }
+      pb[st][0] = pack_bf16x8(&pv[0]);
+      pb[st][1] = pack_bf16x8(&pv[8]);
+    }
+#pragma unroll
+    for (int st = 0; st < 2; ++st)
 #pragma unroll
       for (int hh = 0; hh < 2; ++hh) {
-        const bf16x8 pb = pack_bf16x8(&pv[8 * hh]);
         const uint16_t* vp = &Vs[buf][(st * 32 + hh * 16) * C::VS + tr_base];
 #pragma unroll
-        for (int t = 0; t < C::NT; ++t) {
-          if (t * 32 >= D) {
-            // padding rows of O^T (head dim 80): zero A operand
-            oacc[t] = mfma(as_bf16x8(make_uint4(0, 0, 0, 0)), pb, oacc[t]);
-          } else {
-            const uint2 lo = lds_read_tr16(vp + t * 32);
-            const uint2 hi = lds_read_tr16(vp + 8 * C::VS + t * 32);
-            oacc[t] = mfma(as_bf16x8(make_uint4(lo.x, lo.y, hi.x, hi.y)), pb, oacc[t]);
-          }
+        for (int t2 = 0; t2 < C::NT; ++t2) {
+          const uint2 lo = lds_read_tr16(vp + t2 * 32);
+          const uint2 hi = lds_read_tr16(vp + 8 * C::VS + t2 * 32);
+          oacc[t2] = mfma(as_bf16x8(make_uint4(lo.x, lo.y, hi.x, hi.y)), pb[st][hh], oacc[t2]);
         }
       }
-    }
   };
 
   const int kend = CAUSAL ? min(L, q0 + kBM) : L;
   const int ntiles = (kend + kBN - 1) / kBN;
-  load_k(0);
-  store_k(0);
-  if (ntiles > 1) load_k(1);
-  load_v(0);
+  // prologue: K(0) and V(0) into buffer 0, K(1) into buffer 1
+  load_k(0, 0);
+  load_v(0, 0);
+  if (ntiles > 1) load_k(1, 1);
+  wait_vmem();
   __syncthreads();
   f32x16 sa[2], sb[2];
   qk(0, sa);
 
-  auto iteration = [&](int t, f32x16* s_cur, f32x16* s_next) __attribute__((always_inline)) {
-    const int kt = t * kBN;
-    if (t + 1 < ntiles) store_k((t + 1) & 1);
-    store_v(t & 1);
-    __syncthreads();
-    if (t + 2 < ntiles) load_k(t + 2);
-    if (t + 1 < ntiles) {
-      load_v(t + 1);
-      qk((t + 1) & 1, s_next);
+  // Iteration t: K(t+1) and V(t) are in LDS.  DMA K(t+2) and V(t+1) into the buffers that
+  // held K(t) and V(t-1) (every wave is past their last use: it passed this barrier), then
+  // one straight-line region interleaves S^T(t+1) = K(t+1) Q^T on the MFMA pipe with the
+  // exponentials of tile t on the VALU, and O^T += V(t)^T P^T(t).
+  auto iteration = [&](auto BUF, auto HAS_NEXT, int t, f32x16* s_cur, f32x16* s_next)
+      __attribute__((always_inline)) {
+    constexpr int buf = decltype(BUF)::value;
+    constexpr bool has_next = decltype(HAS_NEXT)::value;
+    if (t > 0) {
+      wait_vmem();
+      __syncthreads();
     }
-    softmax_pv(s_cur, kt, t & 1);
+    if (t + 2 < ntiles) load_k(t + 2, buf);
+    if (has_next) load_v(t + 1, buf ^ 1);
+    tile_max(s_cur, t * kBN);
+    if constexpr (has_next) {
+      qk(buf ^ 1, s_next);
+      exp_pv(s_cur, buf);
+      // request: LDS reads issued a few MFMAs ahead of their use; every MFMA followed by a
+      // slice of the exponential/row-sum/packing VALU work
+      __builtin_amdgcn_sched_group_barrier(0x100, 3, 0);
+      static_for<0, 2 * C::KC>([&](auto I) __attribute__((always_inline)) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, (I + 3 < 2 * C::KC) ? 1 : 2, 0);
+      });
+      __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+      static_for<0, 4 * C::NT>([&](auto) __attribute__((always_inline)) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+      });
+    } else {
+      exp_pv(s_cur, buf);
+    }
   };
   int t = 0;
-  for (; t + 1 < ntiles; t += 2) {
-    iteration(t, sa, sb);
-    iteration(t + 1, sb, sa);
+  for (; t + 2 < ntiles; t += 2) {
+    iteration(std::integral_constant<int, 0>{}, std::true_type{}, t, sa, sb);
+    iteration(std::integral_constant<int, 1>{}, std::true_type{}, t + 1, sb, sa);
   }
-  if (t < ntiles) iteration(t, sa, sb);
+  if (t + 1 < ntiles) {
+    iteration(std::integral_constant<int, 0>{}, std::true_type{}, t, sa, sb);
+    iteration(std::integral_constant<int, 1>{}, std::false_type{}, t + 1, sb, sa);
+  } else {
+    iteration(std::integral_constant<int, 0>{}, std::false_type{}, t, sa, sb);
+  }
 
   // epilogue: normalise, store O (bf16) and LSE
   const float l = l_part + __shfl_xor(l_part, 32, 64);
