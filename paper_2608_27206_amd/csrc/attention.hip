@@ -423,14 +423,25 @@ struct MassParams {
 constexpr int kMassKeys = 256;   // keys per workgroup (4 waves x 64)
 constexpr int kMassQ = 32;       // query rows per tile
 
+template <int D>
+struct MassCfg {
+  static constexpr int KC = D / 16;
+  static constexpr int QROW = D / 8 + 1;                     // 16-byte chunks per Q row (odd)
+  static constexpr int QS = QROW * 8;                        // LDS row stride (elements)
+  static constexpr int QINST = (kMassQ * QROW + 63) / 64;    // wave-wide DMA loads per Q tile
+  static constexpr int QBUF = QINST * 512;                   // elements per buffer (incl. overhang)
+  static constexpr int QPW = (QINST + 3) / 4;
+};
+
+// The mass kernel.  Every wave keeps 64 keys (two sets of 32) of K in registers as the A
+// operand and streams 32-row query tiles through LDS (DMA, two tiles ahead).  Per tile it
+// issues S^T(t+1) = K Q(t+1)^T on the MFMA pipe interleaved with the VALU work of tile t:
+// P = exp2(S * scale * log2 e - LSE * log2 e), the exact normalised probability, summed per
+// key in fp32 (each lane owns 16 keys of one query column).
 template <int D, bool CAUSAL>
-__global__ __launch_bounds__(kThreads) void attn_mass(const MassParams p) {
-  constexpr int KC = D / 16;
-  constexpr int QS = D + 8;
-  constexpr int QCHUNKS = kMassQ * D / 8;
-  constexpr int QLOADS = (QCHUNKS + kThreads - 1) / kThreads;
-  __shared__ __align__(16) uint16_t Qs[2][kMassQ * QS];
-  __shared__ float L2s[2][kMassQ];
+__global__ __launch_bounds__(kThreads, 2) void attn_mass(const MassParams p) {
+  using C = MassCfg<D>;
+  __shared__ __align__(16) uint16_t Qs[2][C::QBUF];
 
   const int lb = remap_block_id(blockIdx.x, gridDim.x);
   const int per_head = p.nseg * p.nkt;
@@ -447,50 +458,59 @@ __global__ __launch_bounds__(kThreads) void attn_mass(const MassParams p) {
   const int ql = p.q_len ? p.q_len[seg] : L;
   const long long moff = p.mass_off ? p.mass_off[seg] : s0;
   const int kvh = h / p.group;
-  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, g = lane >> 5, c32 = lane & 31;
-  const long long qstride = static_cast<long long>(p.Hq) * D;
-  const long long kvstride = static_cast<long long>(p.Hkv) * D;
+  const int tid = threadIdx.x, w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int lane = tid & 63, g = lane >> 5, c32 = lane & 31;
+  const int qstride = p.Hq * D;
+  const int kvstride = p.Hkv * D;
+  const int kw0 = k0 + w * 64;   // first key of this wave
 
-  // K fragments (A operand of S^T = K Q^T) for this wave's two 32-key sets
-  bf16x8 kf[2][KC];
+  // K fragments (A operand of S^T = K Q^T) for the wave's two 32-key sets; keys past the
+  // receiving range load as zeros (their mass is never written)
+  const auto rk = make_rsrc(p.k + static_cast<long long>(s0) * kvstride + kvh * D,
+                            static_cast<unsigned>((klen - 1) * kvstride + D) * 2u);
+  bf16x8 kf[2][C::KC];
 #pragma unroll
   for (int ks = 0; ks < 2; ++ks) {
-    const int key = k0 + w * 64 + ks * 32 + c32;
-    const uint16_t* kp = p.k + static_cast<long long>(s0 + key) * kvstride + kvh * D + g * 8;
+    const unsigned off = static_cast<unsigned>((kw0 + ks * 32 + c32) * kvstride + g * 8) * 2u;
 #pragma unroll
-    for (int c = 0; c < KC; ++c) {
-      uint4 u = make_uint4(0, 0, 0, 0);
-      if (key < klen) u = *reinterpret_cast<const uint4*>(kp + c * 16);
-      kf[ks][c] = as_bf16x8(u);
-    }
+    for (int c = 0; c < C::KC; ++c) kf[ks][c] = as_bf16x8(buf_load16(rk, off + c * 32, 0));
   }
 
-  const uint16_t* qbase = p.q + static_cast<long long>(s0 + qs) * qstride + h * D;
-  const float* lbase = p.lse + static_cast<long long>(h) * p.Ntot + s0 + qs;
-  uint4 qreg[QLOADS];
-  float lreg = INFINITY;
-  auto load_q = [&](int qt) {
-#pragma unroll
-    for (int i = 0; i < QLOADS; ++i) {
-      const int id = tid + i * kThreads;
-      const int r = id / (D / 8), cc = id % (D / 8);
-      uint4 u = make_uint4(0, 0, 0, 0);
-      if (id < QCHUNKS && qt + r < ql)
-        u = *reinterpret_cast<const uint4*>(qbase + static_cast<long long>(qt + r) * qstride + cc * 8);
-      qreg[i] = u;
-    }
-    if (tid < kMassQ) lreg = (qt + tid < ql) ? lbase[qt + tid] * kLog2e : INFINITY;
+  // querying rows [qs, qs + ql) of the segment: Q rows and their LSE
+  const auto rq = make_rsrc(p.q + static_cast<long long>(s0 + qs) * qstride + h * D,
+                            ql > 0 ? static_cast<unsigned>((ql - 1) * qstride + D) * 2u : 0u);
+  const auto rl = make_rsrc(p.lse + static_cast<long long>(h) * p.Ntot + s0 + qs,
+                            static_cast<unsigned>(ql) * 4u);
+  unsigned qoff[C::QPW];
+  static_for<0, C::QPW>([&](auto I) __attribute__((always_inline)) {
+    const int c = (w + 4 * I) * 64 + lane;
+    const int r = c / C::QROW, cc = c % C::QROW;
+    qoff[I] = (cc < D / 8 && r < kMassQ && w + 4 * I < C::QINST)
+                  ? static_cast<unsigned>(r * qstride + cc * 8) * 2u : kOutOfRange;
+  });
+  const unsigned qtile_bytes = static_cast<unsigned>(kMassQ * qstride) * 2u;
+  auto load_q = [&](int t, int buf) __attribute__((always_inline)) {
+    static_for<0, C::QPW>([&](auto I) __attribute__((always_inline)) {
+      if (w + 4 * I < C::QINST) dma16(rq, &Qs[buf][(w + 4 * I) * 512], qoff[I] + t * qtile_bytes);
+    });
   };
-  auto store_q = [&](int buf) {
+  // LSE of this lane's query row of tile t (log2 units); rows past the range get +inf -> P = 0
+  auto load_lse2 = [&](int t) __attribute__((always_inline)) {
+    const int r = t * kMassQ + c32;
+    const float v = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rl, static_cast<unsigned>(r) * 4u, 0, 0));
+    return (r < ql) ? v * kLog2e : INFINITY;
+  };
+  auto s_tile = [&](int buf, f32x16* s) __attribute__((always_inline)) {
+    const uint16_t* qp = &Qs[buf][c32 * C::QS + g * 8];
+    bf16x8 qb[C::KC];
 #pragma unroll
-    for (int i = 0; i < QLOADS; ++i) {
-      const int id = tid + i * kThreads;
-      if (id < QCHUNKS) {
-        const int r = id / (D / 8), cc = id % (D / 8);
-        *reinterpret_cast<uint4*>(&Qs[buf][r * QS + cc * 8]) = qreg[i];
-      }
+    for (int c = 0; c < C::KC; ++c) qb[c] = *reinterpret_cast<const bf16x8*>(qp + c * 16);
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      s[ks] = mfma(kf[ks][0], qb[0], f32x16{});
+#pragma unroll
+      for (int c = 1; c < C::KC; ++c) s[ks] = mfma(kf[ks][c], qb[c], s[ks]);
     }
-    if (tid < kMassQ) L2s[buf][tid] = lreg;
   };
 
   float macc[2][16];
@@ -499,33 +519,67 @@ __global__ __launch_bounds__(kThreads) void attn_mass(const MassParams p) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) macc[ks][r] = 0.f;
 
-  if (ql > 0) load_q(0);
-  int it = 0;
-  for (int qt = 0; qt < ql; qt += kMassQ, ++it) {
-    const int buf = it & 1;
-    store_q(buf);
-    __syncthreads();
-    if (qt + kMassQ < ql) load_q(qt + kMassQ);
-    bf16x8 qb[KC];
+  auto accumulate = [&](f32x16* s, float l2, int t) __attribute__((always_inline)) {
+    const int qrow = qs + t * kMassQ + c32;
+    // causal masking only where some key of the wave lies after some row of the tile
+    const bool need_mask = CAUSAL && (kw0 + 63 > qs + t * kMassQ);
 #pragma unroll
-    for (int c = 0; c < KC; ++c)
-      qb[c] = *reinterpret_cast<const bf16x8*>(&Qs[buf][c32 * QS + c * 16 + g * 8]);
-    const float l2 = L2s[buf][c32];
-    const int qrow = qs + qt + c32;
-#pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-      f32x16 acc = f32x16{};
-#pragma unroll
-      for (int c = 0; c < KC; ++c) acc = mfma(kf[ks][c], qb[c], acc);
+    for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        float pr = fast_exp2(acc[r] * p.scale_log2 - l2);
-        if (CAUSAL) {
-          const int key = k0 + w * 64 + ks * 32 + g * 4 + 8 * (r >> 2) + (r & 3);
+        float pr = fast_exp2(s[ks][r] * p.scale_log2 - l2);
+        if (need_mask) {
+          const int key = kw0 + ks * 32 + g * 4 + 8 * (r >> 2) + (r & 3);
           if (key > qrow) pr = 0.f;
         }
         macc[ks][r] += pr;
       }
+  };
+
+  const int ntiles = (ql + kMassQ - 1) / kMassQ;
+  if (ntiles > 0) {
+    load_q(0, 0);
+    if (ntiles > 1) load_q(1, 1);
+    float l2_cur = load_lse2(0);
+    wait_vmem();
+    __syncthreads();
+    f32x16 sa[2], sb[2];
+    s_tile(0, sa);
+    auto iteration = [&](auto BUF, auto HAS_NEXT, int t, f32x16* s_cur, f32x16* s_next)
+        __attribute__((always_inline)) {
+      constexpr int buf = decltype(BUF)::value;
+      constexpr bool has_next = decltype(HAS_NEXT)::value;
+      if (t > 0) {
+        wait_vmem();
+        __syncthreads();
+      }
+      if (t + 2 < ntiles) load_q(t + 2, buf);
+      float l2_next = INFINITY;
+      if constexpr (has_next) {
+        l2_next = load_lse2(t + 1);
+        s_tile(buf ^ 1, s_next);
+        accumulate(s_cur, l2_cur, t);
+        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+        static_for<0, 2 * C::KC>([&](auto I) __attribute__((always_inline)) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x002, 8, 0);
+          __builtin_amdgcn_sched_group_barrier(0x100, (I + 2 < C::KC) ? 1 : 0, 0);
+        });
+      } else {
+        accumulate(s_cur, l2_cur, t);
+      }
+      l2_cur = l2_next;
+    };
+    int t = 0;
+    for (; t + 2 < ntiles; t += 2) {
+      iteration(std::integral_constant<int, 0>{}, std::true_type{}, t, sa, sb);
+      iteration(std::integral_constant<int, 1>{}, std::true_type{}, t + 1, sb, sa);
+    }
+    if (t + 1 < ntiles) {
+      iteration(std::integral_constant<int, 0>{}, std::true_type{}, t, sa, sb);
+      iteration(std::integral_constant<int, 1>{}, std::false_type{}, t + 1, sb, sa);
+    } else {
+      iteration(std::integral_constant<int, 0>{}, std::false_type{}, t, sa, sb);
     }
   }
   // column sums over the 32 query lanes of each half-wave
@@ -544,7 +598,7 @@ __global__ __launch_bounds__(kThreads) void attn_mass(const MassParams p) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       if (c32 == r) {
-        const int key = k0 + w * 64 + ks * 32 + g * 4 + 8 * (r >> 2) + (r & 3);
+        const int key = kw0 + ks * 32 + g * 4 + 8 * (r >> 2) + (r & 3);
         if (key < klen) mrow[key] = macc[ks][r];
       }
     }
