@@ -19,8 +19,8 @@
 namespace pace {
 namespace {
 
-constexpr int kPatchesPerTile = 16;   // patches of one patch row per workgroup
-constexpr int kApcThreads = 256;      // 16 threads per patch
+constexpr int kPatchesPerTile = 64;   // patches of one patch row per workgroup
+constexpr int kApcThreads = 256;      // 4 threads per patch for the norms
 constexpr int kMaxPatch = 16;
 
 struct DensityParams {
@@ -31,6 +31,7 @@ struct DensityParams {
   int tiles_x;            // tiles per patch row
   int n_tiles;
   int n_tail;
+  int row_dwords;         // LDS dwords per staged pixel row
   float alpha, gamma;
   float* inv_norm;        // [N]
   float* partial;         // [n_tiles, D]
@@ -41,59 +42,78 @@ struct DensityParams {
   float* rho_out;         // [4]
 };
 
-// Loads the tile's pixels (P rows x up to 16 patches) into LDS as floats x/127.5 - 1.
-__device__ __forceinline__ int load_tile(const DensityParams& p, int tile, float* f, int* py_out,
-                                         int* px0_out) {
+// Dword at byte offset a (4-aligned) of a range-checked buffer of `total` bytes.  A dword
+// that straddles the end is assembled from byte loads (a partly out-of-range dword load
+// would return zero for all four bytes).
+__device__ __forceinline__ uint32_t load_dword_tail(__amdgpu_buffer_rsrc_t rs, int a, int total) {
+  if (a + 4 <= total) return __builtin_amdgcn_raw_buffer_load_b32(rs, static_cast<unsigned>(a), 0, 0);
+  uint32_t v = 0;
+  for (int k = 0; k < 4 && a + k < total; ++k)
+    v |= static_cast<uint32_t>(__builtin_amdgcn_raw_buffer_load_b8(rs, static_cast<unsigned>(a + k), 0, 0)) << (8 * k);
+  return v;
+}
+
+// Stages the tile's pixels (P rows x up to 64 patches) in LDS as bytes, through aligned
+// dword loads of a range-checked buffer (reads never leave the image).  Row r of the tile
+// starts at byte shift[r] of its LDS row.
+__device__ __forceinline__ int stage_tile(const DensityParams& p, int tile, uint32_t* px, int* shift,
+                                          int* py_out, int* px0_out) {
   const int py = tile / p.tiles_x;
   const int px0 = (tile % p.tiles_x) * kPatchesPerTile;
   const int np = min(kPatchesPerTile, p.gw - px0);
   const int row_bytes = np * p.P * 3;
-  const long long rowstride = static_cast<long long>(p.W) * 3;
-  const uint8_t* src = p.img + static_cast<long long>(py * p.P) * rowstride + px0 * p.P * 3;
-  const int lds_stride = kPatchesPerTile * p.P * 3;
-  for (int e = threadIdx.x; e < p.P * row_bytes; e += kApcThreads) {
-    const int r = e / row_bytes, cb = e - r * row_bytes;
-    f[r * lds_stride + cb] =
-        static_cast<float>(src[r * rowstride + cb]) * (1.0f / 127.5f) - 1.0f;
+  const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint8_t*>(p.img), (short)0, p.H * p.W * 3, 0x00020000);
+  const int nd = (row_bytes + 3) / 4 + 1;
+  for (int e = threadIdx.x; e < p.P * nd; e += kApcThreads) {
+    const int r = e / nd, dd = e - r * nd;
+    const int b0 = (py * p.P + r) * p.W * 3 + px0 * p.P * 3;
+    const int a0 = b0 & ~3;
+    if (dd == 0) shift[r] = b0 - a0;
+    px[r * p.row_dwords + dd] = load_dword_tail(rs, a0 + 4 * dd, p.H * p.W * 3);
   }
   *py_out = py;
   *px0_out = px0;
   return np;
 }
 
-// Feature component e of patch j within the tile (LDS layout [row][tile column byte]).
-__device__ __forceinline__ float feat(const float* f, int P, int j, int e) {
+// Feature component e (patch row, pixel column, channel) of patch j: x/127.5 - 1.
+__device__ __forceinline__ float feat(const uint8_t* pxb, const int* shift, int row_bytes_lds, int P,
+                                      int j, int e) {
   const int r = e / (3 * P), cb = e - r * (3 * P);
-  return f[r * (kPatchesPerTile * P * 3) + j * 3 * P + cb];
+  return static_cast<float>(pxb[r * row_bytes_lds + shift[r] + j * 3 * P + cb]) * (1.0f / 127.5f) - 1.0f;
 }
 
 template <int PASS>
 __global__ __launch_bounds__(kApcThreads) void apc_patch_pass(const DensityParams p) {
-  extern __shared__ float lds[];
-  float* f = lds;                                                 // [P][16*P*3] floats
-  float* inv = f + p.P * kPatchesPerTile * p.P * 3;               // [16]
+  extern __shared__ uint32_t lds[];
+  uint32_t* px = lds;                                             // [P][row_dwords]
+  float* inv = reinterpret_cast<float*>(px + p.P * p.row_dwords);  // [64]
   float* chat = inv + kPatchesPerTile;                            // [D] (pass 1)
+  __shared__ int shift[kMaxPatch];
   const int tile = blockIdx.x;
   int py, px0;
-  const int np = load_tile(p, tile, f, &py, &px0);
+  const int np = stage_tile(p, tile, px, shift, &py, &px0);
   if (PASS == 1)
     for (int e = threadIdx.x; e < p.D; e += kApcThreads) chat[e] = p.chat[e];
   __syncthreads();
-  const int j = threadIdx.x >> 4, t = threadIdx.x & 15;
+  const uint8_t* pxb = reinterpret_cast<const uint8_t*>(px);
+  const int rb = p.row_dwords * 4;
+  const int j = threadIdx.x >> 2, t = threadIdx.x & 3;
   float acc = 0.f;
   if (j < np) {
     if (PASS == 0) {
-      for (int e = t; e < p.D; e += 16) { const float x = feat(f, p.P, j, e); acc += x * x; }
+      for (int e = t; e < p.D; e += 4) { const float x = feat(pxb, shift, rb, p.P, j, e); acc += x * x; }
     } else {
       const float s = p.inv_norm[py * p.gw + px0 + j];
-      for (int e = t; e < p.D; e += 16) {
-        const float x = feat(f, p.P, j, e) * s - chat[e];
+      for (int e = t; e < p.D; e += 4) {
+        const float x = feat(pxb, shift, rb, p.P, j, e) * s - chat[e];
         acc += x * x;
       }
     }
   }
-#pragma unroll
-  for (int o = 8; o >= 1; o >>= 1) acc += __shfl_xor(acc, o, 64);
+  acc += __shfl_xor(acc, 1, 64);
+  acc += __shfl_xor(acc, 2, 64);
   if (PASS == 0) {
     if (j < np && t == 0) {
       const float in = 1.0f / sqrtf(acc);
@@ -104,7 +124,7 @@ __global__ __launch_bounds__(kApcThreads) void apc_patch_pass(const DensityParam
     // tile partial of sum_i T_i, patches added in index order
     for (int e = threadIdx.x; e < p.D; e += kApcThreads) {
       float s = 0.f;
-      for (int jj = 0; jj < np; ++jj) s += feat(f, p.P, jj, e) * inv[jj];
+      for (int jj = 0; jj < np; ++jj) s += feat(pxb, shift, rb, p.P, jj, e) * inv[jj];
       p.partial[static_cast<long long>(tile) * p.D + e] = s;
     }
   } else {
@@ -175,7 +195,10 @@ __global__ __launch_bounds__(1024) void apc_tail(const DensityParams p) {
 }
 
 // ---------------------------------------------------------------- resize
-constexpr int kRsTX = 64;    // output columns per workgroup
+// One workgroup per output tile of ty x tx pixels.  It computes the tile's column and row
+// tap weights once (LDS), stages the input region it needs (range-checked dword loads,
+// so reads never leave the image), runs the horizontal pass into LDS in fp32 and the
+// vertical pass straight to the output.
 constexpr int kRsThreads = 256;
 constexpr int kRsMaxLds = 64 * 1024;
 
@@ -183,11 +206,13 @@ struct ResizeParams {
   const uint8_t* src;
   uint8_t* dst;
   int H, W, oH, oW;
-  int ty;                 // output rows per workgroup
-  int tx;                 // output columns per workgroup (<= kRsTX)
+  int ty, tx;             // output rows / columns per workgroup
+  int ntx, nty;           // tap slots per output column / row (upper bound of the tap count)
   int rows_cap;           // input rows staged per workgroup
-  float sx, sy;           // input pixels per output pixel
-  float fx, fy;           // kernel stretch (max(1, s))
+  int cols_cap;           // input columns staged per workgroup
+  int row_dwords;         // LDS dwords per staged input row
+  // LDS carve (in 4-byte words)
+  int o_wx, o_wy, o_lox, o_loy, o_pix, o_h;
 };
 
 __device__ __forceinline__ float keys_cubic(float x) {
@@ -197,80 +222,87 @@ __device__ __forceinline__ float keys_cubic(float x) {
   return 0.f;
 }
 
-// Taps of output coordinate o along an axis of n inputs resized to m outputs.  Input
-// pixel i's distance to o's sample point, in kernel units, is
-//   ((2i + 1) m - (2o + 1) n) / (2 max(n, m)),
-// whose numerator is an exact integer, so the weights carry a single rounding.
-struct Taps {
-  int lo, hi;        // inclusive tap range (extra taps at |dist| >= 2 weigh 0)
-  long long num0;    // numerator at i = lo
-  long long step;    // numerator increment per tap (2m)
-  float inv_den;     // 1 / (2 max(n, m))
-  float inv_sum;     // 1 / sum of the weights
-};
-
-__device__ __forceinline__ Taps make_taps(int o, int n, int m) {
-  Taps t;
-  const long long den = 2ll * (n > m ? n : m);
-  // support in input pixels: 2 * max(1, n/m); centre (o + 0.5) n / m
+// Taps of output coordinate o along an axis of n inputs resized to m outputs: input i's
+// distance to o's sample point in kernel units is ((2i+1) m - (2o+1) n) / (2 max(n, m)); its
+// numerator is an exact integer, so every weight carries a single rounding.  Writes
+// `slots` normalised weights for inputs lo .. lo+slots-1 (zero past the image or the
+// support) and returns lo.
+__device__ __forceinline__ int make_taps(int o, int n, int m, int slots, float* w) {
   const float centre = (static_cast<float>(o) + 0.5f) * static_cast<float>(n) / static_cast<float>(m);
   const float support = 2.f * fmaxf(1.f, static_cast<float>(n) / static_cast<float>(m));
-  t.lo = max(static_cast<int>(floorf(centre - support - 0.5f)) - 1, 0);
-  t.hi = min(static_cast<int>(ceilf(centre + support - 0.5f)) + 1, n - 1);
-  t.step = 2ll * m;
-  t.num0 = (2ll * t.lo + 1) * m - (2ll * o + 1) * n;
-  t.inv_den = 1.f / static_cast<float>(den);
+  const int lo = max(static_cast<int>(floorf(centre - support - 0.5f)) - 1, 0);
+  const float inv_den = 1.f / static_cast<float>(2ll * (n > m ? n : m));
+  long long num = (2ll * lo + 1) * m - (2ll * o + 1) * n;
   float sum = 0.f;
-  long long num = t.num0;
-  for (int i = t.lo; i <= t.hi; ++i, num += t.step) sum += keys_cubic(static_cast<float>(num) * t.inv_den);
-  t.inv_sum = 1.f / sum;
-  return t;
+  for (int j = 0; j < slots; ++j, num += 2ll * m) {
+    const float wt = (lo + j < n) ? keys_cubic(static_cast<float>(num) * inv_den) : 0.f;
+    w[j] = wt;
+    sum += wt;
+  }
+  const float inv = 1.f / sum;
+  for (int j = 0; j < slots; ++j) w[j] *= inv;
+  return lo;
 }
 
 __global__ __launch_bounds__(kRsThreads) void apc_resize(const ResizeParams p) {
-  extern __shared__ float hbuf[];   // [rows_cap][tx][3] horizontally filtered rows
-  const int ox0 = blockIdx.x * p.tx;
-  const int oy0 = blockIdx.y * p.ty;
-  const int oy1 = min(p.oH, oy0 + p.ty);
-  // input rows needed by this tile's output rows
-  const Taps tfirst = make_taps(oy0, p.H, p.oH);
-  const Taps tlast = make_taps(oy1 - 1, p.H, p.oH);
-  const int ylo = tfirst.lo;
-  const int nrows = min(tlast.hi - ylo + 1, p.rows_cap);   // the host sizes rows_cap to fit
-  const int ncols = min(p.tx, p.oW - ox0);
-  // horizontal pass into LDS
-  for (int e = threadIdx.x; e < nrows * ncols; e += kRsThreads) {
-    const int r = e / ncols, x = e - r * ncols;
-    const Taps t = make_taps(ox0 + x, p.W, p.oW);
-    const uint8_t* row = p.src + static_cast<long long>(ylo + r) * p.W * 3;
+  extern __shared__ float sm[];
+  float* wx = sm + p.o_wx;                      // [tx][ntx]
+  float* wy = sm + p.o_wy;                      // [ty][nty]
+  int* lox = reinterpret_cast<int*>(sm + p.o_lox);
+  int* loy = reinterpret_cast<int*>(sm + p.o_loy);
+  uint32_t* pix = reinterpret_cast<uint32_t*>(sm + p.o_pix);   // [rows_cap][row_dwords]
+  float* hb = sm + p.o_h;                       // [rows_cap][tx][3]
+  __shared__ int shift[256];                    // byte shift of each staged row
+  const int ox0 = blockIdx.x * p.tx, oy0 = blockIdx.y * p.ty;
+  const int ncols = min(p.tx, p.oW - ox0), nrows = min(p.ty, p.oH - oy0);
+  for (int c = threadIdx.x; c < ncols; c += kRsThreads) lox[c] = make_taps(ox0 + c, p.W, p.oW, p.ntx, wx + c * p.ntx);
+  for (int r = threadIdx.x; r < nrows; r += kRsThreads) loy[r] = make_taps(oy0 + r, p.H, p.oH, p.nty, wy + r * p.nty);
+  __syncthreads();
+  const int xlo = lox[0], ylo = loy[0];
+  const int xin = min(lox[ncols - 1] + p.ntx, p.W) - xlo;      // staged input columns
+  const int yin = min(loy[nrows - 1] + p.nty, p.H) - ylo;      // staged input rows
+  // stage input rows ylo .. ylo+yin-1, bytes [xlo*3, (xlo+xin)*3) of each, as aligned dwords
+  const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint8_t*>(p.src), (short)0, p.H * p.W * 3, 0x00020000);
+  const int nd = (xin * 3 + 3) / 4 + 1;
+  for (int e = threadIdx.x; e < yin * nd; e += kRsThreads) {
+    const int r = e / nd, d = e - r * nd;
+    const int b0 = (ylo + r) * p.W * 3 + xlo * 3;
+    const int a0 = b0 & ~3;
+    if (d == 0) shift[r] = b0 - a0;
+    pix[r * p.row_dwords + d] = load_dword_tail(rs, a0 + 4 * d, p.H * p.W * 3);
+  }
+  __syncthreads();
+  const uint8_t* pixb = reinterpret_cast<const uint8_t*>(pix);
+  // horizontal pass: staged rows x output columns x 3 channels
+  for (int e = threadIdx.x; e < yin * ncols; e += kRsThreads) {
+    const int r = e / ncols, c = e - r * ncols;
+    const uint8_t* row = pixb + r * p.row_dwords * 4 + shift[r] + (lox[c] - xlo) * 3;
+    const float* w = wx + c * p.ntx;
+    const int nt = min(p.ntx, p.W - lox[c]);
     float a0 = 0.f, a1 = 0.f, a2 = 0.f;
-    long long num = t.num0;
-    for (int i = t.lo; i <= t.hi; ++i, num += t.step) {
-      const float w = keys_cubic(static_cast<float>(num) * t.inv_den);
-      a0 += w * static_cast<float>(row[3 * i + 0]);
-      a1 += w * static_cast<float>(row[3 * i + 1]);
-      a2 += w * static_cast<float>(row[3 * i + 2]);
+    for (int j = 0; j < nt; ++j) {
+      const float wt = w[j];
+      a0 += wt * static_cast<float>(row[3 * j + 0]);
+      a1 += wt * static_cast<float>(row[3 * j + 1]);
+      a2 += wt * static_cast<float>(row[3 * j + 2]);
     }
-    float* h = hbuf + (r * p.tx + x) * 3;
-    h[0] = a0 * t.inv_sum; h[1] = a1 * t.inv_sum; h[2] = a2 * t.inv_sum;
+    float* h = hb + (r * p.tx + c) * 3;
+    h[0] = a0; h[1] = a1; h[2] = a2;
   }
   __syncthreads();
   // vertical pass and store
-  for (int e = threadIdx.x; e < (oy1 - oy0) * ncols * 3; e += kRsThreads) {
-    const int yy = e / (ncols * 3), rem = e - yy * ncols * 3;
-    const int x = rem / 3, ch = rem - x * 3;
-    const Taps t = make_taps(oy0 + yy, p.H, p.oH);
+  for (int e = threadIdx.x; e < nrows * ncols * 3; e += kRsThreads) {
+    const int r = e / (ncols * 3), rem = e - r * ncols * 3;
+    const int c = rem / 3, ch = rem - c * 3;
+    const float* w = wy + r * p.nty;
+    const int base = loy[r] - ylo;
+    const int nt = min(p.nty, p.H - loy[r]);
     float acc = 0.f;
-    long long num = t.num0;
-    for (int i = t.lo; i <= t.hi; ++i, num += t.step) {
-      const int r = i - ylo;
-      if (r < 0 || r >= nrows) continue;
-      const float w = keys_cubic(static_cast<float>(num) * t.inv_den);
-      acc += w * hbuf[(r * p.tx + x) * 3 + ch];
-    }
-    const float v = floorf(acc * t.inv_sum + 0.5f);
+    for (int j = 0; j < nt; ++j) acc += w[j] * hb[((base + j) * p.tx + c) * 3 + ch];
+    const float v = floorf(acc + 0.5f);
     const int u = static_cast<int>(fminf(fmaxf(v, 0.f), 255.f));
-    p.dst[(static_cast<long long>(oy0 + yy) * p.oW + ox0 + x) * 3 + ch] = static_cast<uint8_t>(u);
+    p.dst[(static_cast<long long>(oy0 + r) * p.oW + ox0 + c) * 3 + ch] = static_cast<uint8_t>(u);
   }
 }
 
@@ -310,7 +342,8 @@ pace_status_t pace_apc_density(const uint8_t* img, int H, int W, int patch, doub
   PACE_REQUIRE(tail_frac > 0 && tail_frac <= 1, "pace_apc_density: tail_frac must be in (0, 1]");
   PACE_REQUIRE(gamma > 0.f, "pace_apc_density: gamma must be > 0");
   const long long N = static_cast<long long>(H / patch) * (W / patch);
-  PACE_REQUIRE(N < (1ll << 28), "pace_apc_density: too many patches");
+  PACE_REQUIRE(N < (1ll << 28) && static_cast<long long>(H) * W * 3 < (1ll << 31),
+               "pace_apc_density: image too large");
   const size_t need = pace_apc_density_workspace_size(H, W, patch);
   if (workspace == nullptr || workspace_bytes < need)
     return set_error(PACE_ERR_WORKSPACE, "pace_apc_density: workspace %zu < %zu bytes",
@@ -322,6 +355,7 @@ pace_status_t pace_apc_density(const uint8_t* img, int H, int W, int patch, doub
   p.D = 3 * patch * patch;
   p.tiles_x = (p.gw + kPatchesPerTile - 1) / kPatchesPerTile;
   p.n_tiles = p.gh * p.tiles_x;
+  p.row_dwords = (kPatchesPerTile * patch * 3 + 3) / 4 + 2;
   int nt = pace_keep_count(tail_frac, p.N);
   p.n_tail = nt < 1 ? 1 : nt;
   p.alpha = alpha; p.gamma = gamma;
@@ -334,8 +368,7 @@ pace_status_t pace_apc_density(const uint8_t* img, int H, int W, int patch, doub
   float* dws = c.take<float>(p.N);
   p.d = d_out ? d_out : dws;
   p.rho_out = rho_out;
-  const size_t lds = (static_cast<size_t>(patch) * kPatchesPerTile * patch * 3 + kPatchesPerTile +
-                      p.D) * sizeof(float);
+  const size_t lds = (static_cast<size_t>(patch) * p.row_dwords + kPatchesPerTile + p.D) * sizeof(float);
   hipLaunchKernelGGL(apc_patch_pass<0>, dim3(p.n_tiles), dim3(kApcThreads), lds, stream, p);
   pace_status_t st = check_launch("apc_patch_pass<0>");
   if (st != PACE_OK) return st;
@@ -354,29 +387,39 @@ pace_status_t pace_apc_downsample(const uint8_t* src, int H, int W, uint8_t* dst
   PACE_REQUIRE(src && dst, "pace_apc_downsample: null device pointer");
   PACE_REQUIRE(H >= 1 && W >= 1 && oH >= 1 && oW >= 1 && oH <= H && oW <= W,
                "pace_apc_downsample: sizes %dx%d -> %dx%d must shrink or keep", H, W, oH, oW);
+  PACE_REQUIRE(static_cast<long long>(H) * W * 3 < (1ll << 31), "pace_apc_downsample: image too large");
+  const double sx = static_cast<double>(W) / oW, sy = static_cast<double>(H) / oH;
+  if (sx > 32.0 || sy > 32.0)
+    return set_error(PACE_ERR_UNSUPPORTED, "pace_apc_downsample: shrink factor above 32");
   ResizeParams p{};
   p.src = src; p.dst = dst;
   p.H = H; p.W = W; p.oH = oH; p.oW = oW;
-  p.sx = static_cast<float>(static_cast<double>(W) / oW);
-  p.sy = static_cast<float>(static_cast<double>(H) / oH);
-  p.fx = p.sx > 1.f ? p.sx : 1.f;
-  p.fy = p.sy > 1.f ? p.sy : 1.f;
-  if (p.fx > 32.f || p.fy > 32.f)
-    return set_error(PACE_ERR_UNSUPPORTED, "pace_apc_downsample: shrink factor above 32");
-  // rows of input per tile of ty output rows: ty*sy + 4*fy + 5 (generous bound, taps
-  // include one extra zero-weight pixel on each side)
-  int ty = 16, tx = kRsTX;
-  auto rows_for = [&](int t) { return static_cast<int>(ceilf(t * p.sy + 4.f * p.fy)) + 5; };
-  auto lds_for = [&](int t, int x) { return static_cast<size_t>(rows_for(t)) * x * 3 * sizeof(float); };
-  while (lds_for(ty, tx) > kRsMaxLds) {
+  // taps of one output pixel span at most 4*s + 4 inputs (the support plus one zero-weight
+  // guard tap on each side)
+  p.ntx = static_cast<int>(ceil(4.0 * (sx > 1 ? sx : 1))) + 4;
+  p.nty = static_cast<int>(ceil(4.0 * (sy > 1 ? sy : 1))) + 4;
+  int ty = 16, tx = 64;
+  auto plan = [&](int t_y, int t_x, ResizeParams& q) {
+    q.ty = t_y; q.tx = t_x;
+    q.rows_cap = static_cast<int>(ceil((t_y - 1) * sy)) + q.nty + 1;
+    q.cols_cap = static_cast<int>(ceil((t_x - 1) * sx)) + q.ntx + 1;
+    q.row_dwords = (q.cols_cap * 3 + 3) / 4 + 2;
+    int off = 0;
+    q.o_wx = off; off += t_x * q.ntx;
+    q.o_wy = off; off += t_y * q.nty;
+    q.o_lox = off; off += t_x;
+    q.o_loy = off; off += t_y;
+    q.o_pix = off; off += q.rows_cap * q.row_dwords;
+    q.o_h = off; off += q.rows_cap * t_x * 3;
+    return static_cast<size_t>(off) * 4;
+  };
+  size_t lds = plan(ty, tx, p);
+  while (lds > kRsMaxLds || p.rows_cap > 256) {
     if (ty > 1) ty >>= 1;
-    else if (tx > 8) tx >>= 1;
+    else if (tx > 1) tx >>= 1;
     else return set_error(PACE_ERR_UNSUPPORTED, "pace_apc_downsample: shrink factor too large");
+    lds = plan(ty, tx, p);
   }
-  const size_t lds = lds_for(ty, tx);
-  p.ty = ty;
-  p.tx = tx;
-  p.rows_cap = rows_for(ty);
   dim3 grid((oW + tx - 1) / tx, (oH + ty - 1) / ty);
   hipLaunchKernelGGL(apc_resize, grid, dim3(kRsThreads), lds, stream, p);
   return check_launch("apc_resize");

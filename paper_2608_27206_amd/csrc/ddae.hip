@@ -42,29 +42,42 @@ __device__ __forceinline__ int find_segment(const SelectParams& p, int i) {
   return lo;
 }
 
+// Four lanes per token, each summing every fourth head; combined by shuffles in a fixed
+// order (deterministic).
 __global__ __launch_bounds__(256) void ddae_token_maps(const SelectParams p) {
-  const int i = blockIdx.x * 256 + threadIdx.x;
-  if (i >= p.nv_total) return;
-  const int b = find_segment(p, i);
+  const int i = blockIdx.x * 64 + (threadIdx.x >> 2);
+  const int part = threadIdx.x & 3;
+  const bool valid = i < p.nv_total;
+  const int ii = valid ? i : 0;
+  const int b = find_segment(p, ii);
   const int base = p.cu_nv[b];
-  const int local = p.vis_perm ? p.vis_perm[i] : (i - base);
+  const int local = p.vis_perm ? p.vis_perm[ii] : (ii - base);
   const long long patch0 = static_cast<long long>(base + local) * p.merge;
   float v = 0.f;
-  if (p.merge == 4) {
-    for (int h = 0; h < p.Hv; ++h) {
-      const float4 m = *reinterpret_cast<const float4*>(p.vis_mass + h * p.vis_stride + patch0);
-      v += (m.x + m.y) + (m.z + m.w);
-    }
-  } else {
-    for (int h = 0; h < p.Hv; ++h) {
-      const float* row = p.vis_mass + h * p.vis_stride + patch0;
-      for (int t = 0; t < p.merge; ++t) v += row[t];
+  if (valid) {
+    if (p.merge == 4) {
+      for (int h = part; h < p.Hv; h += 4) {
+        const float4 m = *reinterpret_cast<const float4*>(p.vis_mass + h * p.vis_stride + patch0);
+        v += (m.x + m.y) + (m.z + m.w);
+      }
+    } else {
+      for (int h = part; h < p.Hv; h += 4) {
+        const float* row = p.vis_mass + h * p.vis_stride + patch0;
+        for (int t = 0; t < p.merge; ++t) v += row[t];
+      }
     }
   }
   float l = 0.f;
-  for (int h = 0; h < p.Hl; ++h) l += p.llm_mass[static_cast<long long>(h) * p.nv_total + i];
-  p.vraw[i] = v;
-  p.lraw[i] = l;
+  if (valid)
+    for (int h = part; h < p.Hl; h += 4) l += p.llm_mass[static_cast<long long>(h) * p.nv_total + ii];
+  v += __shfl_xor(v, 1, 64);
+  l += __shfl_xor(l, 1, 64);
+  v += __shfl_xor(v, 2, 64);
+  l += __shfl_xor(l, 2, 64);
+  if (valid && part == 0) {
+    p.vraw[i] = v;
+    p.lraw[i] = l;
+  }
 }
 
 constexpr int kSelThreads = 1024;
@@ -174,7 +187,7 @@ __global__ __launch_bounds__(256) void gather_rows(const uint4* __restrict__ hid
 pace_status_t run_select(SelectParams& p, const void* hidden, size_t row_bytes, void* out,
                          hipStream_t stream, bool need_maps) {
   if (need_maps && p.nv_total > 0) {
-    const int blocks = (p.nv_total + 255) / 256;
+    const int blocks = (p.nv_total + 63) / 64;
     hipLaunchKernelGGL(ddae_token_maps, dim3(blocks), dim3(256), 0, stream, p);
     pace_status_t st = check_launch("ddae_token_maps");
     if (st != PACE_OK) return st;

@@ -118,9 +118,22 @@ __device__ uint32_t block_radix_select(int n, int k, Get get, uint32_t* hist, in
   for (int shift = 24; shift >= 0; shift -= 8) {
     for (int i = threadIdx.x; i < 256; i += blockDim.x) hist[i] = 0;
     __syncthreads();
-    for (int i = threadIdx.x; i < n; i += blockDim.x) {
-      const uint32_t key = get(i);
-      if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
+    for (int i0 = 0; i0 < n; i0 += blockDim.x) {
+      const int i = i0 + threadIdx.x;
+      const uint32_t key = (i < n) ? get(i) : 0u;
+      const bool active = (i < n) && (key & mask) == prefix;
+      const uint32_t bin = (key >> shift) & 255u;
+      // values with a common leading part land in one bin: one atomic per wave then
+      const unsigned long long act = __ballot(active);
+      if (act == 0ull) continue;
+      const int leader = __ffsll(static_cast<long long>(act)) - 1;
+      const uint32_t lead_bin = __shfl(bin, leader, 64);
+      const unsigned long long same = __ballot(active && bin == lead_bin);
+      if (same == act) {
+        if ((threadIdx.x & 63) == leader) atomicAdd(&hist[lead_bin], static_cast<uint32_t>(__popcll(act)));
+      } else if (active) {
+        atomicAdd(&hist[bin], 1u);
+      }
     }
     __syncthreads();
     // Suffix sums over digits (high to low) by the first wave: lane j holds digits

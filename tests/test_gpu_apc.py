@@ -40,6 +40,20 @@ def test_density_ragged_tiles_and_tails():
     _check_density(img, 0.2)
 
 
+def test_density_odd_byte_count():
+    """7-pixel patches on a 21 x 35 image: H*W*3 is odd, so the last pixels sit in a
+    partial dword at the end of the buffer."""
+    from paper_2608_27206_amd import pace
+    import torch
+    img = np.random.default_rng(6).integers(0, 256, size=(21, 35, 3), dtype=np.uint8)
+    assert (img.size % 4) != 0
+    rho, d = pace.apc_density(dev_u8(img), 7, 0.1, 0.6, 1.5)
+    torch.cuda.synchronize()
+    ref = oapc.apc_density(img, 7, 0.1)
+    np.testing.assert_allclose(host(d), ref["d"], atol=1e-4)
+    np.testing.assert_allclose(host(rho), [ref["rho_g"], ref["rho_d"], ref["rho"], ref["phi"]], atol=1e-4)
+
+
 def test_density_uniform_and_mirrored():
     u = np.full((56, 84, 3), 77, np.uint8)
     rho = _check_density(u)
