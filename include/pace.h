@@ -67,6 +67,15 @@ int pace_version(void);
 int pace_keep_count(double ratio, int n);
 
 /*
+ * Per-image keep count set by APC's density for a batch of images: the keep ratio is
+ * ratio_lo + (ratio_hi - ratio_lo) * rho, clamped to [ratio_lo, ratio_hi], and
+ * K = pace_keep_count(ratio, n).  (The paper maps rho to an area ratio, Section 3.2; a
+ * batch with per-image token budgets needs a keep ratio, and this linear map is the
+ * reading used here.)  Returns -1 on bad arguments.
+ */
+int pace_keep_from_density(double rho, double ratio_lo, double ratio_hi, int n);
+
+/*
  * Output size of APC's resize (Section 3.2, "Adaptive Condensation"; Appendix
  * implementation details: area ratio r = rho, each side scaled by sqrt(r), and a
  * hard budget overrides rho when it allows less).

@@ -39,6 +39,13 @@ def keep_count(ratio: float, n: int) -> int:
     return max(0, min(n, k))
 
 
+def keep_from_density(rho: float, n: int, ratio_lo: float = 0.05, ratio_hi: float = 0.25) -> int:
+    """Per-image K in a batch whose keep ratios APC's density sets (reading: linear map of rho
+    onto [ratio_lo, ratio_hi])."""
+    r = min(max(ratio_lo + (ratio_hi - ratio_lo) * rho, ratio_lo), ratio_hi)
+    return keep_count(r, n)
+
+
 def minmax(x: np.ndarray) -> np.ndarray:
     lo, hi = float(x.min()), float(x.max())
     if hi == lo:

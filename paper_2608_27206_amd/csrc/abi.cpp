@@ -39,6 +39,13 @@ int pace_keep_count(double ratio, int n) {
   return static_cast<int>(k);
 }
 
+int pace_keep_from_density(double rho, double ratio_lo, double ratio_hi, int n) {
+  if (n < 0 || !isfinite(rho) || !(ratio_lo >= 0) || !(ratio_hi >= ratio_lo) || ratio_hi > 1) return -1;
+  double r = ratio_lo + (ratio_hi - ratio_lo) * rho;
+  r = fmin(fmax(r, ratio_lo), ratio_hi);
+  return pace_keep_count(r, n);
+}
+
 pace_status_t pace_apc_target_size(double rho, int H, int W, double min_pixels, double max_pixels,
                                    int snap, int* oH, int* oW) {
   PACE_REQUIRE(H > 0 && W > 0 && snap > 0, "pace_apc_target_size: H=%d W=%d snap=%d must be > 0",

@@ -29,6 +29,7 @@ _PROTOS = {
     "pace_last_error": (ctypes.c_char_p, []),
     "pace_version": (c_int, []),
     "pace_keep_count": (c_int, [c_double, c_int]),
+    "pace_keep_from_density": (c_int, [c_double, c_double, c_double, c_int]),
     "pace_apc_target_size": (c_int, [c_double, c_int, c_int, c_double, c_double, c_int, c_int_p,
                                      c_int_p]),
     "pace_apc_density_workspace_size": (c_size, [c_int, c_int, c_int]),
@@ -105,6 +106,10 @@ def _ws(nbytes: int, device) -> torch.Tensor:
 # ---------------------------------------------------------------- host helpers
 def keep_count(ratio: float, n: int) -> int:
     return int(lib().pace_keep_count(float(ratio), int(n)))
+
+
+def keep_from_density(rho: float, n: int, ratio_lo: float = 0.05, ratio_hi: float = 0.25) -> int:
+    return int(lib().pace_keep_from_density(float(rho), float(ratio_lo), float(ratio_hi), int(n)))
 
 
 def apc_target_size(rho: float, H: int, W: int, min_pixels: float, max_pixels: float, snap: int):

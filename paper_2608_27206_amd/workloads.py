@@ -68,9 +68,10 @@ def bf16_bits_to_f64(b: np.ndarray) -> np.ndarray:
 
 # ---------------------------------------------------------------- images
 def make_image(config_id: int, H: int, W: int, stream: int = S_IMAGE,
-               textured_frac: float = 0.20) -> np.ndarray:
-    """uint8 HWC RGB image: smooth per-channel sinusoids, with a seeded 20% of the
-    14x14 patches replaced by uniform random texture."""
+               textured_frac: float = 0.20, level: float = 127.5, amplitude: float = 100.0) -> np.ndarray:
+    """uint8 HWC RGB image: smooth per-channel sinusoids around `level` with the given
+    amplitude, with a seeded fraction of the 14x14 patches replaced by uniform random
+    texture."""
     g = rng(config_id, stream)
     a = g.uniform(0.5, 2.0, size=3)
     b = g.uniform(0.5, 2.0, size=3)
@@ -79,7 +80,7 @@ def make_image(config_id: int, H: int, W: int, stream: int = S_IMAGE,
     x = np.arange(W, dtype=np.float64)[None, :]
     img = np.empty((H, W, 3), dtype=np.uint8)
     for c in range(3):
-        v = 127.5 + 100.0 * np.sin(2.0 * math.pi * (a[c] * x / W + b[c] * y / H) + ph[c])
+        v = level + amplitude * np.sin(2.0 * math.pi * (a[c] * x / W + b[c] * y / H) + ph[c])
         img[:, :, c] = np.clip(np.floor(v + 0.5), 0, 255).astype(np.uint8)
     gh, gw = H // PATCH, W // PATCH
     n = gh * gw
@@ -91,6 +92,14 @@ def make_image(config_id: int, H: int, W: int, stream: int = S_IMAGE,
             py, px = divmod(int(p), gw)
             img[py * PATCH:(py + 1) * PATCH, px * PATCH:(px + 1) * PATCH, :] = tex[t]
     return img
+
+
+def varlen_image_styles(config_id: int = 4, count: int = 8):
+    """Seeded per-image (level, amplitude, textured fraction): from document-like pages (bright,
+    flat, sparse detail) to busy scenes, so APC's density differs between images."""
+    g = rng(config_id, S_IMAGE)
+    return [(float(g.uniform(60.0, 235.0)), float(g.uniform(3.0, 80.0)), float(g.uniform(0.01, 0.30)))
+            for _ in range(count)]
 
 
 # ---------------------------------------------------------------- token layout
@@ -300,7 +309,9 @@ def make_workload(config_id: int) -> Workload:
                         downsample_scale=(0.5 if config_id == 3 else None))
     if config_id == 4:
         res = varlen_resolutions(4)
-        imgs = [make_image(4, h, w, stream=S_IMAGE * 100 + i) for i, (h, w) in enumerate(res)]
+        styles = varlen_image_styles(4, len(res))
+        imgs = [make_image(4, h, w, stream=S_IMAGE * 100 + i, textured_frac=tf, level=lv, amplitude=am)
+                for i, ((h, w), (lv, am, tf)) in enumerate(zip(res, styles))]
         lays = [vit_layout(h // PATCH, w // PATCH) for (h, w) in res]
         vit = _vit(4, lays)
         gt = rng(4, S_TEXT)
@@ -310,5 +321,5 @@ def make_workload(config_id: int) -> Workload:
         nv = sum(L.n_vis for L in lays)
         return Workload(config_id=4, name=name, images=imgs, layouts=lays, vit=vit, prefill=pre,
                         vit_mass=None, vit_merge=MERGE, hidden=_hidden(4, nv), keep_ratio=0.10,
-                        fusion_mode=0, meta={"resolutions": res, "text_lens": texts})
+                        fusion_mode=0, meta={"resolutions": res, "text_lens": texts, "styles": styles})
     raise ValueError(f"unknown config {config_id}")

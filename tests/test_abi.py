@@ -41,6 +41,15 @@ def test_keep_count_matches_oracle():
     assert pace.keep_count(0.1, -1) == -1
 
 
+def test_keep_from_density_matches_oracle():
+    from oracle import ddae
+    for rho in (0.0, 0.2, 0.371, 0.5, 0.9999, 1.0, 1.3, -0.2):
+        for n in (1, 37, 256, 2304, 10549):
+            assert pace.keep_from_density(rho, n) == ddae.keep_from_density(rho, n)
+    assert pace.keep_from_density(0.5, 100) == 15
+    assert pace.lib().pace_keep_from_density(0.5, 0.3, 0.2, 10) == -1
+
+
 def test_target_size_matches_oracle():
     from oracle import apc
     cases = [(0.25, 1120, 1680, 0, 1e12, 28), (0.9, 2000, 2000, 0, 1e6, 1), (0.0, 1000, 1000, 250000, 1e12, 1),
