@@ -95,6 +95,18 @@ __device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, void* lds, unsig
 }
 __device__ __forceinline__ void wait_vmem() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
+// (own value, value of lane l ^ 32) via v_permlane32_swap: a VALU op, unlike a shuffle
+__device__ __forceinline__ float max_halves(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(unsigned, x), __builtin_bit_cast(unsigned, x),
+                                                  false, false);
+  return fmaxf(__builtin_bit_cast(float, r[0]), __builtin_bit_cast(float, r[1]));
+}
+__device__ __forceinline__ float sum_halves(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(unsigned, x), __builtin_bit_cast(unsigned, x),
+                                                  false, false);
+  return __builtin_bit_cast(float, r[0]) + __builtin_bit_cast(float, r[1]);
+}
+
 // Compile-time loop: f(integral_constant<int, I>) for I in [B, E), so register arrays
 // are only ever indexed by constants.
 template <int B, int E, typename F>
@@ -255,7 +267,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd(const FwdParams p) {
 #pragma unroll
   for (int t = 0; t < C::NT; ++t) oacc[t] = f32x16{};
   float m_used = -INFINITY;   // max used in the exponentials (log2 domain), per query row
-  float l_part = 0.f;         // this lane's share of the row sum
+  float l_part[4] = {0.f, 0.f, 0.f, 0.f};   // this lane's share of the row sum, 4 chains
 
   // Masks, tile max and the (rare) rescale of the accumulators for the tile in s.
   auto tile_max = [&](f32x16* s, int kt) __attribute__((always_inline)) {
@@ -270,14 +282,18 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd(const FwdParams p) {
           if (!ok) s[st][r] = -INFINITY;
         }
     }
-    // max over the 32 in-lane values (three-input max chain), then across the half-waves
-    float mx = fmaxf(fmaxf(s[0][0], s[0][1]), s[0][2]);
+    // max over the 32 in-lane values as a shallow tree of three-input maxima, then across
+    // the half-waves
+    float m1[11];
 #pragma unroll
-    for (int r = 3; r < 15; r += 2) mx = fmaxf(fmaxf(mx, s[0][r]), s[0][r + 1]);
-    mx = fmaxf(fmaxf(mx, s[0][15]), s[1][0]);
-#pragma unroll
-    for (int r = 1; r < 15; r += 2) mx = fmaxf(fmaxf(mx, s[1][r]), s[1][r + 1]);
-    mx = fmaxf(mx, s[1][15]);
+    for (int i = 0; i < 10; ++i) {
+      const int a = 3 * i;
+      m1[i] = fmaxf(fmaxf(s[a >> 4][a & 15], s[(a + 1) >> 4][(a + 1) & 15]), s[(a + 2) >> 4][(a + 2) & 15]);
+    }
+    m1[10] = fmaxf(s[1][14], s[1][15]);
+    const float m2a = fmaxf(fmaxf(m1[0], m1[1]), m1[2]), m2b = fmaxf(fmaxf(m1[3], m1[4]), m1[5]);
+    const float m2c = fmaxf(fmaxf(m1[6], m1[7]), m1[8]), m2d = fmaxf(m1[9], m1[10]);
+    float mx = fmaxf(fmaxf(m2a, m2b), fmaxf(m2c, m2d));
     mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * p.scale_log2;
     // lazy rescale: only when some row's max moved up by more than the slack
     if (__builtin_amdgcn_ballot_w64(mx > m_used + kRescaleSlack) != 0ull) {
@@ -288,7 +304,8 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd(const FwdParams p) {
       for (int t2 = 0; t2 < C::NT; ++t2)
 #pragma unroll
         for (int r = 0; r < 16; ++r) oacc[t2][r] *= alpha;
-      l_part *= alpha;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) l_part[i] *= alpha;
     }
   };
 
@@ -302,7 +319,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd(const FwdParams p) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         pv[r] = fast_exp2(s[st][r] * p.scale_log2 - m_off);
-        l_part += pv[r];
+        l_part[r & 3] += pv[r];
       }
       pb[st][0] = pack_bf16x8(&pv[0]);
       pb[st][1] = pack_bf16x8(&pv[8]);
@@ -381,7 +398,8 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd(const FwdParams p) {
   }
 
   // epilogue: normalise, store O (bf16) and LSE
-  const float l = l_part + __shfl_xor(l_part, 32, 64);
+  const float lp = (l_part[0] + l_part[1]) + (l_part[2] + l_part[3]);
+  const float l = lp + __shfl_xor(lp, 32, 64);
   const float inv_l = 1.f / l;
   if (qrow < L) {
     uint16_t* op = p.o + static_cast<long long>(s0 + qrow) * qstride + h * D;
