@@ -86,26 +86,34 @@ __device__ __forceinline__ uint4 buf_load16(__amdgpu_buffer_rsrc_t r, unsigned v
 }
 constexpr unsigned kOutOfRange = 0x7FFFFFF0u;
 
-typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(3))) const char lds_char;
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+
+// The same buffer resource as four scalar words, for the DMA below.
+__device__ __forceinline__ i32x4 make_dma_rsrc(const void* base, unsigned bytes) {
+  const unsigned long long a = reinterpret_cast<unsigned long long>(base);
+  i32x4 r;
+  r.x = __builtin_amdgcn_readfirstlane(static_cast<int>(a & 0xffffffffull));
+  r.y = __builtin_amdgcn_readfirstlane(static_cast<int>((a >> 32) & 0xffffull));   // stride 0
+  r.z = __builtin_amdgcn_readfirstlane(static_cast<int>(bytes));
+  r.w = 0x00020000;
+  return r;
+}
 
 // Buffer-to-LDS DMA: every lane's 16 bytes land at lds + 16 * lane (lds is wave-uniform);
-// lanes whose offset is out of range write zeros.
-__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, void* lds, unsigned voff) {
-  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)lds, 16, voff, 0, 0, 0);
+// lanes whose offset is out of range write zeros.  Issued from inline assembly so that the
+// compiler does not track it: otherwise it places a wait for every DMA in flight before
+// each later LDS read, which would stall on the prefetch just issued.  Completion is
+// awaited explicitly with wait_vmem() and a barrier before the tile is read.
+__device__ __forceinline__ unsigned lds_u32(const void* p) {
+  return static_cast<unsigned>(reinterpret_cast<unsigned long long>((const lds_char*)p));
+}
+__device__ __forceinline__ void dma16(i32x4 r, unsigned lds, unsigned voff) {
+  const unsigned m0 = __builtin_amdgcn_readfirstlane(lds);
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+               :: "s"(m0), "v"(voff), "s"(r) : "memory", "m0");
 }
 __device__ __forceinline__ void wait_vmem() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
-
-// (own value, value of lane l ^ 32) via v_permlane32_swap: a VALU op, unlike a shuffle
-__device__ __forceinline__ float max_halves(float x) {
-  const auto r = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(unsigned, x), __builtin_bit_cast(unsigned, x),
-                                                  false, false);
-  return fmaxf(__builtin_bit_cast(float, r[0]), __builtin_bit_cast(float, r[1]));
-}
-__device__ __forceinline__ float sum_halves(float x) {
-  const auto r = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(unsigned, x), __builtin_bit_cast(unsigned, x),
-                                                  false, false);
-  return __builtin_bit_cast(float, r[0]) + __builtin_bit_cast(float, r[1]);
-}
 
 // Compile-time loop: f(integral_constant<int, I>) for I in [B, E), so register arrays
 // are only ever indexed by constants.
@@ -206,8 +214,8 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd(const FwdParams p) {
   const unsigned seg_bytes_q = static_cast<unsigned>((L - 1) * qstride + D) * 2u;
   const unsigned seg_bytes_kv = static_cast<unsigned>((L - 1) * kvstride + D) * 2u;
   const auto rq = make_rsrc(p.q + static_cast<long long>(s0) * qstride + h * D, seg_bytes_q);
-  const auto rk = make_rsrc(kbase, seg_bytes_kv);
-  const auto rv = make_rsrc(vbase, seg_bytes_kv);
+  const auto rk = make_dma_rsrc(kbase, seg_bytes_kv);
+  const auto rv = make_dma_rsrc(vbase, seg_bytes_kv);
 
   bf16x8 qf[C::KC];
   {
@@ -233,14 +241,15 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd(const FwdParams p) {
                                                     : kOutOfRange;
   });
   const unsigned tile_bytes = static_cast<unsigned>(kBN * kvstride) * 2u;
+  const unsigned ks_lds = lds_u32(&Ks[0][0]), vs_lds = lds_u32(&Vs[0][0]);
   auto load_k = [&](int t, int buf) __attribute__((always_inline)) {
     static_for<0, C::KPW>([&](auto I) __attribute__((always_inline)) {
-      if (w + 4 * I < C::KINST) dma16(rk, &Ks[buf][(w + 4 * I) * 512], koff[I] + t * tile_bytes);
+      if (w + 4 * I < C::KINST) dma16(rk, ks_lds + (buf * kBN * C::KS + (w + 4 * I) * 512) * 2, koff[I] + t * tile_bytes);
     });
   };
   auto load_v = [&](int t, int buf) __attribute__((always_inline)) {
     static_for<0, C::VPW>([&](auto I) __attribute__((always_inline)) {
-      if (w + 4 * I < C::VINST) dma16(rv, &Vs[buf][(w + 4 * I) * 512], voff[I] + t * tile_bytes);
+      if (w + 4 * I < C::VINST) dma16(rv, vs_lds + (buf * kBN * C::VS + (w + 4 * I) * 512) * 2, voff[I] + t * tile_bytes);
     });
   };
 
@@ -357,10 +366,9 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd(const FwdParams p) {
       __attribute__((always_inline)) {
     constexpr int buf = decltype(BUF)::value;
     constexpr bool has_next = decltype(HAS_NEXT)::value;
-    if (t > 0) {
-      wait_vmem();
-      __syncthreads();
-    }
+    // every wave is past its reads of K(t) (also the prologue's) before K(t+2) replaces it
+    wait_vmem();
+    __syncthreads();
     if (t + 2 < ntiles) load_k(t + 2, buf);
     if (has_next) load_v(t + 1, buf ^ 1);
     tile_max(s_cur, t * kBN);
@@ -398,6 +406,254 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd(const FwdParams p) {
   }
 
   // epilogue: normalise, store O (bf16) and LSE
+  const float lp = (l_part[0] + l_part[1]) + (l_part[2] + l_part[3]);
+  const float l = lp + __shfl_xor(lp, 32, 64);
+  const float inv_l = 1.f / l;
+  if (qrow < L) {
+    uint16_t* op = p.o + static_cast<long long>(s0 + qrow) * qstride + h * D;
+#pragma unroll
+    for (int t2 = 0; t2 < C::NT; ++t2) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int dv = t2 * 32 + g * 4 + 8 * j;
+        if (dv < D) {
+          uint2 pk;
+          pk.x = pack_bf16x2(oacc[t2][4 * j + 0] * inv_l, oacc[t2][4 * j + 1] * inv_l);
+          pk.y = pack_bf16x2(oacc[t2][4 * j + 2] * inv_l, oacc[t2][4 * j + 3] * inv_l);
+          *reinterpret_cast<uint2*>(op + dv) = pk;
+        }
+      }
+    }
+    if (g == 0 && p.lse)
+      p.lse[static_cast<long long>(h) * p.Ntot + s0 + qrow] = (m_used + __builtin_amdgcn_logf(l)) * kLn2;
+  }
+}
+
+// ---------------------------------------------------------------- forward, ping-pong
+// For long segments without a causal mask.  A workgroup = 8 waves x 32 query rows; wave w
+// runs on SIMD w % 4, so every SIMD holds one wave of each group (waves 0-3 and 4-7).
+// Each wave alternates two phases per 64-key tile t:
+//   A: online softmax of S^T(t) on the VALU (max, exponentials, row sums, bf16 packing);
+//   B: S^T(t+1) = K(t+1) Q^T and O^T += V(t)^T P^T(t) on the MFMA pipe.
+// The second group runs half a tile behind the first, and a workgroup barrier separates
+// consecutive half-steps, so on every SIMD one wave is in its VALU phase while the other
+// keeps the matrix core busy, instead of both contending for the same unit.  The waves
+// of the first group also issue the K/V DMA: K(t+2) and V(t+1) during their phase B of
+// tile t (the buffers' previous tiles were last read a half-step earlier), completed
+// before the barrier that ends their next phase A, i.e. before any wave reads them.
+// Workgroup barrier that also fences the instruction scheduler, so no computation
+// migrates between the two sides of a phase boundary.
+__device__ __forceinline__ void phase_sync() {
+  __builtin_amdgcn_sched_barrier(0);
+  __syncthreads();
+  __builtin_amdgcn_sched_barrier(0);
+}
+
+constexpr int kPPWaves = 8;
+constexpr int kPPThreads = 64 * kPPWaves;
+constexpr int kPPBM = 32 * kPPWaves;   // query rows per workgroup
+
+template <int D>
+__global__ __launch_bounds__(kPPThreads, 2) void attn_fwd_pp(const FwdParams p) {
+  using C = FwdCfg<D>;
+  __shared__ __align__(16) uint16_t Ks[2][kBN * C::KS];
+  __shared__ __align__(16) uint16_t Vs[2][kBN * C::VS];
+
+  const int lb = remap_block_id(blockIdx.x, gridDim.x);
+  const int per_head = p.nseg * p.nqt;
+  const int h = lb / per_head;
+  const int rem = lb - h * per_head;
+  const int seg = rem / p.nqt;
+  const int qt = rem - seg * p.nqt;
+  const int s0 = p.cu[seg];
+  const int L = p.cu[seg + 1] - s0;
+  const int q0 = qt * kPPBM;
+  if (q0 >= L) return;   // the whole workgroup leaves together
+  const int kvh = h / p.group;
+  const int tid = threadIdx.x, w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int grp = w >> 2, wl = w & 3;
+  const int lane = tid & 63, g = lane >> 5, c32 = lane & 31;
+  const int qrow = q0 + w * 32 + c32;
+  const int qstride = p.Hq * D;
+  const int kvstride = p.Hkv * D;
+
+  const unsigned seg_bytes_q = static_cast<unsigned>((L - 1) * qstride + D) * 2u;
+  const unsigned seg_bytes_kv = static_cast<unsigned>((L - 1) * kvstride + D) * 2u;
+  const auto rq = make_rsrc(p.q + static_cast<long long>(s0) * qstride + h * D, seg_bytes_q);
+  const auto rk = make_dma_rsrc(p.k + static_cast<long long>(s0) * kvstride + kvh * D, seg_bytes_kv);
+  const auto rv = make_dma_rsrc(p.v + static_cast<long long>(s0) * kvstride + kvh * D, seg_bytes_kv);
+
+  bf16x8 qf[C::KC];
+  {
+    const unsigned qoff = static_cast<unsigned>(qrow * qstride + g * 8) * 2u;
+#pragma unroll
+    for (int c = 0; c < C::KC; ++c) qf[c] = as_bf16x8(buf_load16(rq, qoff + c * 32, 0));
+  }
+
+  // DMA chunk offsets (same chunk order as attn_fwd), issued by the 4 waves of group 0
+  unsigned koff[C::KPW], voff[C::VPW];
+  static_for<0, C::KPW>([&](auto I) __attribute__((always_inline)) {
+    const int c = (wl + 4 * I) * 64 + lane;
+    const int r = c / C::KROW, cc = c % C::KROW;
+    koff[I] = (cc < D / 8 && wl + 4 * I < C::KINST) ? static_cast<unsigned>(r * kvstride + cc * 8) * 2u
+                                                     : kOutOfRange;
+  });
+  static_for<0, C::VPW>([&](auto I) __attribute__((always_inline)) {
+    const int c = (wl + 4 * I) * 64 + lane;
+    const int r = c / C::VROW, cc = c % C::VROW;
+    voff[I] = (cc < D / 8 && wl + 4 * I < C::VINST) ? static_cast<unsigned>(r * kvstride + cc * 8) * 2u
+                                                     : kOutOfRange;
+  });
+  const unsigned tile_bytes = static_cast<unsigned>(kBN * kvstride) * 2u;
+  const unsigned ks_lds = lds_u32(&Ks[0][0]), vs_lds = lds_u32(&Vs[0][0]);
+  auto load_k = [&](int t, int buf) __attribute__((always_inline)) {
+    static_for<0, C::KPW>([&](auto I) __attribute__((always_inline)) {
+      if (wl + 4 * I < C::KINST) dma16(rk, ks_lds + (buf * kBN * C::KS + (wl + 4 * I) * 512) * 2, koff[I] + t * tile_bytes);
+    });
+  };
+  auto load_v = [&](int t, int buf) __attribute__((always_inline)) {
+    static_for<0, C::VPW>([&](auto I) __attribute__((always_inline)) {
+      if (wl + 4 * I < C::VINST) dma16(rv, vs_lds + (buf * kBN * C::VS + (wl + 4 * I) * 512) * 2, voff[I] + t * tile_bytes);
+    });
+  };
+
+  const int tgrp = lane >> 4, li = lane & 15;
+  const int tr_row = 4 * (tgrp >> 1) + (li >> 2);
+  const int tr_col = 16 * (tgrp & 1) + 4 * (li & 3);
+  const int tr_base = tr_row * C::VS + tr_col;
+
+  f32x16 s[2];
+  auto qk = [&](int buf) __attribute__((always_inline)) {
+#pragma unroll
+    for (int st = 0; st < 2; ++st) {
+      const uint16_t* kp = &Ks[buf][(st * 32 + c32) * C::KS + g * 8];
+      bf16x8 kf[C::KC];
+#pragma unroll
+      for (int c = 0; c < C::KC; ++c) kf[c] = *reinterpret_cast<const bf16x8*>(kp + c * 16);
+      s[st] = mfma(kf[0], qf[0], f32x16{});
+#pragma unroll
+      for (int c = 1; c < C::KC; ++c) s[st] = mfma(kf[c], qf[c], s[st]);
+    }
+  };
+
+  f32x16 oacc[C::NT];
+#pragma unroll
+  for (int t2 = 0; t2 < C::NT; ++t2) oacc[t2] = f32x16{};
+  float m_used = -INFINITY;
+  float l_part[4] = {0.f, 0.f, 0.f, 0.f};
+  bf16x8 pb[2][2];
+
+  // phase A: mask, max, (rare) rescale, exponentials, row sums, packing
+  auto softmax = [&](int kt) __attribute__((always_inline)) {
+    if (kt + kBN > L) {
+#pragma unroll
+      for (int st = 0; st < 2; ++st)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int key = kt + st * 32 + g * 4 + 8 * (r >> 2) + (r & 3);
+          if (key >= L) s[st][r] = -INFINITY;
+        }
+    }
+    float m1[11];
+#pragma unroll
+    for (int i = 0; i < 10; ++i) {
+      const int a = 3 * i;
+      m1[i] = fmaxf(fmaxf(s[a >> 4][a & 15], s[(a + 1) >> 4][(a + 1) & 15]), s[(a + 2) >> 4][(a + 2) & 15]);
+    }
+    m1[10] = fmaxf(s[1][14], s[1][15]);
+    const float m2a = fmaxf(fmaxf(m1[0], m1[1]), m1[2]), m2b = fmaxf(fmaxf(m1[3], m1[4]), m1[5]);
+    const float m2c = fmaxf(fmaxf(m1[6], m1[7]), m1[8]), m2d = fmaxf(m1[9], m1[10]);
+    float mx = fmaxf(fmaxf(m2a, m2b), fmaxf(m2c, m2d));
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * p.scale_log2;
+    if (__builtin_amdgcn_ballot_w64(mx > m_used + kRescaleSlack) != 0ull) {
+      const float m_new = fmaxf(m_used, mx);
+      const float alpha = fast_exp2(m_used - m_new);
+      m_used = m_new;
+#pragma unroll
+      for (int t2 = 0; t2 < C::NT; ++t2)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) oacc[t2][r] *= alpha;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) l_part[i] *= alpha;
+    }
+    const float m_off = (m_used == -INFINITY) ? 0.f : m_used;
+#pragma unroll
+    for (int st = 0; st < 2; ++st) {
+      float pv[16];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        pv[r] = fast_exp2(s[st][r] * p.scale_log2 - m_off);
+        l_part[r & 3] += pv[r];
+      }
+      pb[st][0] = pack_bf16x8(&pv[0]);
+      pb[st][1] = pack_bf16x8(&pv[8]);
+    }
+    // pin the row sums and the packed P here: left alone, the compiler sinks them past the
+    // barrier into the MFMA phase
+#pragma unroll
+    for (int i = 0; i < 4; ++i) asm volatile("" : "+v"(l_part[i]));
+#pragma unroll
+    for (int st = 0; st < 2; ++st)
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh) asm volatile("" : "+v"(pb[st][hh]));
+  };
+
+  auto pv = [&](int buf) __attribute__((always_inline)) {
+#pragma unroll
+    for (int st = 0; st < 2; ++st)
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh) {
+        const uint16_t* vp = &Vs[buf][(st * 32 + hh * 16) * C::VS + tr_base];
+#pragma unroll
+        for (int t2 = 0; t2 < C::NT; ++t2) {
+          const uint2 lo = lds_read_tr16(vp + t2 * 32);
+          const uint2 hi = lds_read_tr16(vp + 8 * C::VS + t2 * 32);
+          oacc[t2] = mfma(as_bf16x8(make_uint4(lo.x, lo.y, hi.x, hi.y)), pb[st][hh], oacc[t2]);
+        }
+      }
+  };
+
+  const int ntiles = (L + kBN - 1) / kBN;
+  if (grp == 0) {
+    load_k(0, 0);
+    load_v(0, 0);
+    if (ntiles > 1) load_k(1, 1);
+    wait_vmem();
+  }
+  phase_sync();
+  qk(0);
+  if (grp == 1) phase_sync();   // group 1 runs half a tile behind
+  int t = 0;
+  for (; t + 1 < ntiles; ++t) {
+    const int b = t & 1;
+    softmax(t * kBN);
+    if (grp == 0) wait_vmem();   // the tiles issued during the previous phase B
+    phase_sync();
+    if (grp == 0) {
+      if (t + 2 < ntiles) load_k(t + 2, b);
+      load_v(t + 1, b ^ 1);
+    }
+    qk(b ^ 1);
+    pv(b);
+    __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+    static_for<0, 2 * C::KC>([&](auto I) __attribute__((always_inline)) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, (I + 4 < 2 * C::KC) ? 1 : 2, 0);
+    });
+    static_for<0, 4 * C::NT>([&](auto) __attribute__((always_inline)) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+    });
+    phase_sync();
+  }
+  // last tile: nothing left to load or to multiply ahead
+  softmax(t * kBN);
+  if (grp == 0) wait_vmem();
+  phase_sync();
+  pv(t & 1);
+  phase_sync();
+  if (grp == 0) phase_sync();
+
   const float lp = (l_part[0] + l_part[1]) + (l_part[2] + l_part[3]);
   const float l = lp + __shfl_xor(lp, 32, 64);
   const float inv_l = 1.f / l;
@@ -495,8 +751,8 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mass(const MassParams p) {
   }
 
   // querying rows [qs, qs + ql) of the segment: Q rows and their LSE
-  const auto rq = make_rsrc(p.q + static_cast<long long>(s0 + qs) * qstride + h * D,
-                            ql > 0 ? static_cast<unsigned>((ql - 1) * qstride + D) * 2u : 0u);
+  const auto rq = make_dma_rsrc(p.q + static_cast<long long>(s0 + qs) * qstride + h * D,
+                                ql > 0 ? static_cast<unsigned>((ql - 1) * qstride + D) * 2u : 0u);
   const auto rl = make_rsrc(p.lse + static_cast<long long>(h) * p.Ntot + s0 + qs,
                             static_cast<unsigned>(ql) * 4u);
   unsigned qoff[C::QPW];
@@ -507,9 +763,10 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mass(const MassParams p) {
                   ? static_cast<unsigned>(r * qstride + cc * 8) * 2u : kOutOfRange;
   });
   const unsigned qtile_bytes = static_cast<unsigned>(kMassQ * qstride) * 2u;
+  const unsigned qs_lds = lds_u32(&Qs[0][0]);
   auto load_q = [&](int t, int buf) __attribute__((always_inline)) {
     static_for<0, C::QPW>([&](auto I) __attribute__((always_inline)) {
-      if (w + 4 * I < C::QINST) dma16(rq, &Qs[buf][(w + 4 * I) * 512], qoff[I] + t * qtile_bytes);
+      if (w + 4 * I < C::QINST) dma16(rq, qs_lds + (buf * C::QBUF + (w + 4 * I) * 512) * 2, qoff[I] + t * qtile_bytes);
     });
   };
   // LSE of this lane's query row of tile t (log2 units); rows past the range get +inf -> P = 0
@@ -567,10 +824,9 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mass(const MassParams p) {
         __attribute__((always_inline)) {
       constexpr int buf = decltype(BUF)::value;
       constexpr bool has_next = decltype(HAS_NEXT)::value;
-      if (t > 0) {
-        wait_vmem();
-        __syncthreads();
-      }
+      // every wave is past its reads of Q(t) (also the prologue's) before Q(t+2) replaces it
+      wait_vmem();
+      __syncthreads();
       if (t + 2 < ntiles) load_q(t + 2, buf);
       float l2_next = INFINITY;
       if constexpr (has_next) {
@@ -622,13 +878,23 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mass(const MassParams p) {
     }
 }
 
+// Segments at least this long (without a causal mask, head dim 80) take the ping-pong
+// forward kernel; at head dim 128 its per-wave state would not fit in registers.
+constexpr int kPPMinSeg = 1024;
+
 template <int D>
-pace_status_t launch_attention(const FwdParams& fp, bool causal, const MassParams* mp, int nfwd,
+pace_status_t launch_attention(FwdParams fp, bool causal, int max_seglen, const MassParams* mp,
                                int nmass, hipStream_t stream) {
-  if (causal)
-    hipLaunchKernelGGL((attn_fwd<D, true>), dim3(nfwd), dim3(kThreads), 0, stream, fp);
-  else
-    hipLaunchKernelGGL((attn_fwd<D, false>), dim3(nfwd), dim3(kThreads), 0, stream, fp);
+  if (causal) {
+    fp.nqt = (max_seglen + kBM - 1) / kBM;
+    hipLaunchKernelGGL((attn_fwd<D, true>), dim3(fp.nqt * fp.nseg * fp.Hq), dim3(kThreads), 0, stream, fp);
+  } else if (D == 80 && max_seglen >= kPPMinSeg) {
+    fp.nqt = (max_seglen + kPPBM - 1) / kPPBM;
+    hipLaunchKernelGGL((attn_fwd_pp<80>), dim3(fp.nqt * fp.nseg * fp.Hq), dim3(kPPThreads), 0, stream, fp);
+  } else {
+    fp.nqt = (max_seglen + kBM - 1) / kBM;
+    hipLaunchKernelGGL((attn_fwd<D, false>), dim3(fp.nqt * fp.nseg * fp.Hq), dim3(kThreads), 0, stream, fp);
+  }
   pace_status_t st = check_launch("attn_fwd");
   if (st != PACE_OK || mp == nullptr || nmass == 0) return st;
   if (causal)
@@ -690,10 +956,9 @@ pace_status_t pace_vit_attention(const uint16_t* q, const uint16_t* k, const uin
   mp.Ntot = N; mp.Hq = H; mp.Hkv = H; mp.group = 1;
   mp.nseg = nseg; mp.nkt = static_cast<int>(nkt);
   mp.scale_log2 = fp.scale_log2;
-  const int nfwd = static_cast<int>(nqt * nseg * H);
   const int nmass = mass ? static_cast<int>(nkt * nseg * H) : 0;
-  if (d == 80) return launch_attention<80>(fp, false, mass ? &mp : nullptr, nfwd, nmass, stream);
-  return launch_attention<128>(fp, false, mass ? &mp : nullptr, nfwd, nmass, stream);
+  if (d == 80) return launch_attention<80>(fp, false, max_seglen, mass ? &mp : nullptr, nmass, stream);
+  return launch_attention<128>(fp, false, max_seglen, mass ? &mp : nullptr, nmass, stream);
 }
 
 pace_status_t pace_vit_attention_mass(const uint16_t* q, const uint16_t* k, int N, int H, int d,
@@ -774,11 +1039,10 @@ pace_status_t pace_prefill_attention_with_mass(
   mp.Ntot = Ntot; mp.Hq = Hq; mp.Hkv = Hkv; mp.group = Hq / Hkv;
   mp.nseg = B; mp.nkt = static_cast<int>(nkt);
   mp.scale_log2 = fp.scale_log2;
-  const int nfwd = static_cast<int>(nqt * B * Hq);
   // the mass kernel also runs when no row queries (it then writes zeros)
   const int nmass = (want_mass && nkt > 0) ? static_cast<int>(nkt * B * Hq) : 0;
-  if (d == 80) return launch_attention<80>(fp, true, want_mass ? &mp : nullptr, nfwd, nmass, stream);
-  return launch_attention<128>(fp, true, want_mass ? &mp : nullptr, nfwd, nmass, stream);
+  if (d == 80) return launch_attention<80>(fp, true, max_seqlen, want_mass ? &mp : nullptr, nmass, stream);
+  return launch_attention<128>(fp, true, max_seqlen, want_mass ? &mp : nullptr, nmass, stream);
 }
 
 }  // extern "C"

@@ -73,6 +73,24 @@ def test_vit_large_logits():
     _check_vit(q, k, v, cu, d)
 
 
+def test_vit_long_segments_d80():
+    """Segments of 1024 rows or more take the two-group (ping-pong) forward kernel at head
+    dim 80; shorter segments of the same call go through it too."""
+    sizes = [1100, 37, 1536, 300, 1]
+    cu = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int32)
+    q, k, v = _vit_case(21, cu, 2, 80)
+    _check_vit(q, k, v, cu, 80)
+
+
+def test_vit_long_segment_large_logits_d80():
+    cu = [0, 1290]
+    N, H, d = 1290, 2, 80
+    q = wl.random_bf16(31, (N, H, d), 2.5)
+    k = wl.random_bf16(32, (N, H, d), 2.5)
+    v = wl.random_bf16(33, (N, H, d))
+    _check_vit(q, k, v, cu, d)
+
+
 def _run_prefill(p, d_override=None):
     from paper_2608_27206_amd import pace
     import torch
