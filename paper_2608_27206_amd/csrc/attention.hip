@@ -429,18 +429,24 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd(const FwdParams p) {
   }
 }
 
-// ---------------------------------------------------------------- forward, ping-pong
-// For long segments without a causal mask.  A workgroup = 8 waves x 32 query rows; wave w
-// runs on SIMD w % 4, so every SIMD holds one wave of each group (waves 0-3 and 4-7).
-// Each wave alternates two phases per 64-key tile t:
-//   A: online softmax of S^T(t) on the VALU (max, exponentials, row sums, bf16 packing);
-//   B: S^T(t+1) = K(t+1) Q^T and O^T += V(t)^T P^T(t) on the MFMA pipe.
-// The second group runs half a tile behind the first, and a workgroup barrier separates
-// consecutive half-steps, so on every SIMD one wave is in its VALU phase while the other
-// keeps the matrix core busy, instead of both contending for the same unit.  The waves
-// of the first group also issue the K/V DMA: K(t+2) and V(t+1) during their phase B of
-// tile t (the buffers' previous tiles were last read a half-step earlier), completed
-// before the barrier that ends their next phase A, i.e. before any wave reads them.
+// ---------------------------------------------------------------- forward, rotation
+// For long segments without a causal mask.  A workgroup = 12 waves x 32 query rows in three
+// groups of four; wave w runs on SIMD w % 4, so every SIMD holds one wave of each group.
+// Each wave processes a 64-key tile t in three phases, one per time slot:
+//   A1: row max (and rare rescale) of S^T(t), exponentials of its first 12 keys per lane;
+//   A2: the remaining 20 exponentials, row sums, bf16 packing of P^T(t), and the first
+//       half of S^T(t+1) = K(t+1) Q^T;
+//   B : the second half of S^T(t+1) and O^T += V(t)^T P^T(t).
+// Group g runs g slots behind group 0 and a workgroup barrier ends every slot, so in each
+// slot the three phases run side by side on every SIMD: a single wave cannot issue VALU
+// work fast enough to keep the VALU busy, two can, and MFMA work overlaps with both.
+// Group 0 also moves the data: during its phase A2 of tile t it transposes V(t) once into
+// the operand layout (transposing LDS reads are slow, so every wave then reads V^T with
+// plain 16-byte reads) and issues the DMA of K(t+2) and V(t+2), which it awaits before
+// the barrier that ends its phase A1 of tile t+1.  K and the row-major V run through three
+// LDS buffers, V^T through two; every buffer's previous tile is read for the last time
+// at least one slot before it is overwritten.
+
 // Workgroup barrier that also fences the instruction scheduler, so no computation
 // migrates between the two sides of a phase boundary.
 __device__ __forceinline__ void phase_sync() {
@@ -449,15 +455,18 @@ __device__ __forceinline__ void phase_sync() {
   __builtin_amdgcn_sched_barrier(0);
 }
 
-constexpr int kPPWaves = 8;
-constexpr int kPPThreads = 64 * kPPWaves;
-constexpr int kPPBM = 32 * kPPWaves;   // query rows per workgroup
+constexpr int kRotWaves = 12;
+constexpr int kRotThreads = 64 * kRotWaves;
+constexpr int kRotBM = 32 * kRotWaves;   // query rows per workgroup
+constexpr int kVtStride = kBN + 8;       // LDS row stride of a transposed V tile (elements)
+constexpr int kA1Vals = 12;              // exponentials per lane in phase A1 (of 32)
 
 template <int D>
-__global__ __launch_bounds__(kPPThreads, 2) void attn_fwd_pp(const FwdParams p) {
+__global__ __launch_bounds__(kRotThreads, 1) void attn_fwd_rot(const FwdParams p) {
   using C = FwdCfg<D>;
-  __shared__ __align__(16) uint16_t Ks[2][kBN * C::KS];
-  __shared__ __align__(16) uint16_t Vs[2][kBN * C::VS];
+  __shared__ __align__(16) uint16_t Ks[3][kBN * C::KS];
+  __shared__ __align__(16) uint16_t Vs[3][kBN * C::VS];          // V tiles as loaded (row-major)
+  __shared__ __align__(16) uint16_t Vt[2][C::DV * kVtStride];    // the same tiles as V^T operands
 
   const int lb = remap_block_id(blockIdx.x, gridDim.x);
   const int per_head = p.nseg * p.nqt;
@@ -467,7 +476,7 @@ __global__ __launch_bounds__(kPPThreads, 2) void attn_fwd_pp(const FwdParams p) 
   const int qt = rem - seg * p.nqt;
   const int s0 = p.cu[seg];
   const int L = p.cu[seg + 1] - s0;
-  const int q0 = qt * kPPBM;
+  const int q0 = qt * kRotBM;
   if (q0 >= L) return;   // the whole workgroup leaves together
   const int kvh = h / p.group;
   const int tid = threadIdx.x, w = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -506,14 +515,14 @@ __global__ __launch_bounds__(kPPThreads, 2) void attn_fwd_pp(const FwdParams p) 
   });
   const unsigned tile_bytes = static_cast<unsigned>(kBN * kvstride) * 2u;
   const unsigned ks_lds = lds_u32(&Ks[0][0]), vs_lds = lds_u32(&Vs[0][0]);
-  auto load_k = [&](int t, int buf) __attribute__((always_inline)) {
+  auto load_kv = [&](int t, int buf) __attribute__((always_inline)) {
     static_for<0, C::KPW>([&](auto I) __attribute__((always_inline)) {
-      if (wl + 4 * I < C::KINST) dma16(rk, ks_lds + (buf * kBN * C::KS + (wl + 4 * I) * 512) * 2, koff[I] + t * tile_bytes);
+      if (wl + 4 * I < C::KINST)
+        dma16(rk, ks_lds + (buf * kBN * C::KS + (wl + 4 * I) * 512) * 2, koff[I] + t * tile_bytes);
     });
-  };
-  auto load_v = [&](int t, int buf) __attribute__((always_inline)) {
     static_for<0, C::VPW>([&](auto I) __attribute__((always_inline)) {
-      if (wl + 4 * I < C::VINST) dma16(rv, vs_lds + (buf * kBN * C::VS + (wl + 4 * I) * 512) * 2, voff[I] + t * tile_bytes);
+      if (wl + 4 * I < C::VINST)
+        dma16(rv, vs_lds + (buf * kBN * C::VS + (wl + 4 * I) * 512) * 2, voff[I] + t * tile_bytes);
     });
   };
 
@@ -523,28 +532,43 @@ __global__ __launch_bounds__(kPPThreads, 2) void attn_fwd_pp(const FwdParams p) 
   const int tr_base = tr_row * C::VS + tr_col;
 
   f32x16 s[2];
-  auto qk = [&](int buf) __attribute__((always_inline)) {
+  // half st of S^T(tile in K buffer kb): keys 32 st .. 32 st + 31
+  auto qk_half = [&](int kb, int st) __attribute__((always_inline)) {
+    const uint16_t* kp = &Ks[kb][(st * 32 + c32) * C::KS + g * 8];
+    bf16x8 kf[C::KC];
 #pragma unroll
-    for (int st = 0; st < 2; ++st) {
-      const uint16_t* kp = &Ks[buf][(st * 32 + c32) * C::KS + g * 8];
-      bf16x8 kf[C::KC];
+    for (int c = 0; c < C::KC; ++c) kf[c] = *reinterpret_cast<const bf16x8*>(kp + c * 16);
+    s[st] = mfma(kf[0], qf[0], f32x16{});
 #pragma unroll
-      for (int c = 0; c < C::KC; ++c) kf[c] = *reinterpret_cast<const bf16x8*>(kp + c * 16);
-      s[st] = mfma(kf[0], qf[0], f32x16{});
-#pragma unroll
-      for (int c = 1; c < C::KC; ++c) s[st] = mfma(kf[c], qf[c], s[st]);
-    }
+    for (int c = 1; c < C::KC; ++c) s[st] = mfma(kf[c], qf[c], s[st]);
   };
 
   f32x16 oacc[C::NT];
 #pragma unroll
   for (int t2 = 0; t2 < C::NT; ++t2) oacc[t2] = f32x16{};
   float m_used = -INFINITY;
+  float m_off = 0.f;
   float l_part[4] = {0.f, 0.f, 0.f, 0.f};
-  bf16x8 pb[2][2];
+  uint32_t pw[2][2][4];   // packed P^T: [half][16-key chunk][bf16 pair]
 
-  // phase A: mask, max, (rare) rescale, exponentials, row sums, packing
-  auto softmax = [&](int kt) __attribute__((always_inline)) {
+  // exponentials, row sums and packing of values [R0, R1) of the 32 per lane (pairs)
+  auto exps = [&](auto R0, auto R1) __attribute__((always_inline)) {
+    static_for<decltype(R0)::value / 2, decltype(R1)::value / 2>([&](auto J) __attribute__((always_inline)) {
+      constexpr int r = 2 * decltype(J)::value, st = r >> 4, rr = r & 15;
+      const float e0 = fast_exp2(s[st][rr] * p.scale_log2 - m_off);
+      const float e1 = fast_exp2(s[st][rr + 1] * p.scale_log2 - m_off);
+      l_part[rr & 3] += e0;
+      l_part[(rr + 1) & 3] += e1;
+      pw[st][rr >> 3][(rr & 7) >> 1] = pack_bf16x2(e0, e1);
+      // pin the results to this phase: left alone, the compiler sinks them past the barrier
+      asm volatile("" : "+v"(pw[st][rr >> 3][(rr & 7) >> 1]));
+    });
+#pragma unroll
+    for (int i = 0; i < 4; ++i) asm volatile("" : "+v"(l_part[i]));
+  };
+
+  // phase A1: mask, max, (rare) rescale, first exponentials
+  auto phase_a1 = [&](int kt) __attribute__((always_inline)) {
     if (kt + kBN > L) {
 #pragma unroll
       for (int st = 0; st < 2; ++st)
@@ -576,83 +600,74 @@ __global__ __launch_bounds__(kPPThreads, 2) void attn_fwd_pp(const FwdParams p) 
 #pragma unroll
       for (int i = 0; i < 4; ++i) l_part[i] *= alpha;
     }
-    const float m_off = (m_used == -INFINITY) ? 0.f : m_used;
-#pragma unroll
-    for (int st = 0; st < 2; ++st) {
-      float pv[16];
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        pv[r] = fast_exp2(s[st][r] * p.scale_log2 - m_off);
-        l_part[r & 3] += pv[r];
-      }
-      pb[st][0] = pack_bf16x8(&pv[0]);
-      pb[st][1] = pack_bf16x8(&pv[8]);
-    }
-    // pin the row sums and the packed P here: left alone, the compiler sinks them past the
-    // barrier into the MFMA phase
-#pragma unroll
-    for (int i = 0; i < 4; ++i) asm volatile("" : "+v"(l_part[i]));
-#pragma unroll
-    for (int st = 0; st < 2; ++st)
-#pragma unroll
-      for (int hh = 0; hh < 2; ++hh) asm volatile("" : "+v"(pb[st][hh]));
+    m_off = (m_used == -INFINITY) ? 0.f : m_used;
+    exps(std::integral_constant<int, 0>{}, std::integral_constant<int, kA1Vals>{});
   };
 
-  auto pv = [&](int buf) __attribute__((always_inline)) {
+  // V^T fragment (st, hh, t2) of a tile: 16 bytes per lane, the A operand of O^T += V^T P^T.
+  // Group 0 moves each V tile once from its row-major copy into Vt (3 fragments per wave).
+  auto transpose_v = [&](int vb, int tb) __attribute__((always_inline)) {
+    static_for<0, 3>([&](auto I) __attribute__((always_inline)) {
+      const int f = wl * 3 + I;
+      const int st = f / 6, hh = (f / 3) & 1, t2 = f % 3;
+      const uint16_t* vp = &Vs[vb][(st * 32 + hh * 16) * C::VS + tr_base + t2 * 32];
+      const uint2 lo = lds_read_tr16(vp);
+      const uint2 hi = lds_read_tr16(vp + 8 * C::VS);
+      *reinterpret_cast<uint4*>(&Vt[tb][(t2 * 32 + c32) * kVtStride + st * 32 + hh * 16 + g * 8]) =
+          make_uint4(lo.x, lo.y, hi.x, hi.y);
+    });
+  };
+  auto pv = [&](int tb) __attribute__((always_inline)) {
 #pragma unroll
     for (int st = 0; st < 2; ++st)
 #pragma unroll
-      for (int hh = 0; hh < 2; ++hh) {
-        const uint16_t* vp = &Vs[buf][(st * 32 + hh * 16) * C::VS + tr_base];
+      for (int hh = 0; hh < 2; ++hh)
 #pragma unroll
         for (int t2 = 0; t2 < C::NT; ++t2) {
-          const uint2 lo = lds_read_tr16(vp + t2 * 32);
-          const uint2 hi = lds_read_tr16(vp + 8 * C::VS + t2 * 32);
-          oacc[t2] = mfma(as_bf16x8(make_uint4(lo.x, lo.y, hi.x, hi.y)), pb[st][hh], oacc[t2]);
+          const uint4 a = *reinterpret_cast<const uint4*>(
+              &Vt[tb][(t2 * 32 + c32) * kVtStride + st * 32 + hh * 16 + g * 8]);
+          const uint4 bp = make_uint4(pw[st][hh][0], pw[st][hh][1], pw[st][hh][2], pw[st][hh][3]);
+          oacc[t2] = mfma(as_bf16x8(a), as_bf16x8(bp), oacc[t2]);
         }
-      }
   };
 
   const int ntiles = (L + kBN - 1) / kBN;
   if (grp == 0) {
-    load_k(0, 0);
-    load_v(0, 0);
-    if (ntiles > 1) load_k(1, 1);
+    load_kv(0, 0);
+    if (ntiles > 1) load_kv(1, 1);
     wait_vmem();
   }
   phase_sync();
-  qk(0);
-  if (grp == 1) phase_sync();   // group 1 runs half a tile behind
-  int t = 0;
+  qk_half(0, 0);
+  qk_half(0, 1);
+  for (int i = 0; i < grp; ++i) phase_sync();   // group g runs g slots behind
+  int t = 0, kb = 0;                            // kb = t % 3
   for (; t + 1 < ntiles; ++t) {
-    const int b = t & 1;
-    softmax(t * kBN);
-    if (grp == 0) wait_vmem();   // the tiles issued during the previous phase B
+    const int kb1 = (kb == 2) ? 0 : kb + 1, kb2 = (kb1 == 2) ? 0 : kb1 + 1;
+    phase_a1(t * kBN);
+    if (grp == 0) wait_vmem();   // K(t+1) and V(t+1), issued during phase A2 of tile t-1
     phase_sync();
+    exps(std::integral_constant<int, kA1Vals>{}, std::integral_constant<int, 32>{});
     if (grp == 0) {
-      if (t + 2 < ntiles) load_k(t + 2, b);
-      load_v(t + 1, b ^ 1);
+      transpose_v(kb, t & 1);
+      if (t + 2 < ntiles) load_kv(t + 2, kb2);
     }
-    qk(b ^ 1);
-    pv(b);
-    __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
-    static_for<0, 2 * C::KC>([&](auto I) __attribute__((always_inline)) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x100, (I + 4 < 2 * C::KC) ? 1 : 2, 0);
-    });
-    static_for<0, 4 * C::NT>([&](auto) __attribute__((always_inline)) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
-    });
+    qk_half(kb1, 0);
     phase_sync();
+    qk_half(kb1, 1);
+    pv(t & 1);
+    phase_sync();
+    kb = kb1;
   }
   // last tile: nothing left to load or to multiply ahead
-  softmax(t * kBN);
-  if (grp == 0) wait_vmem();
+  phase_a1(t * kBN);
+  phase_sync();
+  exps(std::integral_constant<int, kA1Vals>{}, std::integral_constant<int, 32>{});
+  if (grp == 0) transpose_v(kb, t & 1);
   phase_sync();
   pv(t & 1);
   phase_sync();
-  if (grp == 0) phase_sync();
+  for (int i = grp; i < 2; ++i) phase_sync();   // equal barrier counts in every group
 
   const float lp = (l_part[0] + l_part[1]) + (l_part[2] + l_part[3]);
   const float l = lp + __shfl_xor(lp, 32, 64);
@@ -878,9 +893,9 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mass(const MassParams p) {
     }
 }
 
-// Segments at least this long (without a causal mask, head dim 80) take the ping-pong
+// Segments at least this long (without a causal mask, head dim 80) take the rotation
 // forward kernel; at head dim 128 its per-wave state would not fit in registers.
-constexpr int kPPMinSeg = 1024;
+constexpr int kRotMinSeg = 1024;
 
 template <int D>
 pace_status_t launch_attention(FwdParams fp, bool causal, int max_seglen, const MassParams* mp,
@@ -888,9 +903,9 @@ pace_status_t launch_attention(FwdParams fp, bool causal, int max_seglen, const 
   if (causal) {
     fp.nqt = (max_seglen + kBM - 1) / kBM;
     hipLaunchKernelGGL((attn_fwd<D, true>), dim3(fp.nqt * fp.nseg * fp.Hq), dim3(kThreads), 0, stream, fp);
-  } else if (D == 80 && max_seglen >= kPPMinSeg) {
-    fp.nqt = (max_seglen + kPPBM - 1) / kPPBM;
-    hipLaunchKernelGGL((attn_fwd_pp<80>), dim3(fp.nqt * fp.nseg * fp.Hq), dim3(kPPThreads), 0, stream, fp);
+  } else if (D == 80 && max_seglen >= kRotMinSeg) {
+    fp.nqt = (max_seglen + kRotBM - 1) / kRotBM;
+    hipLaunchKernelGGL((attn_fwd_rot<80>), dim3(fp.nqt * fp.nseg * fp.Hq), dim3(kRotThreads), 0, stream, fp);
   } else {
     fp.nqt = (max_seglen + kBM - 1) / kBM;
     hipLaunchKernelGGL((attn_fwd<D, false>), dim3(fp.nqt * fp.nseg * fp.Hq), dim3(kThreads), 0, stream, fp);
