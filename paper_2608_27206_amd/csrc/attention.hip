@@ -3,25 +3,29 @@
 // block) and the LLM's causal grouped-query prefill attention (S_llm from the text
 // query rows).  No attention matrix is ever stored.
 //
-// Two kernels, both on bf16 MFMA (v_mfma_f32_32x32x16_bf16, fp32 accumulation):
+// Three kernels, all on bf16 MFMA (v_mfma_f32_32x32x16_bf16, fp32 accumulation):
 //
 //  attn_fwd   query-stationary.  A workgroup = 4 waves x 32 query rows of one
-//             (segment, head).  K and V tiles of 64 keys are staged through LDS
-//             (double buffered, next tile prefetched into registers).  Each wave
-//             computes S^T = K Q^T so that every lane owns one query row (the MFMA
-//             accumulator column) and 16 keys of it: the row max and row sum are
-//             in-lane, plus one exchange between the two half-waves.  Online softmax
-//             in the log2 domain, P^T feeds O^T = V^T P^T straight from registers
-//             (no LDS round trip); V^T comes from transposing LDS reads of the
-//             row-major V tile.  For head dim 80 the PV product is padded to 96 rows.
-//             Writes O (bf16) and the natural-log LSE (fp32).
+//             (segment, head).  K and V tiles of 64 keys are staged through LDS by
+//             DMA (double buffered).  Each wave computes S^T = K Q^T so that every
+//             lane owns one query row (the MFMA accumulator column) and 16 keys of it:
+//             the row max and row sum are in-lane, plus one exchange between the two
+//             half-waves.  Online softmax in the log2 domain, P^T feeds O^T = V^T P^T
+//             straight from registers (no LDS round trip); V^T comes from transposing
+//             LDS reads of the row-major V tile.  For head dim 80 the PV product is
+//             padded to 96 rows.  Writes O (bf16) and the natural-log LSE (fp32).
+//             Causal segments, short segments and head dim 128.
+//
+//  attn_fwd_rot  the same computation for long segments at head dim 80, with 12 waves
+//             per workgroup in three groups that rotate through three phases (see the
+//             kernel), so that VALU and MFMA work of different waves overlap.
 //
 //  attn_mass  key-stationary.  A workgroup = 4 waves x 64 keys of one (segment,
 //             head); K stays in registers, query tiles of 32 rows stream through LDS
-//             (double buffered).  P = exp2(S * scale * log2 e - LSE * log2 e) is the
-//             exact normalised probability; each lane accumulates column sums for
-//             its 16 keys in fp32, and one butterfly over the half-wave finishes the
-//             sum.  Writes mass[h, key] once (no atomics, deterministic).
+//             (three buffers, up to three workgroups per CU).  P = exp2(S * scale * log2 e -
+//             LSE * log2 e) is the exact normalised probability; each lane accumulates
+//             column sums for its 16 keys in fp32, and one butterfly over the half-wave
+//             finishes the sum.  Writes mass[h, key] once (no atomics, deterministic).
 //
 // Operand layouts of v_mfma_f32_32x32x16_bf16 (wave64, lane l, g = l / 32):
 //   A (32 x 16): lane l holds A[l % 32][8g .. 8g+7]
@@ -724,13 +728,13 @@ struct MassCfg {
 
 // The mass kernel.  Every wave keeps 64 keys (two sets of 32) of K in registers as the A
 // operand and streams 32-row query tiles through LDS (DMA, two tiles ahead).  Per tile it
-// issues S^T(t+1) = K Q(t+1)^T on the MFMA pipe interleaved with the VALU work of tile t:
+// computes S^T(t) = K Q(t)^T on the MFMA pipe, then on the VALU
 // P = exp2(S * scale * log2 e - LSE * log2 e), the exact normalised probability, summed per
 // key in fp32 (each lane owns 16 keys of one query column).
 template <int D, bool CAUSAL>
-__global__ __launch_bounds__(kThreads, 2) void attn_mass(const MassParams p) {
+__global__ __launch_bounds__(kThreads, (D == 80 && !CAUSAL) ? 3 : 2) void attn_mass(const MassParams p) {
   using C = MassCfg<D>;
-  __shared__ __align__(16) uint16_t Qs[2][C::QBUF];
+  __shared__ __align__(16) uint16_t Qs[3][C::QBUF];
 
   const int lb = remap_block_id(blockIdx.x, gridDim.x);
   const int per_head = p.nseg * p.nkt;
@@ -826,49 +830,24 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mass(const MassParams p) {
       }
   };
 
+  // Three query-tile buffers: Q(t+2) is loaded while Q(t) is read, into the buffer of Q(t-1)
+  // that every wave left behind at this iteration's barrier.  No software pipelining within
+  // a wave: three workgroups per CU overlap one wave's MFMAs with the others' VALU work.
   const int ntiles = (ql + kMassQ - 1) / kMassQ;
   if (ntiles > 0) {
     load_q(0, 0);
     if (ntiles > 1) load_q(1, 1);
-    float l2_cur = load_lse2(0);
-    wait_vmem();
-    __syncthreads();
-    f32x16 sa[2], sb[2];
-    s_tile(0, sa);
-    auto iteration = [&](auto BUF, auto HAS_NEXT, int t, f32x16* s_cur, f32x16* s_next)
-        __attribute__((always_inline)) {
-      constexpr int buf = decltype(BUF)::value;
-      constexpr bool has_next = decltype(HAS_NEXT)::value;
-      // every wave is past its reads of Q(t) (also the prologue's) before Q(t+2) replaces it
+    int buf = 0;
+    for (int t = 0; t < ntiles; ++t) {
+      const float l2 = load_lse2(t);
       wait_vmem();
       __syncthreads();
-      if (t + 2 < ntiles) load_q(t + 2, buf);
-      float l2_next = INFINITY;
-      if constexpr (has_next) {
-        l2_next = load_lse2(t + 1);
-        s_tile(buf ^ 1, s_next);
-        accumulate(s_cur, l2_cur, t);
-        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
-        static_for<0, 2 * C::KC>([&](auto I) __attribute__((always_inline)) {
-          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-          __builtin_amdgcn_sched_group_barrier(0x002, 8, 0);
-          __builtin_amdgcn_sched_group_barrier(0x100, (I + 2 < C::KC) ? 1 : 0, 0);
-        });
-      } else {
-        accumulate(s_cur, l2_cur, t);
-      }
-      l2_cur = l2_next;
-    };
-    int t = 0;
-    for (; t + 2 < ntiles; t += 2) {
-      iteration(std::integral_constant<int, 0>{}, std::true_type{}, t, sa, sb);
-      iteration(std::integral_constant<int, 1>{}, std::true_type{}, t + 1, sb, sa);
-    }
-    if (t + 1 < ntiles) {
-      iteration(std::integral_constant<int, 0>{}, std::true_type{}, t, sa, sb);
-      iteration(std::integral_constant<int, 1>{}, std::false_type{}, t + 1, sb, sa);
-    } else {
-      iteration(std::integral_constant<int, 0>{}, std::false_type{}, t, sa, sb);
+      const int buf2 = (buf == 0) ? 2 : buf - 1;   // (t + 2) % 3
+      if (t + 2 < ntiles) load_q(t + 2, buf2);
+      f32x16 s[2];
+      s_tile(buf, s);
+      accumulate(s, l2, t);
+      buf = (buf == 2) ? 0 : buf + 1;
     }
   }
   // column sums over the 32 query lanes of each half-wave
