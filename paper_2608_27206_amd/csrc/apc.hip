@@ -9,6 +9,7 @@
 //                      rho_g = 1 - phi (Eq. 2), c_hat = c/||c||
 //   apc_patch_pass<1>  d_i = ||T_i - c_hat|| (the image is re-read, mostly from L2/MALL)
 //   apc_tail           radix select of the n_tail-th largest d, tail mean, rho_d, rho
+//                      (up to 49,152 distances held in registers, more re-read from memory)
 //
 // The per-patch feature is the patch's pixels mapped to x/127.5 - 1 (component order:
 // patch row, pixel column, channel).  The order does not change norms or cosines.
@@ -77,13 +78,11 @@ __device__ __forceinline__ int stage_tile(const DensityParams& p, int tile, uint
   return np;
 }
 
-// Feature component e (patch row, pixel column, channel) of patch j: x/127.5 - 1.
-__device__ __forceinline__ float feat(const uint8_t* pxb, const int* shift, int row_bytes_lds, int P,
-                                      int j, int e) {
-  const int r = e / (3 * P), cb = e - r * (3 * P);
-  return static_cast<float>(pxb[r * row_bytes_lds + shift[r] + j * 3 * P + cb]) * (1.0f / 127.5f) - 1.0f;
-}
+// Feature value of a staged byte: x/127.5 - 1.
+__device__ __forceinline__ float feat_of(uint8_t b) { return static_cast<float>(b) * (1.0f / 127.5f) - 1.0f; }
 
+// Feature component e = (patch row r, byte cb within the patch row: pixel column, channel)
+// of a tile's patches; patch j of the tile starts at byte j * 3P of each staged row.
 template <int PASS>
 __global__ __launch_bounds__(kApcThreads) void apc_patch_pass(const DensityParams p) {
   extern __shared__ uint32_t lds[];
@@ -99,16 +98,24 @@ __global__ __launch_bounds__(kApcThreads) void apc_patch_pass(const DensityParam
   __syncthreads();
   const uint8_t* pxb = reinterpret_cast<const uint8_t*>(px);
   const int rb = p.row_dwords * 4;
+  const int pb = 3 * p.P;                  // bytes of one patch row
   const int j = threadIdx.x >> 2, t = threadIdx.x & 3;
   float acc = 0.f;
   if (j < np) {
-    if (PASS == 0) {
-      for (int e = t; e < p.D; e += 4) { const float x = feat(pxb, shift, rb, p.P, j, e); acc += x * x; }
-    } else {
-      const float s = p.inv_norm[py * p.gw + px0 + j];
-      for (int e = t; e < p.D; e += 4) {
-        const float x = feat(pxb, shift, rb, p.P, j, e) * s - chat[e];
-        acc += x * x;
+    // the four threads of a patch take every fourth byte of each of its rows
+    float s = 0.f;
+    if (PASS == 1) s = p.inv_norm[py * p.gw + px0 + j];
+    for (int r = 0; r < p.P; ++r) {
+      const uint8_t* row = pxb + r * rb + shift[r] + j * pb;
+      const float* cr = chat + r * pb;
+      for (int cb = t; cb < pb; cb += 4) {
+        const float x = feat_of(row[cb]);
+        if (PASS == 0) {
+          acc += x * x;
+        } else {
+          const float y = x * s - cr[cb];
+          acc += y * y;
+        }
       }
     }
   }
@@ -123,9 +130,11 @@ __global__ __launch_bounds__(kApcThreads) void apc_patch_pass(const DensityParam
     __syncthreads();
     // tile partial of sum_i T_i, patches added in index order
     for (int e = threadIdx.x; e < p.D; e += kApcThreads) {
-      float s = 0.f;
-      for (int jj = 0; jj < np; ++jj) s += feat(pxb, shift, rb, p.P, jj, e) * inv[jj];
-      p.partial[static_cast<long long>(tile) * p.D + e] = s;
+      const int r = e / pb, cb = e - r * pb;
+      const uint8_t* col = pxb + r * rb + shift[r] + cb;
+      float sum = 0.f;
+      for (int jj = 0; jj < np; ++jj) sum += feat_of(col[jj * pb]) * inv[jj];
+      p.partial[static_cast<long long>(tile) * p.D + e] = sum;
     }
   } else {
     if (j < np && t == 0) p.d[py * p.gw + px0 + j] = sqrtf(acc);
@@ -170,17 +179,31 @@ __global__ __launch_bounds__(1024) void apc_finalize_c(const DensityParams p) {
   }
 }
 
+constexpr int kTailR = 48;   // distances per thread held in registers: up to 49,152 patches
+
 __global__ __launch_bounds__(1024) void apc_tail(const DensityParams p) {
   __shared__ uint32_t hist[256 + 8];
   __shared__ float red[16];
   int need = 0;
-  // d >= 0, so the raw bit patterns order like the values
-  const uint32_t T = block_radix_select(p.N, p.n_tail, [&](int i) { return __float_as_uint(p.d[i]); },
-                                        hist, &need);
+  uint32_t T;
   float s = 0.f;
-  for (int i = threadIdx.x; i < p.N; i += 1024) {
-    const float x = p.d[i];
-    if (__float_as_uint(x) > T) s += x;
+  // d >= 0, so the raw bit patterns order like the values
+  if (p.N <= 1024 * kTailR) {
+    // every distance read once: thread t owns patches t * kTailR + j
+    const int base = threadIdx.x * kTailR;
+    uint32_t key[kTailR];
+#pragma unroll
+    for (int j = 0; j < kTailR; ++j) key[j] = (base + j < p.N) ? __float_as_uint(p.d[base + j]) : 0u;
+    T = block_radix_select_regs<kTailR>(key, p.N, p.n_tail, hist, &need);
+#pragma unroll
+    for (int j = 0; j < kTailR; ++j)
+      if (base + j < p.N && key[j] > T) s += __uint_as_float(key[j]);
+  } else {
+    T = block_radix_select(p.N, p.n_tail, [&](int i) { return __float_as_uint(p.d[i]); }, hist, &need);
+    for (int i = threadIdx.x; i < p.N; i += 1024) {
+      const float x = p.d[i];
+      if (__float_as_uint(x) > T) s += x;
+    }
   }
   s = block_reduce<0>(s, red);
   if (threadIdx.x == 0) {

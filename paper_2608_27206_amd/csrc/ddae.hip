@@ -5,7 +5,8 @@
 //   ddae_token_maps   grid-wide: head sums (and 2x2 merge + permutation for S_vis)
 //                     -> raw S_vis, S_llm per LLM visual token (HBM-bound read of the masses)
 //   ddae_select       one workgroup per image: min/max, means, stds, weights, S_final,
-//                     radix top-K with lower-index ties, ascending compaction
+//                     radix top-K with lower-index ties, ascending compaction (images of
+//                     up to 16,384 tokens entirely in registers, larger ones from memory)
 //   gather_rows       grid-wide 16-byte row copy of the kept hidden states
 #include <math.h>
 
@@ -81,14 +82,154 @@ __global__ __launch_bounds__(256) void ddae_token_maps(const SelectParams p) {
 }
 
 constexpr int kSelThreads = 1024;
+constexpr int kSelR = 16;   // scores per thread kept in registers: images up to 16,384 tokens
+
+// Block-wide combinations of two or four per-thread values in one exchange (fixed wave
+// order, deterministic).  `red` holds 4 floats per wave.
+__device__ __forceinline__ void block_minmax2(float& a_min, float& a_max, float& b_min, float& b_max,
+                                              float* red) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  a_min = wave_min(a_min); a_max = wave_max(a_max);
+  b_min = wave_min(b_min); b_max = wave_max(b_max);
+  __syncthreads();
+  if (lane == 0) { red[4 * w] = a_min; red[4 * w + 1] = a_max; red[4 * w + 2] = b_min; red[4 * w + 3] = b_max; }
+  __syncthreads();
+  a_min = red[0]; a_max = red[1]; b_min = red[2]; b_max = red[3];
+  for (int i = 1; i < nw; ++i) {
+    a_min = fminf(a_min, red[4 * i]); a_max = fmaxf(a_max, red[4 * i + 1]);
+    b_min = fminf(b_min, red[4 * i + 2]); b_max = fmaxf(b_max, red[4 * i + 3]);
+  }
+}
+__device__ __forceinline__ void block_sum2(float& a, float& b, float* red) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  a = wave_sum(a);
+  b = wave_sum(b);
+  __syncthreads();
+  if (lane == 0) { red[4 * w] = a; red[4 * w + 1] = b; }
+  __syncthreads();
+  a = red[0]; b = red[1];
+  for (int i = 1; i < nw; ++i) { a += red[4 * i]; b += red[4 * i + 1]; }
+}
+
+// One image whose tokens fit in registers (n <= kSelThreads * kSelR): every map is read
+// once; thread t owns tokens t * kSelR + j.  Same steps and outputs as the general path.
+__device__ void select_in_registers(const SelectParams& p, int b, float* red, uint32_t* hist, int* cnt) {
+  const int n0 = p.cu_nv[b];
+  const int n = p.cu_nv[b + 1] - n0;
+  const int K = p.cu_keep[b + 1] - p.cu_keep[b];
+  const int out0 = p.cu_keep[b];
+  const int tid = threadIdx.x;
+  const int base = tid * kSelR;
+  float sc[kSelR];
+  if (p.scores_in == nullptr) {
+    const float* vr = p.vraw + n0;
+    const float* lr = p.lraw + n0;
+    float a[kSelR], c[kSelR];
+    float vmin = INFINITY, vmax = -INFINITY, lmin = INFINITY, lmax = -INFINITY;
+#pragma unroll
+    for (int j = 0; j < kSelR; ++j) {
+      const bool ok = base + j < n;
+      a[j] = ok ? vr[base + j] : 0.f;
+      c[j] = ok ? lr[base + j] : 0.f;
+      if (ok) {
+        vmin = fminf(vmin, a[j]); vmax = fmaxf(vmax, a[j]);
+        lmin = fminf(lmin, c[j]); lmax = fmaxf(lmax, c[j]);
+      }
+    }
+    block_minmax2(vmin, vmax, lmin, lmax, red);
+    const float vrange = vmax - vmin, lrange = lmax - lmin;
+    // min-max normalised maps (a constant map normalises to zeros)
+    float sum_v = 0.f, sum_l = 0.f;
+#pragma unroll
+    for (int j = 0; j < kSelR; ++j) {
+      a[j] = vrange > 0.f ? (a[j] - vmin) / vrange : 0.f;
+      c[j] = lrange > 0.f ? (c[j] - lmin) / lrange : 0.f;
+      if (base + j < n) { sum_v += a[j]; sum_l += c[j]; }
+    }
+    block_sum2(sum_v, sum_l, red);
+    const float mean_v = sum_v / n, mean_l = sum_l / n;
+    float var_v = 0.f, var_l = 0.f;
+#pragma unroll
+    for (int j = 0; j < kSelR; ++j) {
+      if (base + j < n) {
+        const float da = a[j] - mean_v, dc = c[j] - mean_l;
+        var_v += da * da; var_l += dc * dc;
+      }
+    }
+    block_sum2(var_v, var_l, red);
+    const float sig_v = sqrtf(var_v / n), sig_l = sqrtf(var_l / n);   // population std
+    float w_l, w_v;
+    if (p.mode == 0) {
+      w_l = 1.f / (1.f + expf((sig_v - sig_l) / p.tau));   // softmax over two entries
+      w_v = 1.f - w_l;
+    } else {
+      w_l = p.w_llm_fixed;
+      w_v = 1.f - p.w_llm_fixed;
+    }
+    if (tid == 0 && p.fuse) {
+      p.fuse[4 * b + 0] = sig_l; p.fuse[4 * b + 1] = sig_v;
+      p.fuse[4 * b + 2] = w_l;   p.fuse[4 * b + 3] = w_v;
+    }
+    float* S = p.scores + n0;
+#pragma unroll
+    for (int j = 0; j < kSelR; ++j) {
+      sc[j] = w_l * c[j] + w_v * a[j];
+      if (base + j < n) S[base + j] = sc[j];
+    }
+  } else {
+    const float* S = p.scores_in + n0;
+#pragma unroll
+    for (int j = 0; j < kSelR; ++j) sc[j] = (base + j < n) ? S[base + j] : 0.f;
+  }
+
+  if (K <= 0) return;
+  int32_t* idx = p.idx + out0;
+  if (K >= n) {
+    for (int i = tid; i < n; i += kSelThreads) idx[i] = n0 + i;
+    return;
+  }
+  uint32_t key[kSelR];
+#pragma unroll
+  for (int j = 0; j < kSelR; ++j) key[j] = float_key(sc[j]);
+  int need = 0;
+  const uint32_t T = block_radix_select_regs<kSelR>(key, n, K, hist, &need);
+  // ascending compaction: keep key > T, plus the `need` lowest-index keys == T
+  int n_eq = 0;
+#pragma unroll
+  for (int j = 0; j < kSelR; ++j) n_eq += (base + j < n && key[j] == T) ? 1 : 0;
+  int tot = 0;
+  int eq_rank = block_exclusive_sum(n_eq, cnt, &tot);
+  bool keep[kSelR];
+  int n_keep = 0;
+#pragma unroll
+  for (int j = 0; j < kSelR; ++j) {
+    const bool ok = base + j < n;
+    const bool eq = ok && key[j] == T;
+    keep[j] = (ok && key[j] > T) || (eq && eq_rank < need);
+    eq_rank += eq ? 1 : 0;
+    n_keep += keep[j] ? 1 : 0;
+  }
+  int pos = block_exclusive_sum(n_keep, cnt, &tot);
+#pragma unroll
+  for (int j = 0; j < kSelR; ++j) {
+    if (keep[j]) {
+      if (pos < K) idx[pos] = n0 + base + j;
+      ++pos;
+    }
+  }
+}
 
 __global__ __launch_bounds__(kSelThreads) void ddae_select(const SelectParams p) {
-  __shared__ float red[kSelThreads / 64];
+  __shared__ float red[4 * (kSelThreads / 64)];
   __shared__ uint32_t hist[256 + 8];
   __shared__ int cnt[kSelThreads / 64];
   const int b = blockIdx.x;
   const int n0 = p.cu_nv[b];
   const int n = p.cu_nv[b + 1] - n0;
+  if (n <= kSelThreads * kSelR) {
+    select_in_registers(p, b, red, hist, cnt);
+    return;
+  }
   const int K = p.cu_keep[b + 1] - p.cu_keep[b];
   const int out0 = p.cu_keep[b];
   float* S = p.scores + n0;

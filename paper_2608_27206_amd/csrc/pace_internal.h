@@ -173,6 +173,93 @@ __device__ uint32_t block_radix_select(int n, int k, Get get, uint32_t* hist, in
   return prefix;
 }
 
+// Radix selection as block_radix_select, over keys held in registers: thread t holds the
+// keys of elements t * R + j (j < R), element i valid when i < n.  Same result (the k-th
+// largest key T and *need, the number of elements equal to T in the top k); the keys are
+// read once instead of once per pass.  All threads must call.
+template <int R>
+__device__ uint32_t block_radix_select_regs(const uint32_t (&key)[R], int n, int k, uint32_t* hist,
+                                            int* need) {
+  uint32_t prefix = 0, mask = 0;
+  int remaining = k;
+  uint32_t* sel = hist + 256;  // [0]: digit, [1]: remaining
+  const int base = threadIdx.x * R;
+  for (int shift = 24; shift >= 0; shift -= 8) {
+    for (int i = threadIdx.x; i < 256; i += blockDim.x) hist[i] = 0;
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < R; ++j) {
+      const bool active = (base + j < n) && (key[j] & mask) == prefix;
+      const uint32_t bin = (key[j] >> shift) & 255u;
+      const unsigned long long act = __ballot(active);
+      if (act == 0ull) continue;
+      const int leader = __ffsll(static_cast<long long>(act)) - 1;
+      const uint32_t lead_bin = __shfl(bin, leader, 64);
+      const unsigned long long same = __ballot(active && bin == lead_bin);
+      if (same == act) {
+        if ((threadIdx.x & 63) == leader) atomicAdd(&hist[lead_bin], static_cast<uint32_t>(__popcll(act)));
+      } else if (active) {
+        atomicAdd(&hist[bin], 1u);
+      }
+    }
+    __syncthreads();
+    if (threadIdx.x < 64) {
+      const int lane = threadIdx.x;
+      const int dhi = 255 - 4 * lane;
+      const uint32_t c0 = hist[dhi], c1 = hist[dhi - 1], c2 = hist[dhi - 2], c3 = hist[dhi - 3];
+      const uint32_t tot = c0 + c1 + c2 + c3;
+      uint32_t incl = tot;
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        const uint32_t y = __shfl_up(incl, o, 64);
+        if (lane >= o) incl += y;
+      }
+      uint32_t before = incl - tot;
+      const uint32_t rem = static_cast<uint32_t>(remaining);
+      const uint32_t cs[4] = {c0, c1, c2, c3};
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        if (before < rem && before + cs[t] >= rem) {
+          sel[0] = static_cast<uint32_t>(dhi - t);
+          sel[1] = rem - before;
+        }
+        before += cs[t];
+      }
+    }
+    __syncthreads();
+    const uint32_t digit = sel[0];
+    remaining = static_cast<int>(sel[1]);
+    prefix |= digit << shift;
+    mask |= 255u << shift;
+    __syncthreads();
+  }
+  *need = remaining;
+  return prefix;
+}
+
+// Exclusive prefix sum of a per-thread count across the whole block (in thread order)
+// plus the block total.  `cnt` is LDS scratch of blockDim.x/64 ints.
+__device__ __forceinline__ int block_exclusive_sum(int v, int* cnt, int* total) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  int incl = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(incl, o, 64);
+    if (lane >= o) incl += y;
+  }
+  __syncthreads();
+  if (lane == 63) cnt[w] = incl;
+  __syncthreads();
+  int before = 0, tot = 0;
+  for (int i = 0; i < nw; ++i) {
+    const int c = cnt[i];
+    if (i < w) before += c;
+    tot += c;
+  }
+  *total = tot;
+  return before + incl - v;
+}
+
 // Exclusive prefix count of a per-thread flag across the whole block (in thread
 // order) plus the block total.  `cnt` is LDS scratch of blockDim.x/64 ints.
 __device__ __forceinline__ int block_exclusive_count(bool flag, int* cnt, int* total) {

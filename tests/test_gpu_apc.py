@@ -54,6 +54,23 @@ def test_density_odd_byte_count():
     np.testing.assert_allclose(host(rho), [ref["rho_g"], ref["rho_d"], ref["rho"], ref["phi"]], atol=1e-4)
 
 
+def test_density_more_patches_than_the_register_tail():
+    """51,072 patches: more than the tail kernel holds in registers (49,152), so the
+    distances are re-read from memory for the top-10% selection.  phi is checked through
+    the identity mean pairwise cosine = ||mean T||^2, which the CPU tests pin against the
+    double sum (the double sum itself would take minutes here)."""
+    img = wl.make_image(7, 14 * 228, 14 * 224)
+    say(f"apc density {img.shape} (tail from memory)")
+    rho, d = _density(img)
+    T = oapc.l2_normalise(oapc.patch_features(img, 14))
+    phi = float(np.sum(T.mean(axis=0) ** 2))
+    d_ref = oapc.detail_distances(T, oapc.background_direction(T))
+    rho_d = min(oapc.tail_mean(d_ref, 0.1) / oapc.GAMMA, 1.0)
+    np.testing.assert_allclose(d, d_ref, atol=1e-4)
+    np.testing.assert_allclose(rho, [1 - phi, rho_d, oapc.ALPHA * (1 - phi) + (1 - oapc.ALPHA) * rho_d, phi],
+                               atol=1e-4)
+
+
 def test_density_uniform_and_mirrored():
     u = np.full((56, 84, 3), 77, np.uint8)
     rho = _check_density(u)

@@ -27,7 +27,10 @@ def _topk_case(S32, K, hidden_bits):
 
 @pytest.mark.parametrize("n,K,levels", [(196, 20, None), (10549, 1055, None), (5000, 500, 3),
                                         (1000, 1, None), (1000, 999, None), (777, 77, 1),
-                                        (4096, 1024, 50)])
+                                        (4096, 1024, 50),
+                                        # largest image held in registers, and past it (the
+                                        # scores are then re-read from memory)
+                                        (16384, 1639, None), (16385, 1700, 4), (40000, 4000, None)])
 def test_topk_gather_bit_exact_on_oracle_scores(n, K, levels):
     say(f"topk n={n} K={K} levels={levels}")
     rs = np.random.default_rng(n * 7 + K)
@@ -87,6 +90,15 @@ def test_fuse_dynamic_with_merge_and_perm():
     llm = rs.gamma(0.3, size=(28, nv)).astype(np.float32)
     perm = rs.permutation(nv).astype(np.int32)
     _fuse_case(vis, llm, 4, perm, 0, 231, wl.random_bf16(7, (nv, 3584)))
+
+
+def test_fuse_dynamic_large_image_from_memory():
+    """An image too large for the register-resident path (more than 16,384 tokens)."""
+    rs = np.random.default_rng(12)
+    nv = 20000
+    vis = rs.gamma(0.5, size=(4, nv)).astype(np.float32)
+    llm = rs.gamma(0.3, size=(6, nv)).astype(np.float32)
+    _fuse_case(vis, llm, 1, None, 0, 2000)
 
 
 def test_fuse_fixed_tiny_config_end_to_end_inputs():
