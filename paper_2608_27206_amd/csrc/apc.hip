@@ -189,15 +189,17 @@ __global__ __launch_bounds__(1024) void apc_tail(const DensityParams p) {
   float s = 0.f;
   // d >= 0, so the raw bit patterns order like the values
   if (p.N <= 1024 * kTailR) {
-    // every distance read once: thread t owns patches t * kTailR + j
-    const int base = threadIdx.x * kTailR;
+    // every distance read once (coalesced): thread t owns patches j * 1024 + t
     uint32_t key[kTailR];
 #pragma unroll
-    for (int j = 0; j < kTailR; ++j) key[j] = (base + j < p.N) ? __float_as_uint(p.d[base + j]) : 0u;
-    T = block_radix_select_regs<kTailR>(key, p.N, p.n_tail, hist, &need);
+    for (int j = 0; j < kTailR; ++j) {
+      const int i = j * 1024 + static_cast<int>(threadIdx.x);
+      key[j] = (i < p.N) ? __float_as_uint(p.d[i]) : 0u;
+    }
+    T = block_radix_select_regs<kTailR, true>(key, p.N, p.n_tail, hist, &need);
 #pragma unroll
     for (int j = 0; j < kTailR; ++j)
-      if (base + j < p.N && key[j] > T) s += __uint_as_float(key[j]);
+      if (j * 1024 + static_cast<int>(threadIdx.x) < p.N && key[j] > T) s += __uint_as_float(key[j]);
   } else {
     T = block_radix_select(p.N, p.n_tail, [&](int i) { return __float_as_uint(p.d[i]); }, hist, &need);
     for (int i = threadIdx.x; i < p.N; i += 1024) {

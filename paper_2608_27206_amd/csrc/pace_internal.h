@@ -104,6 +104,21 @@ __device__ __forceinline__ uint32_t float_key(float f) {
   return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
 }
 
+// Adds the active lanes' bins to an LDS histogram.  Keys that share leading digits often
+// land in one bin for a whole wave: then a single atomic adds the wave's count.
+__device__ __forceinline__ void histogram_add(uint32_t* hist, bool active, uint32_t bin) {
+  const unsigned long long act = __ballot(active);
+  if (act == 0ull) return;
+  const int leader = __ffsll(static_cast<long long>(act)) - 1;
+  const uint32_t lead_bin = __builtin_amdgcn_readlane(bin, leader);
+  const unsigned long long same = __ballot(active && bin == lead_bin);
+  if (same == act) {
+    if ((threadIdx.x & 63) == leader) atomicAdd(&hist[lead_bin], static_cast<uint32_t>(__popcll(act)));
+  } else if (active) {
+    atomicAdd(&hist[bin], 1u);
+  }
+}
+
 // Radix selection of the k-th largest key (1 <= k <= n) among n keys produced by
 // `get(i)`, by one workgroup, most significant byte first.
 // Returns the key T of the k-th largest element and writes *need = how many
@@ -124,16 +139,7 @@ __device__ uint32_t block_radix_select(int n, int k, Get get, uint32_t* hist, in
       const bool active = (i < n) && (key & mask) == prefix;
       const uint32_t bin = (key >> shift) & 255u;
       // values with a common leading part land in one bin: one atomic per wave then
-      const unsigned long long act = __ballot(active);
-      if (act == 0ull) continue;
-      const int leader = __ffsll(static_cast<long long>(act)) - 1;
-      const uint32_t lead_bin = __shfl(bin, leader, 64);
-      const unsigned long long same = __ballot(active && bin == lead_bin);
-      if (same == act) {
-        if ((threadIdx.x & 63) == leader) atomicAdd(&hist[lead_bin], static_cast<uint32_t>(__popcll(act)));
-      } else if (active) {
-        atomicAdd(&hist[bin], 1u);
-      }
+      histogram_add(hist, active, bin);
     }
     __syncthreads();
     // Suffix sums over digits (high to low) by the first wave: lane j holds digits
@@ -174,33 +180,26 @@ __device__ uint32_t block_radix_select(int n, int k, Get get, uint32_t* hist, in
 }
 
 // Radix selection as block_radix_select, over keys held in registers: thread t holds the
-// keys of elements t * R + j (j < R), element i valid when i < n.  Same result (the k-th
-// largest key T and *need, the number of elements equal to T in the top k); the keys are
-// read once instead of once per pass.  All threads must call.
-template <int R>
+// keys of elements t * R + j (j < R) or, with STRIDED, of elements j * blockDim.x + t;
+// element i is valid when i < n.  Same result (the k-th largest key T and *need, the
+// number of elements equal to T in the top k); the keys are read once instead of once per
+// pass.  All threads must call.
+template <int R, bool STRIDED = false>
 __device__ uint32_t block_radix_select_regs(const uint32_t (&key)[R], int n, int k, uint32_t* hist,
                                             int* need) {
   uint32_t prefix = 0, mask = 0;
   int remaining = k;
   uint32_t* sel = hist + 256;  // [0]: digit, [1]: remaining
-  const int base = threadIdx.x * R;
+  const int base = STRIDED ? static_cast<int>(threadIdx.x) : static_cast<int>(threadIdx.x) * R;
+  const int step = STRIDED ? static_cast<int>(blockDim.x) : 1;
   for (int shift = 24; shift >= 0; shift -= 8) {
     for (int i = threadIdx.x; i < 256; i += blockDim.x) hist[i] = 0;
     __syncthreads();
 #pragma unroll
     for (int j = 0; j < R; ++j) {
-      const bool active = (base + j < n) && (key[j] & mask) == prefix;
+      const bool active = (base + j * step < n) && (key[j] & mask) == prefix;
       const uint32_t bin = (key[j] >> shift) & 255u;
-      const unsigned long long act = __ballot(active);
-      if (act == 0ull) continue;
-      const int leader = __ffsll(static_cast<long long>(act)) - 1;
-      const uint32_t lead_bin = __shfl(bin, leader, 64);
-      const unsigned long long same = __ballot(active && bin == lead_bin);
-      if (same == act) {
-        if ((threadIdx.x & 63) == leader) atomicAdd(&hist[lead_bin], static_cast<uint32_t>(__popcll(act)));
-      } else if (active) {
-        atomicAdd(&hist[bin], 1u);
-      }
+      histogram_add(hist, active, bin);
     }
     __syncthreads();
     if (threadIdx.x < 64) {
