@@ -27,7 +27,7 @@ if ROOT not in sys.path:
 
 PEAK_BF16_TFLOPS = 2516.6     # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
-TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "attn_fwd_vit_full_frame4k_traffic.md")
+TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "attn_fwd_rot_vit_full_frame4k_traffic.md")
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2608_27206_amd", "csrc", "attention.hip")
 
 
@@ -222,7 +222,7 @@ def main():
                    "windows": int(len(win_sizes)), "prefill_tokens": S, "visual_tokens": Nv,
                    "text_tokens": T, "llm_heads": f"{Hq}/{Hkv}", "llm_head_dim": int(dq),
                    "keep": K, "hidden": int(hidden.shape[1]), "resize_to": f"{oW}x{oH}"},
-        "roofline": {"kernel": "attn_fwd<80> (vision full attention, 42,196 patches x 16 heads)",
+        "roofline": {"kernel": "attn_fwd_rot<80> (vision full attention, 42,196 patches x 16 heads)",
                      "bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
                      "traffic": measured_traffic()},
