@@ -189,6 +189,7 @@ def main():
         for n in names:
             per[n] += ev[n][0].elapsed_time(ev[n][1])
     per = {n: v / a.steps for n, v in per.items()}
+    nxt = measure_next(pace, pq, pk, pv, p_cu, S, p_vis, p_cuv, Nv, T, idx, K, stream)
 
     # algorithmic work
     win_sizes = np.diff(vit.cu_windows).astype(np.float64)
@@ -244,10 +245,63 @@ def main():
             "density_gbs": round(bytes_apc / (per["apc"] * 1e-3) / 1e9, 1) if per["apc"] > 0 else None,
             "resize_gbs": round(bytes_resize / (per["resize"] * 1e-3) / 1e9, 1) if per["resize"] > 0 else None,
         },
+        "next": nxt,
     }
     if a.cpu_seconds > 0:
         result["cpu_baseline"] = cpu_baseline(vit, a.cpu_seconds)
     print(json.dumps(result), flush=True)
+
+
+def measure_next(pace, pq, pk, pv, p_cu, S, p_vis, p_cuv, Nv, T, idx, K, stream, reps=5):
+    """Outside the timed step: (1) the all-query ("Vision + Text") S_llm, i.e. the prefill's
+    mass pass with every row of the sequence querying; (2) the context after pruning: gather
+    Q/K/V of the K kept visual tokens and the T text tokens, then the same prefill kernel on
+    those T + K tokens (what the decoder layers after the extraction layer run)."""
+    import torch
+
+    dev = pq.device
+    Hq, dq = pq.shape[1], pq.shape[2]
+
+    def timed(fn):
+        fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps
+
+    zero = torch.zeros(1, dtype=torch.int32, device=dev)
+    all_rows = torch.tensor([S], dtype=torch.int32, device=dev)
+    o = torch.empty_like(pq)
+    lse = torch.empty((Hq, S), dtype=torch.float32, device=dev)
+    mass = torch.empty((Hq, Nv), dtype=torch.float32, device=dev)
+    t_all = timed(lambda: pace.prefill_attention_with_mass(pq, pk, pv, p_cu, S, p_vis, p_cuv, Nv, Nv, zero,
+                                                            all_rows, S, o=o, lse=lse, mass=mass))
+    keep = torch.cat([idx.long(), torch.arange(Nv, S, device=dev)]).to(torch.int32)
+    Sp = K + T
+    qc, kc, vc = (torch.empty((Sp,) + tuple(x.shape[1:]), dtype=x.dtype, device=dev) for x in (pq, pk, pv))
+    t_gather = timed(lambda: [pace.gather_rows(x, keep, out=y) for x, y in ((pq, qc), (pk, kc), (pv, vc))])
+    cu = torch.tensor([0, Sp], dtype=torch.int32, device=dev)
+    oc = torch.empty_like(qc)
+    lc = torch.empty((Hq, Sp), dtype=torch.float32, device=dev)
+    t_post = timed(lambda: pace.prefill_attention_with_mass(qc, kc, vc, cu, Sp, None, None, 0, 0, None, None, 0,
+                                                             want_mass=False, o=oc, lse=lc))
+    t_full = timed(lambda: pace.prefill_attention_with_mass(pq, pk, pv, p_cu, S, None, None, 0, 0, None, None,
+                                                             0, want_mass=False, o=o, lse=lse))
+    flop_full = 4.0 * dq * Hq * (S * (S + 1) / 2.0)
+    flop_post = 4.0 * dq * Hq * (Sp * (Sp + 1) / 2.0)
+    return {
+        "vision_text_mass": {"ms": round(t_all, 4), "query_rows": int(S),
+                             "note": "prefill forward + all-query mass (the paper's Vision+Text source)"},
+        "post_prune_prefill": {"tokens": int(Sp), "full_tokens": int(S), "gather_qkv_ms": round(t_gather, 4),
+                               "prefill_ms": round(t_post, 4), "full_prefill_ms": round(t_full, 4),
+                               "speedup": round(t_full / t_post, 2) if t_post > 0 else None,
+                               "tflops_post": round(flop_post / (t_post * 1e-3) / 1e12, 1) if t_post > 0 else None,
+                               "tflops_full": round(flop_full / (t_full * 1e-3) / 1e12, 1) if t_full > 0 else None},
+    }
 
 
 def cpu_baseline(vit, budget_s: float):

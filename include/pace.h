@@ -245,6 +245,19 @@ pace_status_t pace_topk_gather(const float* scores, int N, int K, const void* hi
                                size_t row_bytes, int32_t* idx_out, void* out, void* workspace,
                                size_t workspace_bytes, hipStream_t stream);
 
+/*
+ * The compaction step of pruning on its own (Section 3.3 and the prefill after pruning):
+ * dst[r] = src[idx[r]] bit for bit, for r < n_idx, rows of row_bytes bytes.  Gathers the
+ * other per-token tensors of the shortened context with the indices a selection produced
+ * (Q/K/V or KV-cache rows, position ids padded to 16 bytes, ...).
+ *   src  device [src_rows, row_bytes]; dst device [n_idx, row_bytes] (caller-owned, not
+ *        overlapping src); both 16-byte aligned; row_bytes a positive multiple of 16.
+ *   idx  int32 [n_idx] device; entries outside [0, src_rows) leave their dst row unwritten.
+ * n_idx = 0 is a no-op.  Asynchronous on `stream`.
+ */
+pace_status_t pace_gather_rows(const void* src, int src_rows, size_t row_bytes,
+                               const int32_t* idx, int n_idx, void* dst, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

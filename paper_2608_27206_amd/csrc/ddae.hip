@@ -463,4 +463,18 @@ pace_status_t pace_topk_gather(const float* scores, int N, int K, const void* hi
   return run_select(p, hidden, row_bytes, out, stream, false);
 }
 
+pace_status_t pace_gather_rows(const void* src, int src_rows, size_t row_bytes,
+                               const int32_t* idx, int n_idx, void* dst, hipStream_t stream) {
+  PACE_REQUIRE(n_idx >= 0 && src_rows >= 0, "pace_gather_rows: n_idx=%d src_rows=%d", n_idx, src_rows);
+  if (n_idx == 0) return PACE_OK;
+  PACE_REQUIRE(src && idx && dst, "pace_gather_rows: null device pointer");
+  PACE_REQUIRE(row_bytes > 0 && row_bytes % 16 == 0,
+               "pace_gather_rows: row_bytes=%zu must be a positive multiple of 16", row_bytes);
+  PACE_REQUIRE(row_bytes / 16 < (1u << 30), "pace_gather_rows: rows too long");
+  PACE_REQUIRE(aligned16(src) && aligned16(dst), "pace_gather_rows: src/dst not 16-byte aligned");
+  hipLaunchKernelGGL(gather_rows, dim3(n_idx), dim3(256), 0, stream, static_cast<const uint4*>(src), idx,
+                     static_cast<uint4*>(dst), n_idx, static_cast<int>(row_bytes / 16), src_rows);
+  return check_launch("gather_rows");
+}
+
 }  // extern "C"

@@ -55,6 +55,7 @@ _PROTOS = {
                                  c_void, c_size, c_void]),
     "pace_topk_gather": (c_int, [c_void, c_int, c_int, c_void, c_size, c_void, c_void, c_void, c_size,
                                  c_void]),
+    "pace_gather_rows": (c_int, [c_void, c_int, c_size, c_void, c_int, c_void, c_void]),
 }
 
 EXPORTED = tuple(_PROTOS.keys())
@@ -292,3 +293,14 @@ def topk_gather(scores: torch.Tensor, K: int, hidden: Optional[torch.Tensor] = N
     _check(lib().pace_topk_gather(_ptr(scores), N, int(K), _ptr(hidden), row_bytes, _ptr(idx),
                                   _ptr(out), None, 0, _stream()), "pace_topk_gather")
     return idx[:K], (out[:K] if out is not None else None)
+
+
+def gather_rows(src: torch.Tensor, idx: torch.Tensor, out: Optional[torch.Tensor] = None):
+    """out[r] = src[idx[r]] (whole rows, bit for bit); src [rows, ...] with 16-byte rows."""
+    n = idx.numel()
+    if out is None:
+        out = torch.empty((n,) + tuple(src.shape[1:]), dtype=src.dtype, device=src.device)
+    row_bytes = src[0].numel() * src.element_size() if src.shape[0] > 0 else 0
+    _check(lib().pace_gather_rows(_ptr(src), src.shape[0], row_bytes, _ptr(idx), n, _ptr(out),
+                                  _stream()), "pace_gather_rows")
+    return out
