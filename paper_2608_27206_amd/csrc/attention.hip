@@ -21,7 +21,7 @@
 //             kernel), so that VALU and MFMA work of different waves overlap.
 //
 //  attn_mass  key-stationary.  A workgroup = 4 waves x 64 keys of one (segment,
-//             head); K stays in registers, query tiles of 32 rows stream through LDS
+//             head); K stays in registers, query tiles of 64 rows stream through LDS
 //             (three buffers, up to three workgroups per CU).  P = exp2(S * scale * log2 e -
 //             LSE * log2 e) is the exact normalised probability; each lane accumulates
 //             column sums for its 16 keys in fp32, and one butterfly over the half-wave
@@ -714,7 +714,7 @@ struct MassParams {
 };
 
 constexpr int kMassKeys = 256;   // keys per workgroup (4 waves x 64)
-constexpr int kMassQ = 32;       // query rows per tile
+constexpr int kMassQ = 64;       // query rows per tile (two MFMA column blocks of 32)
 
 template <int D>
 struct MassCfg {
@@ -727,7 +727,7 @@ struct MassCfg {
 };
 
 // The mass kernel.  Every wave keeps 64 keys (two sets of 32) of K in registers as the A
-// operand and streams 32-row query tiles through LDS (DMA, two tiles ahead).  Per tile it
+// operand and streams 64-row query tiles through LDS (DMA, two tiles ahead).  Per tile it
 // computes S^T(t) = K Q(t)^T on the MFMA pipe, then on the VALU
 // P = exp2(S * scale * log2 e - LSE * log2 e), the exact normalised probability, summed per
 // key in fp32 (each lane owns 16 keys of one query column).
@@ -789,13 +789,14 @@ __global__ __launch_bounds__(kThreads, (D == 80 && !CAUSAL) ? 3 : 2) void attn_m
     });
   };
   // LSE of this lane's query row of tile t (log2 units); rows past the range get +inf -> P = 0
-  auto load_lse2 = [&](int t) __attribute__((always_inline)) {
-    const int r = t * kMassQ + c32;
+  auto load_lse2 = [&](int t, int u) __attribute__((always_inline)) {
+    const int r = t * kMassQ + u * 32 + c32;
     const float v = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rl, static_cast<unsigned>(r) * 4u, 0, 0));
     return (r < ql) ? v * kLog2e : INFINITY;
   };
-  auto s_tile = [&](int buf, f32x16* s) __attribute__((always_inline)) {
-    const uint16_t* qp = &Qs[buf][c32 * C::QS + g * 8];
+  // S^T of the 32-row half u of the query tile in buffer buf
+  auto s_tile = [&](int buf, int u, f32x16* s) __attribute__((always_inline)) {
+    const uint16_t* qp = &Qs[buf][(u * 32 + c32) * C::QS + g * 8];
     bf16x8 qb[C::KC];
 #pragma unroll
     for (int c = 0; c < C::KC; ++c) qb[c] = *reinterpret_cast<const bf16x8*>(qp + c * 16);
@@ -813,10 +814,10 @@ __global__ __launch_bounds__(kThreads, (D == 80 && !CAUSAL) ? 3 : 2) void attn_m
 #pragma unroll
     for (int r = 0; r < 16; ++r) macc[ks][r] = 0.f;
 
-  auto accumulate = [&](f32x16* s, float l2, int t) __attribute__((always_inline)) {
-    const int qrow = qs + t * kMassQ + c32;
-    // causal masking only where some key of the wave lies after some row of the tile
-    const bool need_mask = CAUSAL && (kw0 + 63 > qs + t * kMassQ);
+  auto accumulate = [&](f32x16* s, float l2, int t, int u) __attribute__((always_inline)) {
+    const int qrow = qs + t * kMassQ + u * 32 + c32;
+    // causal masking only where some key of the wave lies after some row of the half tile
+    const bool need_mask = CAUSAL && (kw0 + 63 > qs + t * kMassQ + u * 32);
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
@@ -839,14 +840,16 @@ __global__ __launch_bounds__(kThreads, (D == 80 && !CAUSAL) ? 3 : 2) void attn_m
     if (ntiles > 1) load_q(1, 1);
     int buf = 0;
     for (int t = 0; t < ntiles; ++t) {
-      const float l2 = load_lse2(t);
+      const float l2a = load_lse2(t, 0), l2b = load_lse2(t, 1);
       wait_vmem();
       __syncthreads();
       const int buf2 = (buf == 0) ? 2 : buf - 1;   // (t + 2) % 3
       if (t + 2 < ntiles) load_q(t + 2, buf2);
-      f32x16 s[2];
-      s_tile(buf, s);
-      accumulate(s, l2, t);
+      f32x16 sa[2], sb[2];
+      s_tile(buf, 0, sa);
+      s_tile(buf, 1, sb);
+      accumulate(sa, l2a, t, 0);
+      accumulate(sb, l2b, t, 1);
       buf = (buf == 2) ? 0 : buf + 1;
     }
   }
