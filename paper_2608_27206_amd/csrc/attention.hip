@@ -696,6 +696,174 @@ __global__ __launch_bounds__(kRotThreads, 1) void attn_fwd_rot(const FwdParams p
   }
 }
 
+// ---------------------------------------------------------------- windows, fused mass
+// Segments of at most 64 tokens (the 8x8-patch windows of the vision encoder), with the
+// mass in the same pass: every key of a window fits in one tile, so each row's max and sum
+// are final after one S^T tile and P = exp2(S * scale * log2 e - m) / l is exact in
+// registers.  A workgroup = 2 waves x 32 query rows = one (window, head): K and V are staged
+// once (DMA), each wave produces its rows' O and LSE, writes its exact P to LDS, and the
+// column sums over the window's query rows give the mass of each key.  Q, K and V are read
+// from HBM once, instead of twice for the forward + mass passes.
+constexpr int kWinWaves = 2;
+constexpr int kWinThreads = 64 * kWinWaves;
+constexpr int kWinMax = 32 * kWinWaves;   // longest segment (tokens)
+constexpr int kPbStride = kBN + 4;        // LDS row stride of the P tile (floats)
+
+template <int D>
+__global__ __launch_bounds__(kWinThreads) void attn_window(const FwdParams p, float* __restrict__ mass) {
+  using C = FwdCfg<D>;
+  constexpr int KPW = (C::KINST + kWinWaves - 1) / kWinWaves;
+  constexpr int VPW = (C::VINST + kWinWaves - 1) / kWinWaves;
+  // K and V tiles; after the PV product the same space holds P[query][key]
+  __shared__ __align__(16) uint16_t lds[kBN * (C::KS + C::VS)];
+  static_assert(kWinMax * kPbStride * 4 <= kBN * (C::KS + C::VS) * 2, "P tile does not fit");
+  uint16_t* Ks = lds;
+  uint16_t* Vs = lds + kBN * C::KS;
+  float* Pb = reinterpret_cast<float*>(lds);
+
+  const int lb = remap_block_id(blockIdx.x, gridDim.x);
+  const int h = lb / p.nseg;
+  const int seg = lb - h * p.nseg;
+  const int s0 = p.cu[seg];
+  const int L = p.cu[seg + 1] - s0;
+  if (L <= 0) return;   // the whole workgroup leaves together
+  const int kvh = h / p.group;
+  const int tid = threadIdx.x, w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int lane = tid & 63, g = lane >> 5, c32 = lane & 31;
+  const int qrow = w * 32 + c32;
+  const int qstride = p.Hq * D;
+  const int kvstride = p.Hkv * D;
+
+  const unsigned seg_bytes_q = static_cast<unsigned>((L - 1) * qstride + D) * 2u;
+  const unsigned seg_bytes_kv = static_cast<unsigned>((L - 1) * kvstride + D) * 2u;
+  const auto rq = make_rsrc(p.q + static_cast<long long>(s0) * qstride + h * D, seg_bytes_q);
+  const auto rk = make_dma_rsrc(p.k + static_cast<long long>(s0) * kvstride + kvh * D, seg_bytes_kv);
+  const auto rv = make_dma_rsrc(p.v + static_cast<long long>(s0) * kvstride + kvh * D, seg_bytes_kv);
+
+  // K and V of the window into LDS (same chunk order as attn_fwd; wave w issues w, w+2, ...)
+  const unsigned ks_lds = lds_u32(&Ks[0]), vs_lds = lds_u32(&Vs[0]);
+  static_for<0, KPW>([&](auto I) __attribute__((always_inline)) {
+    const int inst = w + kWinWaves * I;
+    const int c = inst * 64 + lane;
+    const int r = c / C::KROW, cc = c % C::KROW;
+    if (inst < C::KINST)
+      dma16(rk, ks_lds + inst * 1024, cc < D / 8 ? static_cast<unsigned>(r * kvstride + cc * 8) * 2u : kOutOfRange);
+  });
+  static_for<0, VPW>([&](auto I) __attribute__((always_inline)) {
+    const int inst = w + kWinWaves * I;
+    const int c = inst * 64 + lane;
+    const int r = c / C::VROW, cc = c % C::VROW;
+    if (inst < C::VINST)
+      dma16(rv, vs_lds + inst * 1024, cc < D / 8 ? static_cast<unsigned>(r * kvstride + cc * 8) * 2u : kOutOfRange);
+  });
+  bf16x8 qf[C::KC];
+  {
+    const unsigned qoff = static_cast<unsigned>(qrow * qstride + g * 8) * 2u;
+#pragma unroll
+    for (int c = 0; c < C::KC; ++c) qf[c] = as_bf16x8(buf_load16(rq, qoff + c * 32, 0));
+  }
+  wait_vmem();
+  __syncthreads();
+
+  f32x16 s[2];
+#pragma unroll
+  for (int st = 0; st < 2; ++st) {
+    const uint16_t* kp = &Ks[(st * 32 + c32) * C::KS + g * 8];
+    bf16x8 kf[C::KC];
+#pragma unroll
+    for (int c = 0; c < C::KC; ++c) kf[c] = *reinterpret_cast<const bf16x8*>(kp + c * 16);
+    s[st] = mfma(kf[0], qf[0], f32x16{});
+#pragma unroll
+    for (int c = 1; c < C::KC; ++c) s[st] = mfma(kf[c], qf[c], s[st]);
+  }
+  // keys past the window end, then the exact row max and sum
+  float mx = -INFINITY;
+#pragma unroll
+  for (int st = 0; st < 2; ++st)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int key = st * 32 + g * 4 + 8 * (r >> 2) + (r & 3);
+      if (key >= L) s[st][r] = -INFINITY;
+      mx = fmaxf(mx, s[st][r]);
+    }
+  mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * p.scale_log2;
+  float pv[2][16];
+  float lp = 0.f;
+#pragma unroll
+  for (int st = 0; st < 2; ++st)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      pv[st][r] = fast_exp2(s[st][r] * p.scale_log2 - mx);
+      lp += pv[st][r];
+    }
+  const float l = lp + __shfl_xor(lp, 32, 64);
+  const float inv_l = 1.f / l;
+
+  // O^T = V^T P^T with the unnormalised P (as attn_fwd), then O = O^T / l
+  f32x16 oacc[C::NT];
+#pragma unroll
+  for (int t2 = 0; t2 < C::NT; ++t2) oacc[t2] = f32x16{};
+  const int tgrp = lane >> 4, li = lane & 15;
+  const int tr_base = (4 * (tgrp >> 1) + (li >> 2)) * C::VS + 16 * (tgrp & 1) + 4 * (li & 3);
+#pragma unroll
+  for (int st = 0; st < 2; ++st)
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh) {
+      const bf16x8 pb = pack_bf16x8(&pv[st][hh * 8]);
+      const uint16_t* vp = &Vs[(st * 32 + hh * 16) * C::VS + tr_base];
+#pragma unroll
+      for (int t2 = 0; t2 < C::NT; ++t2) {
+        const uint2 lo = lds_read_tr16(vp + t2 * 32);
+        const uint2 hi = lds_read_tr16(vp + 8 * C::VS + t2 * 32);
+        oacc[t2] = mfma(as_bf16x8(make_uint4(lo.x, lo.y, hi.x, hi.y)), pb, oacc[t2]);
+      }
+    }
+
+  // exact P of this lane's row (zero for rows past the window) into LDS, 4 keys per store,
+  // once both waves are done with K and V
+  __syncthreads();
+  const float rowf = (qrow < L) ? inv_l : 0.f;
+#pragma unroll
+  for (int st = 0; st < 2; ++st)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      float4 v4 = make_float4(pv[st][4 * j] * rowf, pv[st][4 * j + 1] * rowf, pv[st][4 * j + 2] * rowf,
+                              pv[st][4 * j + 3] * rowf);
+      *reinterpret_cast<float4*>(&Pb[qrow * kPbStride + st * 32 + 8 * j + 4 * g]) = v4;
+    }
+
+  if (qrow < L) {
+    uint16_t* op = p.o + static_cast<long long>(s0 + qrow) * qstride + h * D;
+#pragma unroll
+    for (int t2 = 0; t2 < C::NT; ++t2) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int dv = t2 * 32 + g * 4 + 8 * j;
+        if (dv < D) {
+          uint2 pk;
+          pk.x = pack_bf16x2(oacc[t2][4 * j + 0] * inv_l, oacc[t2][4 * j + 1] * inv_l);
+          pk.y = pack_bf16x2(oacc[t2][4 * j + 2] * inv_l, oacc[t2][4 * j + 3] * inv_l);
+          *reinterpret_cast<uint2*>(op + dv) = pk;
+        }
+      }
+    }
+    if (g == 0 && p.lse)
+      p.lse[static_cast<long long>(h) * p.Ntot + s0 + qrow] = (mx + __builtin_amdgcn_logf(l)) * kLn2;
+  }
+  __syncthreads();
+  // mass of key k: its column of P summed over the window's rows (rows past the window
+  // hold zeros); thread k sums rows 0-31 and thread k + 64 rows 32-63, in a fixed order
+  const int key = tid & 63, half = tid >> 6;
+  float m4[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int q = 0; q < 32; ++q) m4[q & 3] += Pb[(half * 32 + q) * kPbStride + key];
+  const float part = (m4[0] + m4[1]) + (m4[2] + m4[3]);
+  __syncthreads();
+  if (half == 1) Pb[key] = part;
+  __syncthreads();
+  if (half == 0 && key < L) mass[static_cast<long long>(h) * p.Ntot + s0 + key] = part + Pb[key];
+}
+
 // ---------------------------------------------------------------- mass
 struct MassParams {
   const uint16_t* q;
@@ -882,6 +1050,11 @@ constexpr int kRotMinSeg = 1024;
 template <int D>
 pace_status_t launch_attention(FwdParams fp, bool causal, int max_seglen, const MassParams* mp,
                                int nmass, hipStream_t stream) {
+  if (!causal && mp != nullptr && nmass > 0 && max_seglen <= kWinMax && mp->mass_stride == fp.Ntot &&
+      mp->key_len == nullptr && mp->q_start == nullptr && mp->q_len == nullptr && mp->mass_off == nullptr) {
+    hipLaunchKernelGGL((attn_window<D>), dim3(fp.nseg * fp.Hq), dim3(kWinThreads), 0, stream, fp, mp->mass);
+    return check_launch("attn_window");
+  }
   if (causal) {
     fp.nqt = (max_seglen + kBM - 1) / kBM;
     hipLaunchKernelGGL((attn_fwd<D, true>), dim3(fp.nqt * fp.nseg * fp.Hq), dim3(kThreads), 0, stream, fp);

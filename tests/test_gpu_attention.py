@@ -63,6 +63,26 @@ def test_vit_windows_and_ragged_segments(d):
     _check_vit(q, k, v, cu, d)
 
 
+@pytest.mark.parametrize("d", [80, 128])
+def test_vit_short_windows_single_pass(d):
+    """Segments of at most 64 tokens with mass requested take the single-pass window kernel
+    (O, LSE and mass together)."""
+    sizes = [64, 16, 4, 1, 33, 64, 50, 63, 64]
+    cu = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int32)
+    q, k, v = _vit_case(7, cu, 3, d)
+    _check_vit(q, k, v, cu, d)
+
+
+def test_vit_short_windows_large_logits():
+    sizes = [64, 7, 64, 40]
+    cu = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int32)
+    N = int(cu[-1])
+    q = wl.random_bf16(41, (N, 2, 80), 2.5)
+    k = wl.random_bf16(42, (N, 2, 80), 2.5)
+    v = wl.random_bf16(43, (N, 2, 80))
+    _check_vit(q, k, v, cu, 80)
+
+
 def test_vit_large_logits():
     """Logits with std ~ 6 stress the online max and the rescaling."""
     cu = [0, 700]
