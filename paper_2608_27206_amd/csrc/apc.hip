@@ -250,9 +250,10 @@ __device__ __forceinline__ float keys_cubic(float x) {
 // Taps of output coordinate o along an axis of n inputs resized to m outputs: input i's
 // distance to o's sample point in kernel units is ((2i+1) m - (2o+1) n) / (2 max(n, m)); its
 // numerator is an exact integer, so every weight carries a single rounding.  Writes
-// `slots` normalised weights for inputs lo .. lo+slots-1 (zero past the image or the
-// support) and returns lo.
-__device__ __forceinline__ int make_taps(int o, int n, int m, int slots, float* w) {
+// normalised weights for inputs lo .. lo+count-1, the span from the first to the last
+// nonzero weight within `slots` candidates (zero past the image or the support), and
+// returns lo (count in *count).
+__device__ __forceinline__ int make_taps(int o, int n, int m, int slots, float* w, int* count) {
   const float centre = (static_cast<float>(o) + 0.5f) * static_cast<float>(n) / static_cast<float>(m);
   const float support = 2.f * fmaxf(1.f, static_cast<float>(n) / static_cast<float>(m));
   const int lo = max(static_cast<int>(floorf(centre - support - 0.5f)) - 1, 0);
@@ -265,27 +266,36 @@ __device__ __forceinline__ int make_taps(int o, int n, int m, int slots, float* 
     sum += wt;
   }
   const float inv = 1.f / sum;
-  for (int j = 0; j < slots; ++j) w[j] *= inv;
-  return lo;
+  int j0 = 0, j1 = slots - 1;
+  while (j0 < j1 && w[j0] == 0.f) ++j0;
+  while (j1 > j0 && w[j1] == 0.f) --j1;
+  for (int j = j0; j <= j1; ++j) w[j - j0] = w[j] * inv;
+  for (int j = j1 - j0 + 1; j < slots; ++j) w[j] = 0.f;
+  *count = j1 - j0 + 1;
+  return lo + j0;
 }
 
 __global__ __launch_bounds__(kRsThreads) void apc_resize(const ResizeParams p) {
   extern __shared__ float sm[];
   float* wx = sm + p.o_wx;                      // [tx][ntx]
   float* wy = sm + p.o_wy;                      // [ty][nty]
-  int* lox = reinterpret_cast<int*>(sm + p.o_lox);
-  int* loy = reinterpret_cast<int*>(sm + p.o_loy);
+  int* lox = reinterpret_cast<int*>(sm + p.o_lox);   // [tx]: first tap, then [tx]: tap count
+  int* loy = reinterpret_cast<int*>(sm + p.o_loy);   // [ty]: first tap, then [ty]: tap count
+  int* cnx = lox + p.tx;
+  int* cny = loy + p.ty;
   uint32_t* pix = reinterpret_cast<uint32_t*>(sm + p.o_pix);   // [rows_cap][row_dwords]
   float* hb = sm + p.o_h;                       // [rows_cap][tx][3]
   __shared__ int shift[256];                    // byte shift of each staged row
   const int ox0 = blockIdx.x * p.tx, oy0 = blockIdx.y * p.ty;
   const int ncols = min(p.tx, p.oW - ox0), nrows = min(p.ty, p.oH - oy0);
-  for (int c = threadIdx.x; c < ncols; c += kRsThreads) lox[c] = make_taps(ox0 + c, p.W, p.oW, p.ntx, wx + c * p.ntx);
-  for (int r = threadIdx.x; r < nrows; r += kRsThreads) loy[r] = make_taps(oy0 + r, p.H, p.oH, p.nty, wy + r * p.nty);
+  for (int c = threadIdx.x; c < ncols; c += kRsThreads)
+    lox[c] = make_taps(ox0 + c, p.W, p.oW, p.ntx, wx + c * p.ntx, &cnx[c]);
+  for (int r = threadIdx.x; r < nrows; r += kRsThreads)
+    loy[r] = make_taps(oy0 + r, p.H, p.oH, p.nty, wy + r * p.nty, &cny[r]);
   __syncthreads();
   const int xlo = lox[0], ylo = loy[0];
-  const int xin = min(lox[ncols - 1] + p.ntx, p.W) - xlo;      // staged input columns
-  const int yin = min(loy[nrows - 1] + p.nty, p.H) - ylo;      // staged input rows
+  const int xin = lox[ncols - 1] + cnx[ncols - 1] - xlo;      // staged input columns
+  const int yin = loy[nrows - 1] + cny[nrows - 1] - ylo;      // staged input rows
   // stage input rows ylo .. ylo+yin-1, bytes [xlo*3, (xlo+xin)*3) of each, as aligned dwords
   const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint8_t*>(p.src), (short)0, p.H * p.W * 3, 0x00020000);
@@ -304,7 +314,7 @@ __global__ __launch_bounds__(kRsThreads) void apc_resize(const ResizeParams p) {
     const int r = e / ncols, c = e - r * ncols;
     const uint8_t* row = pixb + r * p.row_dwords * 4 + shift[r] + (lox[c] - xlo) * 3;
     const float* w = wx + c * p.ntx;
-    const int nt = min(p.ntx, p.W - lox[c]);
+    const int nt = cnx[c];
     float a0 = 0.f, a1 = 0.f, a2 = 0.f;
     for (int j = 0; j < nt; ++j) {
       const float wt = w[j];
@@ -322,7 +332,7 @@ __global__ __launch_bounds__(kRsThreads) void apc_resize(const ResizeParams p) {
     const int c = rem / 3, ch = rem - c * 3;
     const float* w = wy + r * p.nty;
     const int base = loy[r] - ylo;
-    const int nt = min(p.nty, p.H - loy[r]);
+    const int nt = cny[r];
     float acc = 0.f;
     for (int j = 0; j < nt; ++j) acc += w[j] * hb[((base + j) * p.tx + c) * 3 + ch];
     const float v = floorf(acc + 0.5f);
@@ -432,8 +442,8 @@ pace_status_t pace_apc_downsample(const uint8_t* src, int H, int W, uint8_t* dst
     int off = 0;
     q.o_wx = off; off += t_x * q.ntx;
     q.o_wy = off; off += t_y * q.nty;
-    q.o_lox = off; off += t_x;
-    q.o_loy = off; off += t_y;
+    q.o_lox = off; off += 2 * t_x;
+    q.o_loy = off; off += 2 * t_y;
     q.o_pix = off; off += q.rows_cap * q.row_dwords;
     q.o_h = off; off += q.rows_cap * t_x * 3;
     return static_cast<size_t>(off) * 4;
