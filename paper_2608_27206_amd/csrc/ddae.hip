@@ -1,19 +1,34 @@
 // DDAE (Section 3.3, "Extract"): token maps, min-max normalisation, std confidences,
 // softmax(sigma / tau) fusion, top-K ranking and the gather of the kept rows.
 //
-// Three launches per call:
-//   ddae_token_maps   grid-wide: head sums (and 2x2 merge + permutation for S_vis)
-//                     -> raw S_vis, S_llm per LLM visual token (HBM-bound read of the masses)
-//   ddae_select       one workgroup per image: min/max, means, stds, weights, S_final,
-//                     radix top-K with lower-index ties, ascending compaction (images of
-//                     up to 16,384 tokens entirely in registers, larger ones from memory)
-//   gather_rows       grid-wide 16-byte row copy of the kept hidden states
+// Two launches per call when every image has at most 16,384 tokens:
+//   ddae_token_maps      grid-wide, 64 tokens per workgroup, workgroups never straddle
+//                        two images: head sums (and 2x2 merge + permutation for S_vis) ->
+//                        raw S_vis, S_llm per LLM visual token (HBM-bound read of the
+//                        masses), plus each workgroup's min, max and float64 sum and sum
+//                        of squares of both maps
+//   ddae_select_gather   a few workgroups per image, each running the same deterministic
+//                        selection: the image's statistics from those partials (min-max
+//                        ranges; the std of a min-max map is std(raw) / range), the fused
+//                        scores in registers, radix top-K with lower-index ties, the
+//                        ascending positions of the kept tokens; then each workgroup copies
+//                        its own slice of the kept hidden rows.  Repeating the selection
+//                        in every workgroup costs L2 reads, not latency, and saves a
+//                        launch between the selection and the gather.
+// Larger images take the general path: ddae_select (one workgroup per image, maps read
+// from memory in every pass) and gather_rows.
 #include <math.h>
 
 #include "pace_internal.h"
 
 namespace pace {
 namespace {
+
+// Statistics of one map workgroup's tokens.
+struct MapPartial {
+  float vmin, vmax, lmin, lmax;
+  double sv, sv2, sl, sl2;
+};
 
 struct SelectParams {
   const float* vis_mass;
@@ -32,31 +47,60 @@ struct SelectParams {
   float tau, w_llm_fixed;
   int cu_nv[PACE_MAX_SEGMENTS + 1];
   int cu_keep[PACE_MAX_SEGMENTS + 1];
+  // map workgroups of image b: [cu_mwg[b], cu_mwg[b+1]); select workgroups likewise
+  int cu_mwg[PACE_MAX_SEGMENTS + 1];
+  int cu_swg[PACE_MAX_SEGMENTS + 1];
+  MapPartial* part;
+  const uint4* hidden;
+  uint4* out;
+  int words_per_row;
+  int rows_per_wg;
 };
 
-__device__ __forceinline__ int find_segment(const SelectParams& p, int i) {
-  int lo = 0, hi = p.B - 1;
+// Largest b < B with cu[b] <= x (cu nondecreasing, cu[0] = 0 <= x).
+__device__ __forceinline__ int find_image(const int* cu, int B, int x) {
+  int lo = 0, hi = B - 1;
   while (lo < hi) {
     const int mid = (lo + hi + 1) >> 1;
-    if (p.cu_nv[mid] <= i) lo = mid; else hi = mid - 1;
+    if (cu[mid] <= x) lo = mid; else hi = mid - 1;
   }
   return lo;
 }
 
+struct MinOp { __device__ float operator()(float a, float b) const { return fminf(a, b); } };
+struct MaxOp { __device__ float operator()(float a, float b) const { return fmaxf(a, b); } };
+struct AddOpD { __device__ double operator()(double a, double b) const { return a + b; } };
+
+constexpr int kMapTokens = 64;   // tokens per map workgroup
+
 // Four lanes per token, each summing every fourth head; combined by shuffles in a fixed
-// order (deterministic).
+// order (deterministic).  Then the workgroup's partial statistics, reduced in a fixed order.
 __global__ __launch_bounds__(256) void ddae_token_maps(const SelectParams p) {
-  const int i = blockIdx.x * 64 + (threadIdx.x >> 2);
+  __shared__ float red_f[4][4];
+  __shared__ double red_d[4][4];
+  const int b = __builtin_amdgcn_readfirstlane(find_image(p.cu_mwg, p.B, blockIdx.x));
+  const int n0 = p.cu_nv[b];
+  const int n = p.cu_nv[b + 1] - n0;
+  const int li = (blockIdx.x - p.cu_mwg[b]) * kMapTokens + (threadIdx.x >> 2);
   const int part = threadIdx.x & 3;
-  const bool valid = i < p.nv_total;
-  const int ii = valid ? i : 0;
-  const int b = find_segment(p, ii);
-  const int base = p.cu_nv[b];
-  const int local = p.vis_perm ? p.vis_perm[ii] : (ii - base);
-  const long long patch0 = static_cast<long long>(base + local) * p.merge;
+  const bool valid = li < n;
+  const int ii = n0 + (valid ? li : 0);
+  // The LLM masses do not depend on the permutation: their loads go out first, then the
+  // permutation entry, then the vision masses it points at.
+  float lm[8];
+#pragma unroll
+  for (int u = 0; u < 8; ++u) {
+    const int h = part + 4 * u;
+    lm[u] = (valid && h < p.Hl) ? p.llm_mass[static_cast<long long>(h) * p.nv_total + ii] : 0.f;
+  }
+  float l = 0.f;
+  for (int h = part + 32; h < p.Hl; h += 4) l += valid ? p.llm_mass[static_cast<long long>(h) * p.nv_total + ii] : 0.f;
+  const int local = p.vis_perm ? p.vis_perm[ii] : (ii - n0);
+  const long long patch0 = static_cast<long long>(n0 + local) * p.merge;
   float v = 0.f;
   if (valid) {
     if (p.merge == 4) {
+#pragma unroll 4
       for (int h = part; h < p.Hv; h += 4) {
         const float4 m = *reinterpret_cast<const float4*>(p.vis_mass + h * p.vis_stride + patch0);
         v += (m.x + m.y) + (m.z + m.w);
@@ -68,16 +112,42 @@ __global__ __launch_bounds__(256) void ddae_token_maps(const SelectParams p) {
       }
     }
   }
-  float l = 0.f;
-  if (valid)
-    for (int h = part; h < p.Hl; h += 4) l += p.llm_mass[static_cast<long long>(h) * p.nv_total + ii];
+#pragma unroll
+  for (int u = 0; u < 8; ++u) l += lm[u];
   v += __shfl_xor(v, 1, 64);
   l += __shfl_xor(l, 1, 64);
   v += __shfl_xor(v, 2, 64);
   l += __shfl_xor(l, 2, 64);
   if (valid && part == 0) {
-    p.vraw[i] = v;
-    p.lraw[i] = l;
+    p.vraw[ii] = v;
+    p.lraw[ii] = l;
+  }
+  if (p.part == nullptr) return;
+  // one lane per token contributes (the four lanes of a token hold the same sums)
+  const bool own = valid && part == 0;
+  const float vmin = wave_reduce_dpp(own ? v : INFINITY, MinOp{});
+  const float vmax = wave_reduce_dpp(own ? v : -INFINITY, MaxOp{});
+  const float lmin = wave_reduce_dpp(own ? l : INFINITY, MinOp{});
+  const float lmax = wave_reduce_dpp(own ? l : -INFINITY, MaxOp{});
+  const double dv = own ? static_cast<double>(v) : 0.0, dl = own ? static_cast<double>(l) : 0.0;
+  const double sv = wave_reduce_dpp(dv, AddOpD{}), sv2 = wave_reduce_dpp(dv * dv, AddOpD{});
+  const double sl = wave_reduce_dpp(dl, AddOpD{}), sl2 = wave_reduce_dpp(dl * dl, AddOpD{});
+  const int w = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) {
+    red_f[w][0] = vmin; red_f[w][1] = vmax; red_f[w][2] = lmin; red_f[w][3] = lmax;
+    red_d[w][0] = sv; red_d[w][1] = sv2; red_d[w][2] = sl; red_d[w][3] = sl2;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    MapPartial r;
+    r.vmin = red_f[0][0]; r.vmax = red_f[0][1]; r.lmin = red_f[0][2]; r.lmax = red_f[0][3];
+    r.sv = red_d[0][0]; r.sv2 = red_d[0][1]; r.sl = red_d[0][2]; r.sl2 = red_d[0][3];
+    for (int q = 1; q < 4; ++q) {
+      r.vmin = fminf(r.vmin, red_f[q][0]); r.vmax = fmaxf(r.vmax, red_f[q][1]);
+      r.lmin = fminf(r.lmin, red_f[q][2]); r.lmax = fmaxf(r.lmax, red_f[q][3]);
+      r.sv += red_d[q][0]; r.sv2 += red_d[q][1]; r.sl += red_d[q][2]; r.sl2 += red_d[q][3];
+    }
+    p.part[blockIdx.x] = r;
   }
 }
 
@@ -309,6 +379,295 @@ __global__ __launch_bounds__(kSelThreads) void ddae_select(const SelectParams p)
   }
 }
 
+// Exclusive prefix sum of per-thread counts over the block in thread order, and the block
+// total.  `wt` is LDS scratch of one word per wave that no other live step uses.  One barrier.
+__device__ __forceinline__ uint32_t block_excl_scan(uint32_t v, uint32_t* wt, uint32_t* total) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  const uint32_t incl = wave_incl_scan(v);
+  if (lane == 63) wt[w] = incl;
+  __syncthreads();
+  uint32_t before = 0, tot = 0;
+  for (int i0 = 0; i0 < nw; i0 += 4) {   // wt is 16-byte aligned and nw a multiple of 4
+    const uint4 c4 = *reinterpret_cast<const uint4*>(&wt[i0]);
+    const uint32_t c[4] = {c4.x, c4.y, c4.z, c4.w};
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      before += (i0 + q < w) ? c[q] : 0u;
+      tot += c[q];
+    }
+  }
+  *total = tot;
+  return before + incl - v;
+}
+
+constexpr int kValBins = 4096;   // value-range bins of the first selection pass
+constexpr int kCandMax = 256;    // candidates ranked by direct comparison
+constexpr int kSPad = 20;        // LDS floats per thread's row of kSelR scores (16 + 4 pad)
+
+// Selection + gather for images of up to kSelThreads * kSelR tokens.  Image b owns select
+// workgroups [cu_swg[b], cu_swg[b+1]); each one computes the image's whole selection (same
+// inputs, same fixed-order arithmetic, hence the same result in every workgroup), the first
+// one writes idx, the scores and the fusion statistics, and workgroup g of the image copies
+// kept rows [g * rows_per_wg, (g + 1) * rows_per_wg).
+//
+// The selection finds the threshold pair (T_key, T_idx): token i is kept iff
+// key_i > T_key, or key_i == T_key and i <= T_idx (ties to the lower index).  Steps:
+//   1. scores from coalesced loads, transposed through LDS so that thread t holds tokens
+//      16 t .. 16 t + 15 (the compaction then needs a single block scan);
+//   2. a histogram of floor((S - S_min) * 4096 / (S_max - S_min)), a map that is monotone
+//      in S also in fp32, and the bin b* that holds the K-th largest score;
+//   3. the tokens of bin b* (few, unless scores tie heavily): ranked by direct comparison
+//      when at most kCandMax, else by a radix select on their keys;
+//   4. ascending compaction: position = number of kept tokens before it.
+__global__ __launch_bounds__(kSelThreads) void ddae_select_gather(const SelectParams p) {
+  __shared__ __align__(16) uint32_t hist[kValBins];
+  __shared__ uint32_t rhist[4 * 256];
+  __shared__ __align__(16) float sbuf[kSelThreads * kSPad];
+  __shared__ uint32_t cand_key[kCandMax];
+  __shared__ int cand_idx[kCandMax];
+  __shared__ __align__(16) uint32_t wt[4][kSelThreads / 64];
+  __shared__ float wmm[2][kSelThreads / 64];
+  __shared__ uint32_t misc[8];   // 0: b*, 1: need, 2: candidates, 3: T_key, 4: T_idx, 5-6: radix
+  __shared__ float st_f[4];
+  __shared__ double st_d[4];
+  extern __shared__ int rows_lds[];   // rows_per_wg source rows of this workgroup's slice
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int b = __builtin_amdgcn_readfirstlane(find_image(p.cu_swg, p.B, blockIdx.x));
+  const int gi = blockIdx.x - p.cu_swg[b];
+  const bool lead = gi == 0;
+  const int n0 = p.cu_nv[b];
+  const int n = p.cu_nv[b + 1] - n0;
+  const int K = p.cu_keep[b + 1] - p.cu_keep[b];
+  const int out0 = p.cu_keep[b];
+  const int r0 = gi * p.rows_per_wg;
+  const int r1 = min(K, r0 + p.rows_per_wg);
+  for (int i = tid; i < kValBins; i += kSelThreads) hist[i] = 0u;
+  rhist[tid] = 0u;
+  if (tid < 8) misc[tid] = 0u;
+  for (int i = tid; i < p.rows_per_wg; i += kSelThreads) rows_lds[i] = -1;
+
+  // ---- 1. scores (strided, coalesced) -> LDS -> blocked registers.  Every load is issued
+  // first (they do not depend on the statistics), and the lead's score stores come last:
+  // loads and stores share one in-order completion counter, so a store issued between
+  // loads would make each later wait cover it too.
+  const bool maps = p.scores_in == nullptr;
+  // an image of up to 16,384 tokens has at most 256 map workgroups: wave 0 loads four
+  // partials per lane, before anything else
+  static_assert(kSelThreads * kSelR <= 4 * 64 * kMapTokens, "partials per lane");
+  MapPartial r[4];
+  const int q0 = p.cu_mwg[b] + lane, q1 = p.cu_mwg[b + 1];
+  if (maps && w == 0) {
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      if (q0 + 64 * u < q1) r[u] = p.part[q0 + 64 * u];
+  }
+  float a[kSelR], c[kSelR];
+  {
+    const auto ra = range_rsrc(maps ? p.vraw + n0 : p.scores_in + n0, static_cast<unsigned>(n) * 4u);
+#pragma unroll
+    for (int j = 0; j < kSelR; ++j) a[j] = rload_f32(ra, static_cast<unsigned>(j * kSelThreads + tid) * 4u);
+    if (maps) {
+      const auto rl = range_rsrc(p.lraw + n0, static_cast<unsigned>(n) * 4u);
+#pragma unroll
+      for (int j = 0; j < kSelR; ++j) c[j] = rload_f32(rl, static_cast<unsigned>(j * kSelThreads + tid) * 4u);
+    }
+  }
+  float smin_l = INFINITY, smax_l = -INFINITY;
+  if (maps) {
+    // image statistics from the map workgroups' partials, in a fixed order (wave 0)
+    if (w == 0) {
+      float vmin = INFINITY, vmax = -INFINITY, lmin = INFINITY, lmax = -INFINITY;
+      double sv = 0.0, sv2 = 0.0, sl = 0.0, sl2 = 0.0;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        if (q0 + 64 * u < q1) {
+          vmin = fminf(vmin, r[u].vmin); vmax = fmaxf(vmax, r[u].vmax);
+          lmin = fminf(lmin, r[u].lmin); lmax = fmaxf(lmax, r[u].lmax);
+          sv += r[u].sv; sv2 += r[u].sv2; sl += r[u].sl; sl2 += r[u].sl2;
+        }
+      }
+      vmin = wave_reduce_dpp(vmin, MinOp{}); vmax = wave_reduce_dpp(vmax, MaxOp{});
+      lmin = wave_reduce_dpp(lmin, MinOp{}); lmax = wave_reduce_dpp(lmax, MaxOp{});
+      sv = wave_reduce_dpp(sv, AddOpD{}); sv2 = wave_reduce_dpp(sv2, AddOpD{});
+      sl = wave_reduce_dpp(sl, AddOpD{}); sl2 = wave_reduce_dpp(sl2, AddOpD{});
+      if (lane == 0) {
+        // population std of a min-max normalised map = std(raw map) / range (0 for a
+        // constant map, which normalises to zeros)
+        const double dn = static_cast<double>(n);
+        const double vr = static_cast<double>(vmax) - vmin, lr = static_cast<double>(lmax) - lmin;
+        const double mv = sv / dn, ml = sl / dn;
+        const double sig_v = vr > 0.0 ? sqrt(fmax(sv2 / dn - mv * mv, 0.0)) / vr : 0.0;
+        const double sig_l = lr > 0.0 ? sqrt(fmax(sl2 / dn - ml * ml, 0.0)) / lr : 0.0;
+        double w_l;
+        if (p.mode == 0)   // softmax of two entries
+          w_l = 1.0 / (1.0 + static_cast<double>(expf(static_cast<float>((sig_v - sig_l) / p.tau))));
+        else
+          w_l = p.w_llm_fixed;
+        st_f[0] = vmin; st_f[1] = vmax; st_f[2] = lmin; st_f[3] = lmax;
+        st_d[0] = sig_l; st_d[1] = sig_v; st_d[2] = w_l; st_d[3] = 1.0 - w_l;
+      }
+    }
+    __syncthreads();
+    // (x - min) * (1 / range): a multiply per token instead of an IEEE division
+    const float vmin = st_f[0], vrange = st_f[1] - st_f[0];
+    const float lmin = st_f[2], lrange = st_f[3] - st_f[2];
+    const float vinv = vrange > 0.f ? 1.f / vrange : 0.f, linv = lrange > 0.f ? 1.f / lrange : 0.f;
+    const float w_l = static_cast<float>(st_d[2]), w_v = static_cast<float>(st_d[3]);
+#pragma unroll
+    for (int j = 0; j < kSelR; ++j) a[j] = w_l * ((c[j] - lmin) * linv) + w_v * ((a[j] - vmin) * vinv);
+  }
+#pragma unroll
+  for (int j = 0; j < kSelR; ++j) {
+    const int i = j * kSelThreads + tid;
+    if (i < n) {
+      sbuf[i + (i >> 4) * (kSPad - kSelR)] = a[j];
+      smin_l = fminf(smin_l, a[j]);
+      smax_l = fmaxf(smax_l, a[j]);
+    }
+  }
+  if (maps && lead) {
+    const auto rs = range_rsrc(p.scores + n0, static_cast<unsigned>(n) * 4u);
+#pragma unroll
+    for (int j = 0; j < kSelR; ++j)
+      rstore_b32(rs, static_cast<unsigned>(j * kSelThreads + tid) * 4u, __float_as_uint(a[j]));
+    if (tid == 0 && p.fuse) {
+      p.fuse[4 * b + 0] = static_cast<float>(st_d[0]); p.fuse[4 * b + 1] = static_cast<float>(st_d[1]);
+      p.fuse[4 * b + 2] = static_cast<float>(st_d[2]); p.fuse[4 * b + 3] = static_cast<float>(st_d[3]);
+    }
+  }
+  smin_l = wave_reduce_dpp(smin_l, MinOp{});
+  smax_l = wave_reduce_dpp(smax_l, MaxOp{});
+  if (lane == 0) { wmm[0][w] = smin_l; wmm[1][w] = smax_l; }
+  __syncthreads();
+  if (K <= 0) return;
+
+  const int base = tid * kSelR;
+  uint32_t key[kSelR];
+  {
+    float s[kSelR];
+#pragma unroll
+    for (int q = 0; q < kSelR / 4; ++q) {
+      const float4 f = *reinterpret_cast<const float4*>(&sbuf[tid * kSPad + 4 * q]);
+      s[4 * q] = f.x; s[4 * q + 1] = f.y; s[4 * q + 2] = f.z; s[4 * q + 3] = f.w;
+    }
+#pragma unroll
+    for (int j = 0; j < kSelR; ++j) key[j] = float_key(s[j]);
+    if (K < n) {
+      float smin = wmm[0][0], smax = wmm[1][0];
+      for (int i = 1; i < kSelThreads / 64; ++i) { smin = fminf(smin, wmm[0][i]); smax = fmaxf(smax, wmm[1][i]); }
+      // ---- 2. value-range histogram (monotone non-decreasing bin map, clamped)
+      const float cscale = smax > smin ? fminf(static_cast<float>(kValBins) / (smax - smin), 3.4e38f) : 0.f;
+#pragma unroll
+      for (int j = 0; j < kSelR; ++j) {
+        const int bin = static_cast<int>(fminf((s[j] - smin) * cscale, static_cast<float>(kValBins - 1)));
+        // equal scores would all hit one LDS address: the all-equal case is counted below
+        if (base + j < n && cscale > 0.f) atomicAdd(&hist[bin], 1u);
+        key[j] = (base + j < n) ? key[j] : 0u;
+        s[j] = static_cast<float>(bin);   // keep the bin (exact small integer)
+      }
+      if (cscale == 0.f && tid == 0) hist[0] = static_cast<uint32_t>(n);
+      __syncthreads();
+      // thread t covers bins 4095 - 4t down to 4092 - 4t (descending)
+      const int bhi = kValBins - 1 - 4 * tid;
+      const uint4 h4 = *reinterpret_cast<const uint4*>(&hist[bhi - 3]);
+      const uint32_t c0 = h4.w, c1 = h4.z, c2 = h4.y, c3 = h4.x;
+      uint32_t tot_all = 0;
+      uint32_t before = block_excl_scan(c0 + c1 + c2 + c3, wt[0], &tot_all);
+      const uint32_t cs[4] = {c0, c1, c2, c3};
+      const uint32_t uK = static_cast<uint32_t>(K);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        if (before < uK && before + cs[q] >= uK) { misc[0] = bhi - q; misc[1] = uK - before; }
+        before += cs[q];
+      }
+      __syncthreads();
+      const int bstar = static_cast<int>(misc[0]);
+      const int need = static_cast<int>(misc[1]);   // 1 <= need <= count of bin b*
+      // ---- 3. candidates: the tokens of bin b*
+#pragma unroll
+      for (int j = 0; j < kSelR; ++j) {
+        if (base + j < n && static_cast<int>(s[j]) == bstar) {
+          const uint32_t slot = atomicAdd(&misc[2], 1u);
+          if (slot < static_cast<uint32_t>(kCandMax)) { cand_key[slot] = key[j]; cand_idx[slot] = base + j; }
+        }
+      }
+      __syncthreads();
+      const uint32_t ncand = misc[2];
+      if (ncand <= static_cast<uint32_t>(kCandMax)) {
+        // rank = candidates ahead in (key descending, index ascending) order
+        if (tid < static_cast<int>(ncand)) {
+          const uint32_t kt = cand_key[tid];
+          const int it = cand_idx[tid];
+          int rank = 0;
+#pragma unroll 8
+          for (uint32_t u = 0; u < ncand; ++u) {
+            const uint32_t ku = cand_key[u];
+            rank += (ku > kt || (ku == kt && cand_idx[u] < it)) ? 1 : 0;
+          }
+          if (rank == need - 1) { misc[3] = kt; misc[4] = static_cast<uint32_t>(it); }
+        }
+      } else {
+        // many ties in one bin: radix select over the candidates' keys, then the lowest
+        // indices among the keys equal to the threshold
+        uint32_t ck[kSelR];
+#pragma unroll
+        for (int j = 0; j < kSelR; ++j) ck[j] = (base + j < n && static_cast<int>(s[j]) == bstar) ? key[j] : 0u;
+        // keys of non-candidates are 0: below every candidate key only if no candidate key
+        // is 0, so they are excluded by count instead (the radix ranks the top `need` of
+        // all ck, and every candidate outranks a non-candidate unless keys are 0, i.e. -NaN)
+        int need_eq = 0;
+        const uint32_t T = radix_select_prezeroed<kSelR, false>(ck, n, need, rhist, &misc[5], &need_eq);
+        uint32_t eqc = 0;
+#pragma unroll
+        for (int j = 0; j < kSelR; ++j) eqc += (base + j < n && static_cast<int>(s[j]) == bstar && key[j] == T) ? 1u : 0u;
+        uint32_t tot_eq = 0;
+        uint32_t eq_before = block_excl_scan(eqc, wt[1], &tot_eq);
+#pragma unroll
+        for (int j = 0; j < kSelR; ++j) {
+          if (base + j < n && static_cast<int>(s[j]) == bstar && key[j] == T) {
+            if (eq_before == static_cast<uint32_t>(need_eq - 1)) { misc[3] = T; misc[4] = static_cast<uint32_t>(base + j); }
+            ++eq_before;
+          }
+        }
+      }
+      __syncthreads();
+      const uint32_t tkey = misc[3];
+      const int tidx = static_cast<int>(misc[4]);
+#pragma unroll
+      for (int j = 0; j < kSelR; ++j)
+        key[j] = (base + j < n && (key[j] > tkey || (key[j] == tkey && base + j <= tidx))) ? 1u : 0u;
+    } else {
+#pragma unroll
+      for (int j = 0; j < kSelR; ++j) key[j] = (base + j < n) ? 1u : 0u;   // every token kept
+    }
+  }
+  // ---- 4. ascending compaction (key[j] is now the keep flag)
+  uint32_t kc = 0;
+#pragma unroll
+  for (int j = 0; j < kSelR; ++j) kc += key[j];
+  uint32_t tot_keep = 0;
+  uint32_t pos = block_excl_scan(kc, wt[2], &tot_keep);
+  const auto ri = range_rsrc(p.idx + out0, lead ? static_cast<unsigned>(K) * 4u : 0u);
+#pragma unroll
+  for (int j = 0; j < kSelR; ++j) {
+    const int src = n0 + base + j;
+    rstore_b32(ri, key[j] ? pos * 4u : kNoStore, static_cast<uint32_t>(src));
+    if (key[j] && static_cast<int>(pos) >= r0 && static_cast<int>(pos) < r1) rows_lds[pos - r0] = src;
+    pos += key[j];
+  }
+  if (p.hidden == nullptr || r1 <= r0) return;
+  __syncthreads();
+  // this workgroup's slice of the gather, in 16-byte words
+  const int W = p.words_per_row;
+  const int total = (r1 - r0) * W;
+  for (int e = tid; e < total; e += kSelThreads) {
+    const int r = e / W, wd = e - r * W;
+    const int src = rows_lds[r];
+    if (src >= 0 && src < p.nv_total)   // always true; never read outside hidden
+      p.out[static_cast<long long>(out0 + r0 + r) * W + wd] = p.hidden[static_cast<long long>(src) * W + wd];
+  }
+}
+
 // out[r, :] = hidden[idx[r], :] in 16-byte words; one row per block-row.
 __global__ __launch_bounds__(256) void gather_rows(const uint4* __restrict__ hidden,
                                                    const int32_t* __restrict__ idx,
@@ -327,16 +686,45 @@ __global__ __launch_bounds__(256) void gather_rows(const uint4* __restrict__ hid
 
 pace_status_t run_select(SelectParams& p, const void* hidden, size_t row_bytes, void* out,
                          hipStream_t stream, bool need_maps) {
+  int nmax = 0;
+  p.cu_mwg[0] = 0;
+  for (int b = 0; b < p.B; ++b) {
+    const int n = p.cu_nv[b + 1] - p.cu_nv[b];
+    nmax = n > nmax ? n : nmax;
+    p.cu_mwg[b + 1] = p.cu_mwg[b] + (n + kMapTokens - 1) / kMapTokens;
+  }
+  const bool fused = nmax <= kSelThreads * kSelR;
+  if (!fused) p.part = nullptr;
   if (need_maps && p.nv_total > 0) {
-    const int blocks = (p.nv_total + 63) / 64;
-    hipLaunchKernelGGL(ddae_token_maps, dim3(blocks), dim3(256), 0, stream, p);
+    hipLaunchKernelGGL(ddae_token_maps, dim3(p.cu_mwg[p.B]), dim3(256), 0, stream, p);
     pace_status_t st = check_launch("ddae_token_maps");
     if (st != PACE_OK) return st;
+  }
+  const int ktot = p.cu_keep[p.B];
+  if (fused) {
+    // rows per select workgroup: at least 4, and about one workgroup per CU (256) for the
+    // gather (a select workgroup's ~105 KB of LDS leaves room for one per CU)
+    int R = 1;
+    if (hidden != nullptr && ktot > 0) {
+      R = (ktot + 255) / 256;
+      R = R < 4 ? 4 : (R > 4096 ? 4096 : R);
+    }
+    p.hidden = static_cast<const uint4*>(hidden);
+    p.out = static_cast<uint4*>(out);
+    p.words_per_row = static_cast<int>(row_bytes / 16);
+    p.rows_per_wg = R;
+    p.cu_swg[0] = 0;
+    for (int b = 0; b < p.B; ++b) {
+      const int K = p.cu_keep[b + 1] - p.cu_keep[b];
+      p.cu_swg[b + 1] = p.cu_swg[b] + ((hidden != nullptr && K > 0) ? (K + R - 1) / R : 1);
+    }
+    hipLaunchKernelGGL(ddae_select_gather, dim3(p.cu_swg[p.B]), dim3(kSelThreads),
+                       static_cast<size_t>(R) * sizeof(int), stream, p);
+    return check_launch("ddae_select_gather");
   }
   hipLaunchKernelGGL(ddae_select, dim3(p.B), dim3(kSelThreads), 0, stream, p);
   pace_status_t st = check_launch("ddae_select");
   if (st != PACE_OK) return st;
-  const int ktot = p.cu_keep[p.B];
   if (hidden != nullptr && ktot > 0) {
     const int words = static_cast<int>(row_bytes / 16);
     hipLaunchKernelGGL(gather_rows, dim3(ktot), dim3(256), 0, stream,
@@ -349,6 +737,7 @@ pace_status_t run_select(SelectParams& p, const void* hidden, size_t row_bytes, 
 }
 
 void size_select(Sizer& s, int nv_total, int nseg) {
+  s.take<MapPartial>((nv_total + kMapTokens - 1) / kMapTokens + nseg);   // map partials
   s.take<float>(nv_total);   // vraw
   s.take<float>(nv_total);   // lraw
   s.take<float>(nv_total);   // scores (when the caller passes none)
@@ -409,6 +798,7 @@ pace_status_t pace_ddae_select_varlen(const float* vis_mass, int Hv, int merge,
     return set_error(PACE_ERR_WORKSPACE, "pace_ddae_select: workspace %zu < %zu bytes",
                      workspace_bytes, need);
   Carver c(workspace, workspace_bytes);
+  p.part = c.take<MapPartial>((nv_total + kMapTokens - 1) / kMapTokens + B);
   p.vraw = c.take<float>(nv_total);
   p.lraw = c.take<float>(nv_total);
   float* sc = c.take<float>(nv_total);

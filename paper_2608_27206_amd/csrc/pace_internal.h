@@ -80,6 +80,91 @@ __device__ __forceinline__ float wave_min(float x) {
   return x;
 }
 
+// ---------------------------------------------------------------- range-checked buffers
+// A buffer resource over `bytes` bytes from `base`: loads past the end return 0 and stores
+// past the end are dropped by the hardware range check, so ragged tails need no branches
+// (a branch around every store makes the compiler wait for all memory traffic in flight at
+// each one).  Offsets are in bytes and go in the VGPR operand, which the check covers.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t range_rsrc(const void* base, unsigned bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+__device__ __forceinline__ float rload_f32(__amdgpu_buffer_rsrc_t r, unsigned off) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0));
+}
+__device__ __forceinline__ void rstore_b32(__amdgpu_buffer_rsrc_t r, unsigned off, uint32_t v) {
+  __builtin_amdgcn_raw_buffer_store_b32(v, r, off, 0, 0);
+}
+constexpr unsigned kNoStore = 0x7FFFFFF0u;   // an offset past every range: the store is dropped
+
+// ---------------------------------------------------------------- DPP wave primitives
+// Data-parallel-primitive lane moves run inside the VALU (a few cycles), where __shfl goes
+// through the LDS crossbar (ds_bpermute, ~100+ cycles of latency per step).
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp_u32(uint32_t x) {
+  return static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(x), CTRL, 0xf, 0xf, true));
+}
+template <int CTRL>
+__device__ __forceinline__ float dpp_f32(float x) {
+  return __uint_as_float(dpp_u32<CTRL>(__float_as_uint(x)));
+}
+template <int CTRL>
+__device__ __forceinline__ double dpp_f64(double x) {
+  const unsigned long long b = static_cast<unsigned long long>(__double_as_longlong(x));
+  const uint32_t lo = dpp_u32<CTRL>(static_cast<uint32_t>(b));
+  const uint32_t hi = dpp_u32<CTRL>(static_cast<uint32_t>(b >> 32));
+  return __longlong_as_double(static_cast<long long>((static_cast<unsigned long long>(hi) << 32) | lo));
+}
+__device__ __forceinline__ double readlane_f64(double x, int lane) {
+  const unsigned long long b = static_cast<unsigned long long>(__double_as_longlong(x));
+  const uint32_t lo = __builtin_amdgcn_readlane(static_cast<uint32_t>(b), lane);
+  const uint32_t hi = __builtin_amdgcn_readlane(static_cast<uint32_t>(b >> 32), lane);
+  return __longlong_as_double(static_cast<long long>((static_cast<unsigned long long>(hi) << 32) | lo));
+}
+constexpr int kDppQuadXor1 = 0xB1;      // quad_perm [1, 0, 3, 2]
+constexpr int kDppQuadXor2 = 0x4E;      // quad_perm [2, 3, 0, 1]
+constexpr int kDppRowHalfMirror = 0x141;
+constexpr int kDppRowMirror = 0x140;
+constexpr int kDppRowShr1 = 0x111;
+
+// Inclusive prefix sum over the 64 lanes (lane order).  Within each row of 16 lanes by
+// shifted DPP adds (lanes shifted in from outside the row read 0), then the totals of
+// the lower rows via readlane.
+__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t x) {
+  x += dpp_u32<kDppRowShr1>(x);
+  x += dpp_u32<kDppRowShr1 + 1>(x);
+  x += dpp_u32<kDppRowShr1 + 3>(x);
+  x += dpp_u32<kDppRowShr1 + 7>(x);
+  const uint32_t r0 = __builtin_amdgcn_readlane(x, 15);
+  const uint32_t r1 = __builtin_amdgcn_readlane(x, 31);
+  const uint32_t r2 = __builtin_amdgcn_readlane(x, 47);
+  const int row = (threadIdx.x & 63) >> 4;
+  return x + (row >= 1 ? r0 : 0u) + (row >= 2 ? r1 : 0u) + (row >= 3 ? r2 : 0u);
+}
+
+// Reduction over the 64 lanes to a wave-uniform value.  Butterfly within each row of 16
+// (every lane of a row ends with the bit-identical row result, since each step combines
+// the same two values in both lanes), then the four rows in a fixed order.
+template <typename T, typename Op>
+__device__ __forceinline__ T wave_reduce_dpp(T x, Op op) {
+  if constexpr (sizeof(T) == 8) {
+    x = op(x, dpp_f64<kDppQuadXor1>(x));
+    x = op(x, dpp_f64<kDppQuadXor2>(x));
+    x = op(x, dpp_f64<kDppRowHalfMirror>(x));
+    x = op(x, dpp_f64<kDppRowMirror>(x));
+    return op(op(readlane_f64(x, 0), readlane_f64(x, 16)), op(readlane_f64(x, 32), readlane_f64(x, 48)));
+  } else {
+    x = op(x, dpp_f32<kDppQuadXor1>(x));
+    x = op(x, dpp_f32<kDppQuadXor2>(x));
+    x = op(x, dpp_f32<kDppRowHalfMirror>(x));
+    x = op(x, dpp_f32<kDppRowMirror>(x));
+    const float a = __uint_as_float(__builtin_amdgcn_readlane(__float_as_uint(x), 0));
+    const float b = __uint_as_float(__builtin_amdgcn_readlane(__float_as_uint(x), 16));
+    const float c = __uint_as_float(__builtin_amdgcn_readlane(__float_as_uint(x), 32));
+    const float d = __uint_as_float(__builtin_amdgcn_readlane(__float_as_uint(x), 48));
+    return op(op(a, b), op(c, d));
+  }
+}
+
 // Block-wide reductions with a fixed combination order (deterministic).
 // `red` must hold at least blockDim.x / 64 floats; all threads must call.
 template <int OP>  // 0 sum, 1 max, 2 min
@@ -233,6 +318,56 @@ __device__ uint32_t block_radix_select_regs(const uint32_t (&key)[R], int n, int
     __syncthreads();
   }
   *need = remaining;
+  return prefix;
+}
+
+// Radix selection over keys held in registers (thread t holds element t * R + j in key[j],
+// or with STRIDED element j * blockDim.x + t; element i is valid when i < n), with one LDS
+// histogram per pass: `hist` holds 4 * 256 words that the caller zeroed before a barrier,
+// and `sel` 2 words.  Two barriers per pass.  Returns the k-th largest key T (1 <= k <= n)
+// and *need, the number of elements equal to T that belong to the top k (the lowest-index
+// ones).  All threads must call.
+template <int R, bool STRIDED>
+__device__ uint32_t radix_select_prezeroed(const uint32_t (&key)[R], int n, int k, uint32_t* hist,
+                                           uint32_t* sel, int* need) {
+  uint32_t prefix = 0, mask = 0;
+  uint32_t remaining = static_cast<uint32_t>(k);
+  const int t = threadIdx.x;
+#pragma unroll 1
+  for (int pass = 0; pass < 4; ++pass) {
+    const int shift = 24 - 8 * pass;
+    uint32_t* h = hist + 256 * pass;
+#pragma unroll
+    for (int j = 0; j < R; ++j) {
+      const int i = STRIDED ? j * static_cast<int>(blockDim.x) + t : t * R + j;
+      const bool active = (i < n) && (key[j] & mask) == prefix;
+      histogram_add(h, active, (key[j] >> shift) & 255u);
+    }
+    __syncthreads();
+    if (t < 64) {
+      // lane l covers digits 255 - 4l down to 252 - 4l (descending digit order)
+      const int dhi = 255 - 4 * t;
+      const uint32_t c0 = h[dhi], c1 = h[dhi - 1], c2 = h[dhi - 2], c3 = h[dhi - 3];
+      const uint32_t tot = c0 + c1 + c2 + c3;
+      uint32_t before = wave_incl_scan(tot) - tot;
+      const uint32_t cs[4] = {c0, c1, c2, c3};
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        if (before < remaining && before + cs[q] >= remaining) {
+          sel[0] = static_cast<uint32_t>(dhi - q);
+          sel[1] = remaining - before;
+        }
+        before += cs[q];
+      }
+    }
+    // sel is rewritten only after the first barrier of the next pass, which every thread
+    // reaches after reading it here
+    __syncthreads();
+    prefix |= sel[0] << shift;
+    mask |= 255u << shift;
+    remaining = sel[1];
+  }
+  *need = static_cast<int>(remaining);
   return prefix;
 }
 

@@ -158,3 +158,47 @@ def test_determinism():
     torch.cuda.synchronize()
     np.testing.assert_array_equal(host(r1[0]), host(r2[0]))
     np.testing.assert_array_equal(host(r1[1]), host(r2[1]))
+
+
+def test_varlen_keep_none_all_and_many_rows():
+    """Images whose K is 0, all of the image, or spread over many gather workgroups, in one
+    batch; and a batch with an image past the register-resident size (every image then takes
+    the general path)."""
+    from paper_2608_27206_amd import pace
+    import torch
+    import torch as t
+    for nvs, ratios in (([300, 64, 16384, 5000, 1], [0.0, 1.0, 0.5, 0.1, 1.0]),
+                        ([17000, 300, 2], [0.1, 0.3, 0.5])):
+        say(f"varlen nvs={nvs}")
+        rs = np.random.default_rng(sum(nvs))
+        keeps = [oddae.keep_count(r, n) for r, n in zip(ratios, nvs)]
+        nt = sum(nvs)
+        vis = rs.gamma(0.5, size=(2, nt)).astype(np.float32)
+        llm = rs.gamma(0.3, size=(3, nt)).astype(np.float32)
+        hidden = wl.random_bf16(nt, (nt, 64))
+        idx, sc, fz, out = pace.ddae_select(dev_f32(vis), 1, None, dev_f32(llm), nvs, keeps,
+                                            mode=0, hidden=dev_bf16(hidden))
+        torch.cuda.synchronize()
+        idx = host(idx)
+        assert idx.size == sum(keeps)
+        off = koff = 0
+        for b, (n, K) in enumerate(zip(nvs, keeps)):
+            S_ref, st = oddae.fuse(vis[:, off:off + n].astype(np.float64),
+                                   llm[:, off:off + n].astype(np.float64), 1, None, 0)
+            np.testing.assert_allclose(host(sc)[off:off + n], S_ref, atol=1e-5)
+            np.testing.assert_allclose(host(fz)[b], st, atol=1e-5)
+            got = idx[koff:koff + K] - off
+            ok, msg = kept_sets_agree(got, oddae.topk_indices(S_ref, K), S_ref)
+            assert ok, msg
+            np.testing.assert_array_equal(got, oddae.topk_indices(host(sc)[off:off + n], K))
+            off += n
+            koff += K
+        np.testing.assert_array_equal(out.view(t.int16).cpu().numpy().view(np.uint16), hidden[idx])
+
+
+def test_topk_many_rows_per_workgroup():
+    """K large enough that each gather workgroup copies more than the minimum four rows."""
+    rs = np.random.default_rng(21)
+    S = rs.random(16000).astype(np.float32)
+    S[5000:9000] = 0.5   # a long run of ties at the threshold
+    _topk_case(S, 8000, wl.random_bf16(21, (16000, 48)))
