@@ -43,11 +43,15 @@ struct DensityParams {
   float* rho_out;         // [4]
 };
 
-// Dword at byte offset a (4-aligned) of a range-checked buffer of `total` bytes.  A dword
-// that straddles the end is assembled from byte loads (a partly out-of-range dword load
-// would return zero for all four bytes).
-__device__ __forceinline__ uint32_t load_dword_tail(__amdgpu_buffer_rsrc_t rs, int a, int total) {
-  if (a + 4 <= total) return __builtin_amdgcn_raw_buffer_load_b32(rs, static_cast<unsigned>(a), 0, 0);
+// Dword at byte offset a (4-aligned) of a range-checked buffer of `total` bytes.  The plain
+// load returns zero for a dword that straddles the end (the range check is per dword), so
+// that one dword, the image's last, is assembled from byte loads in a separate fix-up
+// after a batch of plain loads (a branch per load would serialise the batch).
+__device__ __forceinline__ uint32_t load_dword(__amdgpu_buffer_rsrc_t rs, int a) {
+  return __builtin_amdgcn_raw_buffer_load_b32(rs, static_cast<unsigned>(a), 0, 0);
+}
+__device__ __forceinline__ bool straddles(int a, int total) { return a < total && a + 4 > total; }
+__device__ __noinline__ uint32_t load_dword_bytes(__amdgpu_buffer_rsrc_t rs, int a, int total) {
   uint32_t v = 0;
   for (int k = 0; k < 4 && a + k < total; ++k)
     v |= static_cast<uint32_t>(__builtin_amdgcn_raw_buffer_load_b8(rs, static_cast<unsigned>(a + k), 0, 0)) << (8 * k);
@@ -63,15 +67,45 @@ __device__ __forceinline__ int stage_tile(const DensityParams& p, int tile, uint
   const int px0 = (tile % p.tiles_x) * kPatchesPerTile;
   const int np = min(kPatchesPerTile, p.gw - px0);
   const int row_bytes = np * p.P * 3;
+  const int total = p.H * p.W * 3;
   const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<uint8_t*>(p.img), (short)0, p.H * p.W * 3, 0x00020000);
-  const int nd = (row_bytes + 3) / 4 + 1;
-  for (int e = threadIdx.x; e < p.P * nd; e += kApcThreads) {
-    const int r = e / nd, dd = e - r * nd;
-    const int b0 = (py * p.P + r) * p.W * 3 + px0 * p.P * 3;
-    const int a0 = b0 & ~3;
-    if (dd == 0) shift[r] = b0 - a0;
-    px[r * p.row_dwords + dd] = load_dword_tail(rs, a0 + 4 * dd, p.H * p.W * 3);
+      const_cast<uint8_t*>(p.img), (short)0, total, 0x00020000);
+  const int nd = (row_bytes + 3) / 4 + 1;   // <= 4 * kApcThreads dwords per row
+  // four rows at a time, all sixteen loads of a thread in flight before the LDS writes
+  for (int r0 = 0; r0 < p.P; r0 += 4) {
+    uint32_t v[4][4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int r = r0 + q;
+      const int a0 = ((py * p.P + r) * p.W * 3 + px0 * p.P * 3) & ~3;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int dd = static_cast<int>(threadIdx.x) + u * kApcThreads;
+        v[q][u] = (r < p.P && dd < nd) ? load_dword(rs, a0 + 4 * dd) : 0u;
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int a0 = ((py * p.P + r0 + q) * p.W * 3 + px0 * p.P * 3) & ~3;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int a = a0 + 4 * (static_cast<int>(threadIdx.x) + u * kApcThreads);
+        if (r0 + q < p.P && straddles(a, total)) v[q][u] = load_dword_bytes(rs, a, total);
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int r = r0 + q;
+      if (r < p.P) {
+        const int b0 = (py * p.P + r) * p.W * 3 + px0 * p.P * 3;
+        if (threadIdx.x == 0) shift[r] = b0 - (b0 & ~3);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int dd = static_cast<int>(threadIdx.x) + u * kApcThreads;
+          if (dd < nd) px[r * p.row_dwords + dd] = v[q][u];
+        }
+      }
+    }
   }
   *py_out = py;
   *px0_out = px0;
@@ -108,6 +142,7 @@ __global__ __launch_bounds__(kApcThreads) void apc_patch_pass(const DensityParam
     for (int r = 0; r < p.P; ++r) {
       const uint8_t* row = pxb + r * rb + shift[r] + j * pb;
       const float* cr = chat + r * pb;
+#pragma unroll 4
       for (int cb = t; cb < pb; cb += 4) {
         const float x = feat_of(row[cb]);
         if (PASS == 0) {
@@ -133,6 +168,7 @@ __global__ __launch_bounds__(kApcThreads) void apc_patch_pass(const DensityParam
       const int r = e / pb, cb = e - r * pb;
       const uint8_t* col = pxb + r * rb + shift[r] + cb;
       float sum = 0.f;
+#pragma unroll 8
       for (int jj = 0; jj < np; ++jj) sum += feat_of(col[jj * pb]) * inv[jj];
       p.partial[static_cast<long long>(tile) * p.D + e] = sum;
     }
@@ -149,8 +185,19 @@ __global__ __launch_bounds__(1024) void apc_reduce_c(const DensityParams p) {
   const int e = blockIdx.x * 64 + c;
   const int g = threadIdx.x >> 6;
   float s = 0.f;
-  if (e < p.D)
-    for (int t = g; t < p.n_tiles; t += 16) s += p.partial[static_cast<long long>(t) * p.D + e];
+  if (e < p.D) {
+    // eight tiles' loads in flight, added in tile order
+    for (int t0 = g; t0 < p.n_tiles; t0 += 16 * 8) {
+      float v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int t = t0 + 16 * u;
+        v[u] = t < p.n_tiles ? p.partial[static_cast<long long>(t) * p.D + e] : 0.f;
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) s += v[u];
+    }
+  }
   part[g][c] = s;
   __syncthreads();
   if (g == 0 && e < p.D) {
@@ -179,37 +226,125 @@ __global__ __launch_bounds__(1024) void apc_finalize_c(const DensityParams p) {
   }
 }
 
-constexpr int kTailR = 48;   // distances per thread held in registers: up to 49,152 patches
+constexpr int kTailR = 48;       // distances per thread held in registers: up to 49,152 patches
+constexpr int kTailBins = 4096;  // value bins over [0, 2], the range of d
+constexpr int kTailCand = 256;   // candidates ranked by direct comparison
 
+struct TailAdd { __device__ float operator()(float a, float b) const { return a + b; } };
+
+// Sum of the n_tail largest distances, then rho_d and rho.  d >= 0, so the raw bit patterns
+// order like the values.  With the distances in registers (thread t holds patches
+// j * 1024 + t): a histogram of floor(d * 2048) (monotone in d, clamped), the bin b* that
+// holds the n_tail-th largest value, the threshold T (the need-th largest key in bin b*,
+// by direct comparison among the bin's few candidates, or a radix select when it holds
+// many ties), and sum = (sum of d > T) + need_eq * T, reduced in a fixed order.
 __global__ __launch_bounds__(1024) void apc_tail(const DensityParams p) {
-  __shared__ uint32_t hist[256 + 8];
+  __shared__ __align__(16) uint32_t hist[kTailBins];
+  __shared__ uint32_t rhist[4 * 256];
+  __shared__ uint32_t cand_key[kTailCand];
+  __shared__ int cand_idx[kTailCand];
+  __shared__ __align__(16) uint32_t wt[16];
+  __shared__ uint32_t misc[8];   // 0: b*, 1: need, 2: candidates, 3: T, 4: need_eq, 5-6: radix
   __shared__ float red[16];
-  int need = 0;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   uint32_t T;
+  int need_eq;
   float s = 0.f;
-  // d >= 0, so the raw bit patterns order like the values
   if (p.N <= 1024 * kTailR) {
-    // every distance read once (coalesced): thread t owns patches j * 1024 + t
+    for (int i = tid; i < kTailBins; i += 1024) hist[i] = 0u;
+    rhist[tid] = 0u;
+    if (tid < 8) misc[tid] = 0u;
     uint32_t key[kTailR];
-#pragma unroll
-    for (int j = 0; j < kTailR; ++j) {
-      const int i = j * 1024 + static_cast<int>(threadIdx.x);
-      key[j] = (i < p.N) ? __float_as_uint(p.d[i]) : 0u;
-    }
-    T = block_radix_select_regs<kTailR, true>(key, p.N, p.n_tail, hist, &need);
+    const auto rd = range_rsrc(p.d, static_cast<unsigned>(p.N) * 4u);
 #pragma unroll
     for (int j = 0; j < kTailR; ++j)
-      if (j * 1024 + static_cast<int>(threadIdx.x) < p.N && key[j] > T) s += __uint_as_float(key[j]);
+      key[j] = __float_as_uint(rload_f32(rd, static_cast<unsigned>(j * 1024 + tid) * 4u));
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < kTailR; ++j) {
+      const int bin = static_cast<int>(fminf(__uint_as_float(key[j]) * 2048.f, static_cast<float>(kTailBins - 1)));
+      if (j * 1024 + tid < p.N) atomicAdd(&hist[bin], 1u);
+    }
+    __syncthreads();
+    // thread t covers bins 4095 - 4t down to 4092 - 4t (descending)
+    {
+      const int bhi = kTailBins - 1 - 4 * tid;
+      const uint4 h4 = *reinterpret_cast<const uint4*>(&hist[bhi - 3]);
+      const uint32_t cs[4] = {h4.w, h4.z, h4.y, h4.x};
+      const uint32_t tot = cs[0] + cs[1] + cs[2] + cs[3];
+      const uint32_t incl = wave_incl_scan(tot);
+      if (lane == 63) wt[w] = incl;
+      __syncthreads();
+      uint32_t before = incl - tot;
+      for (int i = 0; i < w; ++i) before += wt[i];
+      const uint32_t K = static_cast<uint32_t>(p.n_tail);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        if (before < K && before + cs[q] >= K) { misc[0] = bhi - q; misc[1] = K - before; }
+        before += cs[q];
+      }
+    }
+    __syncthreads();
+    const int bstar = static_cast<int>(misc[0]);
+    const int need = static_cast<int>(misc[1]);   // 1 <= need <= count of bin b*
+#pragma unroll
+    for (int j = 0; j < kTailR; ++j) {
+      const int bin = static_cast<int>(fminf(__uint_as_float(key[j]) * 2048.f, static_cast<float>(kTailBins - 1)));
+      if (j * 1024 + tid < p.N && bin == bstar) {
+        const uint32_t slot = atomicAdd(&misc[2], 1u);
+        if (slot < static_cast<uint32_t>(kTailCand)) { cand_key[slot] = key[j]; cand_idx[slot] = j * 1024 + tid; }
+      }
+    }
+    __syncthreads();
+    const uint32_t ncand = misc[2];
+    if (ncand <= static_cast<uint32_t>(kTailCand)) {
+      if (tid < static_cast<int>(ncand)) {
+        const uint32_t kt = cand_key[tid];
+        const int it = cand_idx[tid];
+        int rank = 0, greater = 0;
+#pragma unroll 8
+        for (uint32_t u = 0; u < ncand; ++u) {
+          const uint32_t ku = cand_key[u];
+          rank += (ku > kt || (ku == kt && cand_idx[u] < it)) ? 1 : 0;
+          greater += ku > kt ? 1 : 0;
+        }
+        if (rank == need - 1) { misc[3] = kt; misc[4] = static_cast<uint32_t>(need - greater); }
+      }
+    } else {
+      // many equal distances in one bin: radix select over the candidates' keys (+1, so
+      // that every candidate ranks above the non-candidates' 0)
+      uint32_t ck[kTailR];
+#pragma unroll
+      for (int j = 0; j < kTailR; ++j) {
+        const int bin = static_cast<int>(fminf(__uint_as_float(key[j]) * 2048.f, static_cast<float>(kTailBins - 1)));
+        ck[j] = (j * 1024 + tid < p.N && bin == bstar) ? key[j] + 1u : 0u;
+      }
+      int ne = 0;
+      const uint32_t T1 = radix_select_prezeroed<kTailR, true>(ck, p.N, need, rhist, &misc[5], &ne);
+      if (tid == 0) { misc[3] = T1 - 1u; misc[4] = static_cast<uint32_t>(ne); }
+    }
+    __syncthreads();
+    T = misc[3];
+    need_eq = static_cast<int>(misc[4]);
+#pragma unroll
+    for (int j = 0; j < kTailR; ++j)
+      if (j * 1024 + tid < p.N && key[j] > T) s += __uint_as_float(key[j]);
   } else {
-    T = block_radix_select(p.N, p.n_tail, [&](int i) { return __float_as_uint(p.d[i]); }, hist, &need);
-    for (int i = threadIdx.x; i < p.N; i += 1024) {
+    int need = 0;
+    T = block_radix_select(p.N, p.n_tail, [&](int i) { return __float_as_uint(p.d[i]); }, rhist, &need);
+    need_eq = need;
+    for (int i = tid; i < p.N; i += 1024) {
       const float x = p.d[i];
       if (__float_as_uint(x) > T) s += x;
     }
   }
-  s = block_reduce<0>(s, red);
-  if (threadIdx.x == 0) {
-    const float d_top = (s + static_cast<float>(need) * __uint_as_float(T)) / static_cast<float>(p.n_tail);
+  s = wave_reduce_dpp(s, TailAdd{});
+  if (lane == 0) red[w] = s;
+  __syncthreads();
+  if (tid == 0) {
+    float tot = 0.f;
+    for (int i = 0; i < 16; ++i) tot += red[i];
+    const float d_top = (tot + static_cast<float>(need_eq) * __uint_as_float(T)) / static_cast<float>(p.n_tail);
     const float rho_g = p.stats[1];
     const float rho_d = fminf(d_top / p.gamma, 1.0f);
     p.rho_out[0] = rho_g;
@@ -275,6 +410,150 @@ __device__ __forceinline__ int make_taps(int o, int n, int m, int slots, float* 
   return lo + j0;
 }
 
+// make_taps with the candidate weights in registers (slots <= kRegTaps): one LDS write per
+// weight instead of a read-modify-write sequence through LDS.  Same weights, lo and count.
+constexpr int kRegTaps = 16;
+__device__ __forceinline__ int make_taps_reg(int o, int n, int m, int slots, float* w_out, int* count) {
+  const float centre = (static_cast<float>(o) + 0.5f) * static_cast<float>(n) / static_cast<float>(m);
+  const float support = 2.f * fmaxf(1.f, static_cast<float>(n) / static_cast<float>(m));
+  const int lo = max(static_cast<int>(floorf(centre - support - 0.5f)) - 1, 0);
+  const float inv_den = 1.f / static_cast<float>(2ll * (n > m ? n : m));
+  long long num = (2ll * lo + 1) * m - (2ll * o + 1) * n;
+  float w[kRegTaps];
+  float sum = 0.f;
+  int j0 = kRegTaps, j1 = 0;
+#pragma unroll
+  for (int j = 0; j < kRegTaps; ++j, num += 2ll * m) {
+    const float wt = (j < slots && lo + j < n) ? keys_cubic(static_cast<float>(num) * inv_den) : 0.f;
+    w[j] = wt;
+    sum += wt;
+    if (wt != 0.f) { j0 = min(j0, j); j1 = j; }
+  }
+  if (j0 > j1) j0 = j1;
+  const float inv = 1.f / sum;
+  const int cnt = j1 - j0 + 1;
+#pragma unroll
+  for (int j = 0; j < kRegTaps; ++j) {
+    if (j >= j0 && j <= j1) w_out[j - j0] = w[j] * inv;
+    if (j >= cnt && j < slots) w_out[j] = 0.f;
+  }
+  *count = cnt;
+  return lo + j0;
+}
+
+// The resize with taps of at most kRegTaps per axis (shrinks up to 3x per side) and
+// tx dividing the block: the horizontal pass keeps one output column per thread, its
+// weights in registers, and reads each staged row's bytes as aligned dwords; the vertical
+// pass keeps one (column, channel) per thread.  Same arithmetic, in the same order, as
+// apc_resize.
+__global__ __launch_bounds__(kRsThreads) void apc_resize_reg(const ResizeParams p) {
+  extern __shared__ float sm[];
+  float* wx = sm + p.o_wx;                      // [tx][ntx], ntx a multiple of 4
+  float* wy = sm + p.o_wy;                      // [ty][nty]
+  int* lox = reinterpret_cast<int*>(sm + p.o_lox);
+  int* loy = reinterpret_cast<int*>(sm + p.o_loy);
+  int* cnx = lox + p.tx;
+  int* cny = loy + p.ty;
+  uint32_t* pix = reinterpret_cast<uint32_t*>(sm + p.o_pix);
+  float* hb = sm + p.o_h;
+  __shared__ int shift[256];
+  const int tid = threadIdx.x;
+  const int ox0 = blockIdx.x * p.tx, oy0 = blockIdx.y * p.ty;
+  const int ncols = min(p.tx, p.oW - ox0), nrows = min(p.ty, p.oH - oy0);
+  // columns on the first waves, rows on the last wave
+  if (tid < ncols) lox[tid] = make_taps_reg(ox0 + tid, p.W, p.oW, p.ntx, wx + tid * p.ntx, &cnx[tid]);
+  if (tid >= kRsThreads - 64 && tid - (kRsThreads - 64) < nrows) {
+    const int r = tid - (kRsThreads - 64);
+    loy[r] = make_taps_reg(oy0 + r, p.H, p.oH, p.nty, wy + r * p.nty, &cny[r]);
+  }
+  __syncthreads();
+  const int xlo = lox[0], ylo = loy[0];
+  const int xin = lox[ncols - 1] + cnx[ncols - 1] - xlo;
+  const int yin = loy[nrows - 1] + cny[nrows - 1] - ylo;
+  const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint8_t*>(p.src), (short)0, p.H * p.W * 3, 0x00020000);
+  const int nd = (xin * 3 + 3) / 4 + 1;
+  const int total = p.H * p.W * 3;
+  for (int r = tid; r < yin; r += kRsThreads) {
+    const int b0 = (ylo + r) * p.W * 3 + xlo * 3;
+    shift[r] = b0 - (b0 & ~3);
+  }
+  for (int e0 = tid; e0 < yin * nd; e0 += 8 * kRsThreads) {
+    uint32_t v[8];
+    int slot[8], addr[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int e = e0 + u * kRsThreads;
+      const int r = e / nd, d = e - r * nd;
+      const int a0 = ((ylo + r) * p.W * 3 + xlo * 3) & ~3;
+      slot[u] = (e < yin * nd) ? r * p.row_dwords + d : -1;
+      addr[u] = a0 + 4 * d;
+      v[u] = (e < yin * nd) ? load_dword(rs, addr[u]) : 0u;
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      if (slot[u] >= 0 && straddles(addr[u], total)) v[u] = load_dword_bytes(rs, addr[u], total);
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      if (slot[u] >= 0) pix[slot[u]] = v[u];
+  }
+  __syncthreads();
+  // horizontal pass: thread -> output column c, staged rows g, g + G, ...
+  {
+    const int c = tid % p.tx, g = tid / p.tx, G = kRsThreads / p.tx;
+    if (c < ncols) {
+      float wr[kRegTaps];
+#pragma unroll
+      for (int q = 0; q < kRegTaps / 4; ++q) {
+        const float4 f = (4 * q < p.ntx) ? *reinterpret_cast<const float4*>(wx + c * p.ntx + 4 * q)
+                                         : make_float4(0.f, 0.f, 0.f, 0.f);
+        wr[4 * q] = f.x; wr[4 * q + 1] = f.y; wr[4 * q + 2] = f.z; wr[4 * q + 3] = f.w;
+      }
+      const int nt = cnx[c];
+      const int xoff = (lox[c] - xlo) * 3;
+      for (int r = g; r < yin; r += G) {
+        const int off = shift[r] + xoff;                       // byte offset in the staged row
+        const uint32_t* dp = pix + r * p.row_dwords + (off >> 2);
+        const uint32_t sh = static_cast<uint32_t>(off & 3);
+        uint32_t d[13];
+#pragma unroll
+        for (int k = 0; k < 13; ++k) d[k] = dp[k];
+        uint32_t e[12];
+#pragma unroll
+        for (int k = 0; k < 12; ++k) e[k] = __builtin_amdgcn_alignbyte(d[k + 1], d[k], sh);
+        float a0 = 0.f, a1 = 0.f, a2 = 0.f;
+#pragma unroll
+        for (int j = 0; j < kRegTaps; ++j) {
+          if (j < nt) {
+            const int b = 3 * j;
+            a0 += wr[j] * static_cast<float>((e[b >> 2] >> (8 * (b & 3))) & 255u);
+            a1 += wr[j] * static_cast<float>((e[(b + 1) >> 2] >> (8 * ((b + 1) & 3))) & 255u);
+            a2 += wr[j] * static_cast<float>((e[(b + 2) >> 2] >> (8 * ((b + 2) & 3))) & 255u);
+          }
+        }
+        float* h = hb + (r * p.tx + c) * 3;
+        h[0] = a0; h[1] = a1; h[2] = a2;
+      }
+    }
+  }
+  __syncthreads();
+  // vertical pass: thread -> (column, channel), every output row of the tile
+  if (tid < 3 * ncols) {
+    const int c = tid / 3, ch = tid - 3 * c;
+    for (int r = 0; r < nrows; ++r) {
+      const float* w = wy + r * p.nty;
+      const int base = loy[r] - ylo;
+      const int nt = cny[r];
+      float acc = 0.f;
+#pragma unroll 4
+      for (int j = 0; j < nt; ++j) acc += w[j] * hb[((base + j) * p.tx + c) * 3 + ch];
+      const float v = floorf(acc + 0.5f);
+      const int u = static_cast<int>(fminf(fmaxf(v, 0.f), 255.f));
+      p.dst[(static_cast<long long>(oy0 + r) * p.oW + ox0 + c) * 3 + ch] = static_cast<uint8_t>(u);
+    }
+  }
+}
+
 __global__ __launch_bounds__(kRsThreads) void apc_resize(const ResizeParams p) {
   extern __shared__ float sm[];
   float* wx = sm + p.o_wx;                      // [tx][ntx]
@@ -300,12 +579,30 @@ __global__ __launch_bounds__(kRsThreads) void apc_resize(const ResizeParams p) {
   const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint8_t*>(p.src), (short)0, p.H * p.W * 3, 0x00020000);
   const int nd = (xin * 3 + 3) / 4 + 1;
-  for (int e = threadIdx.x; e < yin * nd; e += kRsThreads) {
-    const int r = e / nd, d = e - r * nd;
+  const int total = p.H * p.W * 3;
+  for (int r = threadIdx.x; r < yin; r += kRsThreads) {
     const int b0 = (ylo + r) * p.W * 3 + xlo * 3;
-    const int a0 = b0 & ~3;
-    if (d == 0) shift[r] = b0 - a0;
-    pix[r * p.row_dwords + d] = load_dword_tail(rs, a0 + 4 * d, p.H * p.W * 3);
+    shift[r] = b0 - (b0 & ~3);
+  }
+  // eight loads in flight per thread before their LDS writes
+  for (int e0 = threadIdx.x; e0 < yin * nd; e0 += 8 * kRsThreads) {
+    uint32_t v[8];
+    int slot[8], addr[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int e = e0 + u * kRsThreads;
+      const int r = e / nd, d = e - r * nd;
+      const int a0 = ((ylo + r) * p.W * 3 + xlo * 3) & ~3;
+      slot[u] = (e < yin * nd) ? r * p.row_dwords + d : -1;
+      addr[u] = a0 + 4 * d;
+      v[u] = (e < yin * nd) ? load_dword(rs, addr[u]) : 0u;
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      if (slot[u] >= 0 && straddles(addr[u], total)) v[u] = load_dword_bytes(rs, addr[u], total);
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      if (slot[u] >= 0) pix[slot[u]] = v[u];
   }
   __syncthreads();
   const uint8_t* pixb = reinterpret_cast<const uint8_t*>(pix);
@@ -316,6 +613,7 @@ __global__ __launch_bounds__(kRsThreads) void apc_resize(const ResizeParams p) {
     const float* w = wx + c * p.ntx;
     const int nt = cnx[c];
     float a0 = 0.f, a1 = 0.f, a2 = 0.f;
+#pragma unroll 4
     for (int j = 0; j < nt; ++j) {
       const float wt = w[j];
       a0 += wt * static_cast<float>(row[3 * j + 0]);
@@ -334,6 +632,7 @@ __global__ __launch_bounds__(kRsThreads) void apc_resize(const ResizeParams p) {
     const int base = loy[r] - ylo;
     const int nt = cny[r];
     float acc = 0.f;
+#pragma unroll 4
     for (int j = 0; j < nt; ++j) acc += w[j] * hb[((base + j) * p.tx + c) * 3 + ch];
     const float v = floorf(acc + 0.5f);
     const int u = static_cast<int>(fminf(fmaxf(v, 0.f), 255.f));
@@ -456,6 +755,17 @@ pace_status_t pace_apc_downsample(const uint8_t* src, int H, int W, uint8_t* dst
     lds = plan(ty, tx, p);
   }
   dim3 grid((oW + tx - 1) / tx, (oH + ty - 1) / ty);
+  const int ntx4 = (p.ntx + 3) / 4 * 4;
+  if (ntx4 <= kRegTaps && p.nty <= kRegTaps && kRsThreads % tx == 0 && 3 * tx <= kRsThreads &&
+      (tx == 64 || tx == 32 || tx == 16)) {
+    ResizeParams q = p;
+    q.ntx = ntx4;
+    const size_t lds_q = plan(ty, tx, q);
+    if (lds_q <= kRsMaxLds) {
+      hipLaunchKernelGGL(apc_resize_reg, grid, dim3(kRsThreads), lds_q, stream, q);
+      return check_launch("apc_resize_reg");
+    }
+  }
   hipLaunchKernelGGL(apc_resize, grid, dim3(kRsThreads), lds, stream, p);
   return check_launch("apc_resize");
 }
