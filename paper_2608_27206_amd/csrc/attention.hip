@@ -118,6 +118,26 @@ __device__ __forceinline__ void dma16(i32x4 r, unsigned lds, unsigned voff) {
                :: "s"(m0), "v"(voff), "s"(r) : "memory", "m0");
 }
 __device__ __forceinline__ void wait_vmem() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+// As dma16 with 4 bytes per lane (lds + 4 * lane).
+__device__ __forceinline__ void dma4(i32x4 r, unsigned lds, unsigned voff) {
+  const unsigned m0 = __builtin_amdgcn_readfirstlane(lds);
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dword %1, %2, 0 offen lds"
+               :: "s"(m0), "v"(voff), "s"(r) : "memory", "m0");
+}
+// Waits until at most n (wave-uniform, <= 7) of this wave's vector memory operations are
+// outstanding: the older ones, issued first, have completed.
+__device__ __forceinline__ void wait_vmem_upto(int n) {
+  switch (n) {
+    case 0: asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); break;
+    case 1: asm volatile("s_waitcnt vmcnt(1)" ::: "memory"); break;
+    case 2: asm volatile("s_waitcnt vmcnt(2)" ::: "memory"); break;
+    case 3: asm volatile("s_waitcnt vmcnt(3)" ::: "memory"); break;
+    case 4: asm volatile("s_waitcnt vmcnt(4)" ::: "memory"); break;
+    case 5: asm volatile("s_waitcnt vmcnt(5)" ::: "memory"); break;
+    case 6: asm volatile("s_waitcnt vmcnt(6)" ::: "memory"); break;
+    default: asm volatile("s_waitcnt vmcnt(7)" ::: "memory"); break;
+  }
+}
 
 // Compile-time loop: f(integral_constant<int, I>) for I in [B, E), so register arrays
 // are only ever indexed by constants.
@@ -903,6 +923,7 @@ template <int D, bool CAUSAL>
 __global__ __launch_bounds__(kThreads, (D == 80 && !CAUSAL) ? 3 : 2) void attn_mass(const MassParams p) {
   using C = MassCfg<D>;
   __shared__ __align__(16) uint16_t Qs[3][C::QBUF];
+  __shared__ __align__(16) float Ls[3][kMassQ];   // LSE of each Q tile's rows (natural log)
 
   const int lb = remap_block_id(blockIdx.x, gridDim.x);
   const int per_head = p.nseg * p.nkt;
@@ -940,8 +961,8 @@ __global__ __launch_bounds__(kThreads, (D == 80 && !CAUSAL) ? 3 : 2) void attn_m
   // querying rows [qs, qs + ql) of the segment: Q rows and their LSE
   const auto rq = make_dma_rsrc(p.q + static_cast<long long>(s0 + qs) * qstride + h * D,
                                 ql > 0 ? static_cast<unsigned>((ql - 1) * qstride + D) * 2u : 0u);
-  const auto rl = make_rsrc(p.lse + static_cast<long long>(h) * p.Ntot + s0 + qs,
-                            static_cast<unsigned>(ql) * 4u);
+  const auto rl = make_dma_rsrc(p.lse + static_cast<long long>(h) * p.Ntot + s0 + qs,
+                                static_cast<unsigned>(ql) * 4u);
   unsigned qoff[C::QPW];
   static_for<0, C::QPW>([&](auto I) __attribute__((always_inline)) {
     const int c = (w + 4 * I) * 64 + lane;
@@ -951,15 +972,23 @@ __global__ __launch_bounds__(kThreads, (D == 80 && !CAUSAL) ? 3 : 2) void attn_m
   });
   const unsigned qtile_bytes = static_cast<unsigned>(kMassQ * qstride) * 2u;
   const unsigned qs_lds = lds_u32(&Qs[0][0]);
+  // The LSE rows of a tile come with its Q rows, by DMA from the wave with the fewest Q chunks.
+  constexpr int kLseWave = C::QINST % 4;
+  const unsigned ls_lds = lds_u32(&Ls[0][0]);
   auto load_q = [&](int t, int buf) __attribute__((always_inline)) {
     static_for<0, C::QPW>([&](auto I) __attribute__((always_inline)) {
       if (w + 4 * I < C::QINST) dma16(rq, qs_lds + (buf * C::QBUF + (w + 4 * I) * 512) * 2, qoff[I] + t * qtile_bytes);
     });
+    if (w == kLseWave) dma4(rl, ls_lds + buf * kMassQ * 4, static_cast<unsigned>(t * kMassQ + lane) * 4u);
   };
-  // LSE of this lane's query row of tile t (log2 units); rows past the range get +inf -> P = 0
-  auto load_lse2 = [&](int t, int u) __attribute__((always_inline)) {
+  // DMA instructions this wave issues per tile
+  int dma_per_tile = (w == kLseWave) ? 1 : 0;
+  static_for<0, C::QPW>([&](auto I) __attribute__((always_inline)) { dma_per_tile += (w + 4 * I < C::QINST) ? 1 : 0; });
+  // LSE of this lane's query row of the tile in buffer buf (log2 units); rows past the range
+  // get +inf -> P = 0
+  auto load_lse2 = [&](int t, int buf, int u) __attribute__((always_inline)) {
     const int r = t * kMassQ + u * 32 + c32;
-    const float v = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rl, static_cast<unsigned>(r) * 4u, 0, 0));
+    const float v = Ls[buf][u * 32 + c32];
     return (r < ql) ? v * kLog2e : INFINITY;
   };
   // S^T of the 32-row half u of the query tile in buffer buf
@@ -999,18 +1028,21 @@ __global__ __launch_bounds__(kThreads, (D == 80 && !CAUSAL) ? 3 : 2) void attn_m
       }
   };
 
-  // Three query-tile buffers: Q(t+2) is loaded while Q(t) is read, into the buffer of Q(t-1)
-  // that every wave left behind at this iteration's barrier.  No software pipelining within
-  // a wave: three workgroups per CU overlap one wave's MFMAs with the others' VALU work.
+  // Three query-tile buffers: Q(t+2) and its LSE rows are loaded while Q(t) is read, into the
+  // buffer of Q(t-1) that every wave left behind at this iteration's barrier.  No software
+  // pipelining within a wave: three workgroups per CU overlap one wave's MFMAs with the
+  // others' VALU work.
   const int ntiles = (ql + kMassQ - 1) / kMassQ;
   if (ntiles > 0) {
     load_q(0, 0);
     if (ntiles > 1) load_q(1, 1);
     int buf = 0;
     for (int t = 0; t < ntiles; ++t) {
-      const float l2a = load_lse2(t, 0), l2b = load_lse2(t, 1);
-      wait_vmem();
+      // tile t's DMA (issued two iterations ago) has landed once at most tile t+1's
+      // instructions are outstanding
+      wait_vmem_upto(t + 1 < ntiles ? dma_per_tile : 0);
       __syncthreads();
+      const float l2a = load_lse2(t, buf, 0), l2b = load_lse2(t, buf, 1);
       const int buf2 = (buf == 0) ? 2 : buf - 1;   // (t + 2) % 3
       if (t + 2 < ntiles) load_q(t + 2, buf2);
       f32x16 sa[2], sb[2];
