@@ -116,6 +116,41 @@ def density_from_features(T: np.ndarray, tail_frac: float = TAIL_FRAC, alpha: fl
             "d_top": d_top, "c_hat": c_hat}
 
 
+def normalise_embeddings(x: np.ndarray, eps: float = 1e-12) -> np.ndarray:
+    """T_i = x_i / max(||x_i||, eps) for caller-supplied preview embeddings (Section 3.2: the
+    embeddings are l2-normalised).  Reading: a zero embedding is a zero direction (T_i = 0)."""
+    x = np.asarray(x, dtype=np.float64)
+    n = np.linalg.norm(x, axis=1, keepdims=True)
+    return x / np.maximum(n, eps)
+
+
+def global_density_dot(T: np.ndarray, chunk: int = 1024) -> float:
+    """Eq. 1 for normalised rows written as dot products, (1/N^2) sum_i sum_j T_i . T_j over all
+    ordered pairs; equal to global_density for unit rows and defined when a row is zero."""
+    N = T.shape[0]
+    total = 0.0
+    for a in range(0, N, chunk):
+        b = min(N, a + chunk)
+        total += float((T[a:b] @ T.T).sum())
+    return total / (N * N)
+
+
+def embedding_density(x: np.ndarray, tail_frac: float = TAIL_FRAC, alpha: float = ALPHA,
+                      gamma: float = GAMMA) -> dict:
+    """The APC scores of caller-supplied preview embeddings x [N, D] (the paper's preview is the
+    first vision-encoder block): the steps of density_from_features after normalisation."""
+    T = normalise_embeddings(x)
+    phi = global_density_dot(T)
+    rho_g = 1.0 - phi                                   # Eq. 2
+    c_hat = background_direction(T)
+    d = detail_distances(T, c_hat)
+    d_top = tail_mean(d, tail_frac)
+    rho_d = min(d_top / gamma, 1.0)
+    rho = alpha * rho_g + (1.0 - alpha) * rho_d
+    return {"phi": phi, "rho_g": rho_g, "rho_d": rho_d, "rho": rho, "d": d,
+            "d_top": d_top, "c_hat": c_hat}
+
+
 def apc_density(img: np.ndarray, patch: int = 14, tail_frac: float = TAIL_FRAC,
                 alpha: float = ALPHA, gamma: float = GAMMA) -> dict:
     """APC density of a uint8 HWC image, with the pixel stand-in feature."""

@@ -161,3 +161,51 @@ def test_target_size_rules():
     # never larger than the input, never below one snap
     assert apc.target_size(1.0, 50, 50, 0, 1e12, 28) == (28, 28)
     assert apc.target_size(0.0, 3000, 3000, 0, 1e12, 28) == (28, 28)
+
+
+# ---------------------------------------------------------------- caller-supplied embeddings
+def test_embedding_density_equals_image_path_on_patch_features():
+    """Feeding the pixel stand-in features as embeddings reproduces the image path."""
+    img = np.random.default_rng(5).integers(0, 256, size=(112, 140, 3), dtype=np.uint8)
+    ref = apc.apc_density(img, 14)
+    got = apc.embedding_density(apc.patch_features(img, 14))
+    for key in ("phi", "rho_g", "rho_d", "rho"):
+        assert abs(got[key] - ref[key]) < 1e-12
+    np.testing.assert_allclose(got["d"], ref["d"], atol=1e-12)
+
+
+def test_embedding_density_is_scale_invariant_per_row():
+    rs = np.random.default_rng(3)
+    x = rs.normal(size=(300, 40))
+    scale = rs.uniform(0.01, 100.0, size=(300, 1))
+    a = apc.embedding_density(x)
+    b = apc.embedding_density(x * scale)
+    for key in ("phi", "rho_g", "rho_d", "rho"):
+        assert abs(a[key] - b[key]) < 1e-12
+
+
+def test_embedding_density_dot_form_matches_cosines_for_nonzero_rows():
+    rs = np.random.default_rng(4)
+    x = rs.normal(size=(257, 33)) + 0.3
+    T = apc.normalise_embeddings(x)
+    assert abs(apc.global_density_dot(T) - apc.global_density(T)) < 1e-12
+    # explicit double loop on a small case
+    y = rs.normal(size=(7, 5))
+    Ty = apc.normalise_embeddings(y)
+    brute = sum(float(Ty[i] @ Ty[j]) for i in range(7) for j in range(7)) / 49
+    assert abs(apc.global_density_dot(Ty) - brute) < 1e-14
+
+
+def test_embedding_density_opposite_rows_and_zero_row():
+    """Rows and their negatives: c = 0, so phi = 0, rho_g = 1 and every unit row has d = 1; a zero
+    row is a zero direction, so its distance is ||c_hat|| (here 0)."""
+    rs = np.random.default_rng(5)
+    x = rs.normal(size=(50, 16))
+    x = np.concatenate([x, -x, np.zeros((1, 16))])
+    r = apc.embedding_density(x)
+    assert abs(r["phi"]) < 1e-15 and abs(r["rho_g"] - 1.0) < 1e-15
+    np.testing.assert_allclose(r["d"][:100], 1.0, atol=1e-12)
+    assert r["d"][100] == 0.0
+    # identical rows: phi = 1 and every distance is 0
+    s = apc.embedding_density(np.tile(rs.normal(size=(1, 16)), (20, 1)))
+    assert abs(s["phi"] - 1.0) < 1e-12 and np.max(s["d"]) < 1e-7
