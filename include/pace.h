@@ -111,6 +111,26 @@ pace_status_t pace_apc_density(const uint8_t* img, int H, int W, int patch, doub
                                float alpha, float gamma, float* d_out, float* rho_out,
                                void* workspace, size_t workspace_bytes, hipStream_t stream);
 
+/* Workspace bytes for pace_apc_density_features. */
+size_t pace_apc_density_features_workspace_size(int N, int D);
+
+/*
+ * APC information density of caller-supplied preview embeddings (Section 3.2: the shallow
+ * feature preview's l2-normalised patch embeddings; Eq. 1-2, the background direction, the
+ * detail distances, the tail mean, rho_d and rho).  The paper's preview is the vision
+ * encoder's first block at the original resolution; a caller that runs it passes its output.
+ *   feat      bf16 [N, D] row-major, N >= 1, D >= 1 (read as 16-byte vectors when D is a
+ *             multiple of 8 and feat is 16-byte aligned, value by value otherwise).
+ *             T_i = feat_i / max(||feat_i||, 1e-12) (a zero row is a zero direction).
+ *   tail_frac, alpha, gamma, d_out, rho_out   as in pace_apc_density.
+ * Same arithmetic as pace_apc_density after its pixel features: phi = ||mean_i T_i||^2,
+ * c_hat zero when ||c|| <= 1e-5, n_tail = max(1, pace_keep_count(tail_frac, N)).
+ * Reads the matrix twice.  Asynchronous on `stream`.
+ */
+pace_status_t pace_apc_density_features(const uint16_t* feat, int N, int D, double tail_frac,
+                                        float alpha, float gamma, float* d_out, float* rho_out,
+                                        void* workspace, size_t workspace_bytes, hipStream_t stream);
+
 /*
  * APC resize (Appendix implementation details: bicubic resize of both sides).
  *   src uint8 [H, W, 3] -> dst uint8 [oH, oW, 3], with 1 <= oH <= H and 1 <= oW <= W.

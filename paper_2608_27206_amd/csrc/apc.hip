@@ -26,6 +26,7 @@ constexpr int kMaxPatch = 16;
 
 struct DensityParams {
   const uint8_t* img;
+  const uint16_t* feat;   // caller-supplied embeddings, bf16 [N, D] (feature entry point)
   int H, W, P;            // image and patch size
   int gh, gw, N;          // patch grid
   int D;                  // 3 * P * P
@@ -174,6 +175,119 @@ __global__ __launch_bounds__(kApcThreads) void apc_patch_pass(const DensityParam
     }
   } else {
     if (j < np && t == 0) p.d[py * p.gw + px0 + j] = sqrtf(acc);
+  }
+}
+
+// ---------------------------------------------------------------- caller-supplied embeddings
+// Density of bf16 embeddings x [N, D] (the first vision block's output in the paper's
+// preview): T_i = x_i / max(||x_i||, 1e-12).  Two passes over the matrix:
+//   apc_feat_pass<0>  per block of 64 rows: each wave takes 16 rows, values spread over its
+//                     lanes, for 1/||x_i||; then each thread sums its columns (8-column chunks
+//                     when rows are 16-byte vectors) of x_i / ||x_i|| over the block's rows
+//                     (L2-resident) -> the block partial
+//   apc_feat_pass<1>  one wave per row: d_i = ||x_i / ||x_i|| - c_hat||
+// The partials then go through apc_reduce_c, apc_finalize_c and apc_tail as for images.
+constexpr int kFeatRows = 64;
+
+__device__ __forceinline__ float bf16_lo(uint32_t u) { return __uint_as_float(u << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t u) { return __uint_as_float(u & 0xFFFF0000u); }
+
+struct FeatAdd { __device__ float operator()(float a, float b) const { return a + b; } };
+
+// VEC: rows are read as 16-byte chunks of 8 values (D a multiple of 8, aligned rows);
+// otherwise value by value.
+template <int PASS, bool VEC>
+__global__ __launch_bounds__(256) void apc_feat_pass(const DensityParams p) {
+  __shared__ float inv[kFeatRows];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int nchunk = p.D / 8;
+  auto bf = [](uint16_t b) { return __uint_as_float(static_cast<uint32_t>(b) << 16); };
+  if (PASS == 0) {
+    const int r0 = blockIdx.x * kFeatRows;
+    for (int rr = w; rr < kFeatRows; rr += 4) {
+      const int i = r0 + rr;
+      float ss = 0.f;
+      if (i < p.N) {
+        const uint16_t* rowp = p.feat + static_cast<long long>(i) * p.D;
+        if constexpr (VEC) {
+          const uint4* row = reinterpret_cast<const uint4*>(rowp);
+          for (int c = lane; c < nchunk; c += 64) {
+            const uint4 v = row[c];
+            const float a[8] = {bf16_lo(v.x), bf16_hi(v.x), bf16_lo(v.y), bf16_hi(v.y),
+                                bf16_lo(v.z), bf16_hi(v.z), bf16_lo(v.w), bf16_hi(v.w)};
+#pragma unroll
+            for (int k = 0; k < 8; ++k) ss += a[k] * a[k];
+          }
+        } else {
+          for (int e = lane; e < p.D; e += 64) {
+            const float a = bf(rowp[e]);
+            ss += a * a;
+          }
+        }
+      }
+      ss = wave_reduce_dpp(ss, FeatAdd{});
+      if (lane == 0) {
+        const float in = (i < p.N) ? 1.0f / fmaxf(sqrtf(ss), 1e-12f) : 0.f;
+        inv[rr] = in;
+        if (i < p.N) p.inv_norm[i] = in;
+      }
+    }
+    __syncthreads();
+    // block partial of sum_i T_i, rows added in index order
+    const int nrows = min(kFeatRows, p.N - r0);
+    const uint16_t* blk = p.feat + static_cast<long long>(r0) * p.D;
+    float* part = p.partial + static_cast<long long>(blockIdx.x) * p.D;
+    if constexpr (VEC) {
+      for (int c = threadIdx.x; c < nchunk; c += 256) {
+        float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+        const uint4* col = reinterpret_cast<const uint4*>(blk) + c;
+#pragma unroll 4
+        for (int rr = 0; rr < nrows; ++rr) {
+          const uint4 v = col[static_cast<long long>(rr) * nchunk];
+          const float s = inv[rr];
+          acc[0] += bf16_lo(v.x) * s; acc[1] += bf16_hi(v.x) * s;
+          acc[2] += bf16_lo(v.y) * s; acc[3] += bf16_hi(v.y) * s;
+          acc[4] += bf16_lo(v.z) * s; acc[5] += bf16_hi(v.z) * s;
+          acc[6] += bf16_lo(v.w) * s; acc[7] += bf16_hi(v.w) * s;
+        }
+        float4* out = reinterpret_cast<float4*>(part + c * 8);
+        out[0] = make_float4(acc[0], acc[1], acc[2], acc[3]);
+        out[1] = make_float4(acc[4], acc[5], acc[6], acc[7]);
+      }
+    } else {
+      for (int e = threadIdx.x; e < p.D; e += 256) {
+        float acc = 0.f;
+#pragma unroll 4
+        for (int rr = 0; rr < nrows; ++rr) acc += bf(blk[static_cast<long long>(rr) * p.D + e]) * inv[rr];
+        part[e] = acc;
+      }
+    }
+  } else {
+    const int i = blockIdx.x * 4 + w;
+    if (i >= p.N) return;
+    const float s = p.inv_norm[i];
+    const uint16_t* rowp = p.feat + static_cast<long long>(i) * p.D;
+    float acc = 0.f;
+    if constexpr (VEC) {
+      const uint4* row = reinterpret_cast<const uint4*>(rowp);
+      const float4* ch = reinterpret_cast<const float4*>(p.chat);
+      for (int c = lane; c < nchunk; c += 64) {
+        const uint4 v = row[c];
+        const float4 c0 = ch[2 * c], c1 = ch[2 * c + 1];
+        const float a[8] = {bf16_lo(v.x) * s - c0.x, bf16_hi(v.x) * s - c0.y, bf16_lo(v.y) * s - c0.z,
+                            bf16_hi(v.y) * s - c0.w, bf16_lo(v.z) * s - c1.x, bf16_hi(v.z) * s - c1.y,
+                            bf16_lo(v.w) * s - c1.z, bf16_hi(v.w) * s - c1.w};
+#pragma unroll
+        for (int k = 0; k < 8; ++k) acc += a[k] * a[k];
+      }
+    } else {
+      for (int e = lane; e < p.D; e += 64) {
+        const float a = bf(rowp[e]) * s - p.chat[e];
+        acc += a * a;
+      }
+    }
+    acc = wave_reduce_dpp(acc, FeatAdd{});
+    if (lane == 0) p.d[i] = sqrtf(acc);
   }
 }
 
@@ -712,6 +826,66 @@ pace_status_t pace_apc_density(const uint8_t* img, int H, int W, int patch, doub
   if ((st = check_launch("apc_finalize_c")) != PACE_OK) return st;
   hipLaunchKernelGGL(apc_patch_pass<1>, dim3(p.n_tiles), dim3(kApcThreads), lds, stream, p);
   if ((st = check_launch("apc_patch_pass<1>")) != PACE_OK) return st;
+  hipLaunchKernelGGL(apc_tail, dim3(1), dim3(1024), 0, stream, p);
+  return check_launch("apc_tail");
+}
+
+size_t pace_apc_density_features_workspace_size(int N, int D) {
+  if (N <= 0 || D <= 0) return 0;
+  Sizer s;
+  const int blocks = (N + kFeatRows - 1) / kFeatRows;
+  s.take<float>(N);                                  // inv_norm
+  s.take<float>(static_cast<size_t>(blocks) * D);    // partials
+  s.take<float>(D);                                  // csum
+  s.take<float>(D);                                  // chat
+  s.take<float>(8);                                  // stats
+  s.take<float>(N);                                  // d (when d_out is null)
+  return s.off;
+}
+
+pace_status_t pace_apc_density_features(const uint16_t* feat, int N, int D, double tail_frac,
+                                        float alpha, float gamma, float* d_out, float* rho_out,
+                                        void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  PACE_REQUIRE(feat && rho_out, "pace_apc_density_features: null device pointer");
+  PACE_REQUIRE((reinterpret_cast<uintptr_t>(feat) & 1u) == 0, "pace_apc_density_features: feat must be 2-byte aligned");
+  PACE_REQUIRE(N >= 1 && D >= 1, "pace_apc_density_features: N=%d and D=%d must be >= 1", N, D);
+  PACE_REQUIRE(static_cast<long long>(N) * D < (1ll << 40) && D <= (1 << 20),
+               "pace_apc_density_features: matrix too large");
+  PACE_REQUIRE(tail_frac > 0 && tail_frac <= 1, "pace_apc_density_features: tail_frac must be in (0, 1]");
+  PACE_REQUIRE(gamma > 0.f, "pace_apc_density_features: gamma must be > 0");
+  const size_t need = pace_apc_density_features_workspace_size(N, D);
+  if (workspace == nullptr || workspace_bytes < need)
+    return set_error(PACE_ERR_WORKSPACE, "pace_apc_density_features: workspace %zu < %zu bytes",
+                     workspace_bytes, need);
+  DensityParams p{};
+  p.feat = feat;
+  p.N = N;
+  p.D = D;
+  p.n_tiles = (N + kFeatRows - 1) / kFeatRows;
+  int nt = pace_keep_count(tail_frac, p.N);
+  p.n_tail = nt < 1 ? 1 : nt;
+  p.alpha = alpha; p.gamma = gamma;
+  Carver c(workspace, workspace_bytes);
+  p.inv_norm = c.take<float>(N);
+  p.partial = c.take<float>(static_cast<size_t>(p.n_tiles) * D);
+  p.csum = c.take<float>(D);
+  p.chat = c.take<float>(D);
+  p.stats = c.take<float>(8);
+  float* dws = c.take<float>(N);
+  p.d = d_out ? d_out : dws;
+  p.rho_out = rho_out;
+  const bool vec = D % 8 == 0 && aligned16(feat);
+  if (vec) hipLaunchKernelGGL((apc_feat_pass<0, true>), dim3(p.n_tiles), dim3(256), 0, stream, p);
+  else hipLaunchKernelGGL((apc_feat_pass<0, false>), dim3(p.n_tiles), dim3(256), 0, stream, p);
+  pace_status_t st = check_launch("apc_feat_pass<0>");
+  if (st != PACE_OK) return st;
+  hipLaunchKernelGGL(apc_reduce_c, dim3((p.D + 63) / 64), dim3(1024), 0, stream, p);
+  if ((st = check_launch("apc_reduce_c")) != PACE_OK) return st;
+  hipLaunchKernelGGL(apc_finalize_c, dim3(1), dim3(1024), 0, stream, p);
+  if ((st = check_launch("apc_finalize_c")) != PACE_OK) return st;
+  if (vec) hipLaunchKernelGGL((apc_feat_pass<1, true>), dim3((N + 3) / 4), dim3(256), 0, stream, p);
+  else hipLaunchKernelGGL((apc_feat_pass<1, false>), dim3((N + 3) / 4), dim3(256), 0, stream, p);
+  if ((st = check_launch("apc_feat_pass<1>")) != PACE_OK) return st;
   hipLaunchKernelGGL(apc_tail, dim3(1), dim3(1024), 0, stream, p);
   return check_launch("apc_tail");
 }

@@ -35,6 +35,9 @@ _PROTOS = {
     "pace_apc_density_workspace_size": (c_size, [c_int, c_int, c_int]),
     "pace_apc_density": (c_int, [c_void, c_int, c_int, c_int, c_double, c_float, c_float, c_void,
                                  c_void, c_void, c_size, c_void]),
+    "pace_apc_density_features_workspace_size": (c_size, [c_int, c_int]),
+    "pace_apc_density_features": (c_int, [c_void, c_int, c_int, c_double, c_float, c_float, c_void,
+                                          c_void, c_void, c_size, c_void]),
     "pace_apc_downsample": (c_int, [c_void, c_int, c_int, c_void, c_int, c_int, c_void]),
     "pace_vit_attention_workspace_size": (c_size, [c_int, c_int]),
     "pace_vit_attention": (c_int, [c_void, c_void, c_void, c_int, c_int, c_int, c_void, c_int, c_int,
@@ -138,6 +141,27 @@ def apc_density(img: torch.Tensor, patch: int = 14, tail_frac: float = 0.10, alp
     _check(lib().pace_apc_density(_ptr(img), H, W, patch, float(tail_frac), float(alpha),
                                   float(gamma), _ptr(d_out), _ptr(rho_out), _ptr(workspace),
                                   workspace.numel(), _stream()), "pace_apc_density")
+    return rho_out, d_out
+
+
+def apc_density_features(feat: torch.Tensor, tail_frac: float = 0.10, alpha: float = 0.6,
+                         gamma: float = 1.5, d_out: Optional[torch.Tensor] = None,
+                         rho_out: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None):
+    """feat: bf16 [N, D] preview embeddings on the GPU.  Returns (rho [4] = rho_g, rho_d, rho, phi;
+    d [N])."""
+    if feat.dtype != torch.bfloat16 or feat.dim() != 2:
+        raise PaceError("feat must be a 2-D bfloat16 tensor")
+    N, D = feat.shape
+    dev = feat.device
+    if d_out is None:
+        d_out = torch.empty(N, dtype=torch.float32, device=dev)
+    if rho_out is None:
+        rho_out = torch.empty(4, dtype=torch.float32, device=dev)
+    if workspace is None:
+        workspace = _ws(lib().pace_apc_density_features_workspace_size(N, D), dev)
+    _check(lib().pace_apc_density_features(_ptr(feat), N, D, float(tail_frac), float(alpha),
+                                           float(gamma), _ptr(d_out), _ptr(rho_out), _ptr(workspace),
+                                           workspace.numel(), _stream()), "pace_apc_density_features")
     return rho_out, d_out
 
 

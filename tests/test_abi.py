@@ -114,6 +114,14 @@ def test_errors_before_launch():
     assert st == 1
     st = L.pace_apc_downsample(fake, 10, 10, fake, 11, 10, None)
     assert st == 1
+    # APC on embeddings: empty, odd address, workspace too small
+    st = L.pace_apc_density_features(fake, 100, 0, 0.1, 0.6, 1.5, None, fake, fake, 1 << 30, None)
+    assert st == 1
+    st = L.pace_apc_density_features(ctypes.c_void_p(0x1001), 100, 16, 0.1, 0.6, 1.5, None, fake, fake,
+                                     1 << 30, None)
+    assert st == 1
+    st = L.pace_apc_density_features(fake, 100, 16, 0.1, 0.6, 1.5, None, fake, fake, 16, None)
+    assert st == 3
     st = L.pace_apc_downsample(fake, 1000, 1000, fake, 10, 10, None)
     assert st == 2
 

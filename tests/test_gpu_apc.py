@@ -110,3 +110,48 @@ def test_resize_rejects_shrink_beyond_32x():
     img = wl.make_image(3, 64, 64)
     with pytest.raises(pace.PaceError, match="shrink factor"):
         pace.apc_downsample(dev_u8(img), 1, 1)
+
+
+# ---------------------------------------------------------------- caller-supplied embeddings
+def _check_features(bits, tail=0.1, atol=1e-4):
+    from paper_2608_27206_amd import pace
+    import torch
+    from tests.gpu_util import dev_bf16
+    say(f"apc density features {bits.shape}")
+    rho, d = pace.apc_density_features(dev_bf16(bits), tail, 0.6, 1.5)
+    torch.cuda.synchronize()
+    ref = oapc.embedding_density(wl.bf16_bits_to_f64(bits), tail)
+    np.testing.assert_allclose(host(d), ref["d"], atol=atol)
+    np.testing.assert_allclose(host(rho), [ref["rho_g"], ref["rho_d"], ref["rho"], ref["phi"]], atol=atol)
+    return host(rho), host(d)
+
+
+@pytest.mark.parametrize("n,dim", [(3000, 1280), (777, 8), (130, 592), (64, 3584), (500, 3), (257, 100)])
+def test_density_features_random(n, dim):
+    rs = np.random.default_rng(n + dim)
+    x = rs.normal(size=(n, dim)).astype(np.float32) + rs.normal(size=(1, dim)).astype(np.float32)
+    _check_features(wl.f32_to_bf16_bits(x))
+
+
+def test_density_features_of_patch_pixels_match_image_path():
+    """The pixel stand-in features, rounded to bf16 and fed as embeddings."""
+    img = wl.make_image(1, 448, 448)
+    f = oapc.patch_features(img, 14).astype(np.float32)
+    _check_features(wl.f32_to_bf16_bits(f))
+
+
+def test_density_features_opposite_identical_and_zero_rows():
+    rs = np.random.default_rng(6)
+    x = rs.normal(size=(50, 64)).astype(np.float32)
+    x = np.concatenate([x, -x, np.zeros((1, 64), np.float32)])
+    rho, d = _check_features(wl.f32_to_bf16_bits(x))
+    assert abs(rho[0] - 1.0) < 1e-5 and d[100] == 0.0
+    rho, d = _check_features(wl.f32_to_bf16_bits(np.tile(x[:1], (33, 1))))
+    assert abs(rho[3] - 1.0) < 1e-5 and np.max(d) < 1e-3
+
+
+def test_density_features_beyond_the_register_tail():
+    """More rows than the tail kernel holds in registers (49,152): the tail re-reads d."""
+    rs = np.random.default_rng(8)
+    x = rs.normal(size=(50000, 16)).astype(np.float32)
+    _check_features(wl.f32_to_bf16_bits(x))
