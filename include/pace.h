@@ -25,8 +25,11 @@
  *     scaled logits).
  *   - On bad arguments a call returns an error status WITHOUT launching
  *     anything; pace_last_error() then returns a message (thread-local).
- *   - Device-side metadata (cu_seqlens and the like) is trusted: it must be
- *     monotone and consistent with the host-side maxima passed alongside it.
+ *   - Device-side metadata (cu_seqlens, vis_len, cu_vis, mq_start/mq_len, vis_perm) is
+ *     trusted: it must be monotone and consistent with the host-side maxima passed
+ *     alongside it.  With the environment variable PACE_DEBUG=1 every call copies it to
+ *     the host, synchronises the stream and checks it first, returning
+ *     PACE_ERR_INVALID_ARG before any launch when it is inconsistent.
  *   - The library keeps no global mutable state other than the thread-local
  *     error message, so independent calls may run concurrently on different
  *     streams.

@@ -2,6 +2,9 @@
 #include <math.h>
 #include <stdarg.h>
 #include <stdio.h>
+#include <stdlib.h>
+
+#include <vector>
 
 #include "pace_internal.h"
 
@@ -20,6 +23,52 @@ pace_status_t set_error(pace_status_t st, const char* fmt, ...) {
 pace_status_t check_launch(const char* what) {
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return set_error(PACE_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+  return PACE_OK;
+}
+
+bool debug_checks() {
+  const char* e = getenv("PACE_DEBUG");
+  return e != nullptr && e[0] == '1' && e[1] == '\0';
+}
+
+pace_status_t copy_to_host(int32_t* dst, const int32_t* src, int n, hipStream_t stream) {
+  if (n <= 0) return PACE_OK;
+  if (hipMemcpyAsync(dst, src, static_cast<size_t>(n) * sizeof(int32_t), hipMemcpyDeviceToHost, stream) !=
+          hipSuccess ||
+      hipStreamSynchronize(stream) != hipSuccess)
+    return set_error(PACE_ERR_HIP, "metadata copy to the host failed");
+  return PACE_OK;
+}
+
+pace_status_t check_offsets(const int32_t* cu, int n, long long total, int max_len, const char* what,
+                            hipStream_t stream) {
+  if (!debug_checks()) return PACE_OK;
+  std::vector<int32_t> h(static_cast<size_t>(n) + 1);
+  pace_status_t st = copy_to_host(h.data(), cu, n + 1, stream);
+  if (st != PACE_OK) return st;
+  if (h[0] != 0) return set_error(PACE_ERR_INVALID_ARG, "%s: offsets[0] = %d, not 0", what, h[0]);
+  for (int b = 0; b < n; ++b) {
+    const long long len = static_cast<long long>(h[b + 1]) - h[b];
+    if (len < 0 || len > max_len)
+      return set_error(PACE_ERR_INVALID_ARG, "%s: segment %d has length %lld, outside [0, %d]", what, b,
+                       len, max_len);
+  }
+  if (h[n] > total)
+    return set_error(PACE_ERR_INVALID_ARG, "%s: offsets end at %d, past %lld", what, h[n], total);
+  return PACE_OK;
+}
+
+pace_status_t check_values(const int32_t* v, int n, const int32_t* upper_host, int lo, int vmax,
+                           const char* what, hipStream_t stream) {
+  if (!debug_checks()) return PACE_OK;
+  std::vector<int32_t> h(static_cast<size_t>(n));
+  pace_status_t st = copy_to_host(h.data(), v, n, stream);
+  if (st != PACE_OK) return st;
+  for (int b = 0; b < n; ++b) {
+    const int hi = upper_host ? (upper_host[b] < vmax ? upper_host[b] : vmax) : vmax;
+    if (h[b] < lo || h[b] > hi)
+      return set_error(PACE_ERR_INVALID_ARG, "%s[%d] = %d outside [%d, %d]", what, b, h[b], lo, hi);
+  }
   return PACE_OK;
 }
 

@@ -37,6 +37,8 @@
 
 #include <type_traits>
 
+#include <vector>
+
 #include "pace_internal.h"
 
 namespace pace {
@@ -1139,6 +1141,8 @@ pace_status_t pace_vit_attention(const uint16_t* q, const uint16_t* k, const uin
   const long long nkt = (max_seglen + kMassKeys - 1) / kMassKeys;
   PACE_REQUIRE(nqt * nseg * H < (1ll << 31) && 2ll * max_seglen * H * d < (1ll << 31),
                "pace_vit_attention: a segment must span less than 2 GiB of q/k/v");
+  pace_status_t chk = check_offsets(cu_seqlens, nseg, N, max_seglen, "pace_vit_attention: cu_seqlens", stream);
+  if (chk != PACE_OK) return chk;
   float* lse_buf = lse;
   if (mass != nullptr && lse == nullptr) {
     const size_t need = pace_vit_attention_workspace_size(N, H);
@@ -1177,6 +1181,9 @@ pace_status_t pace_vit_attention_mass(const uint16_t* q, const uint16_t* k, int 
   const long long nkt = (max_seglen + kMassKeys - 1) / kMassKeys;
   PACE_REQUIRE(nkt * nseg * H < (1ll << 31) && 2ll * max_seglen * H * d < (1ll << 31),
                "pace_vit_attention_mass: a segment must span less than 2 GiB of q/k");
+  pace_status_t chk = check_offsets(cu_seqlens, nseg, N, max_seglen, "pace_vit_attention_mass: cu_seqlens",
+                                    stream);
+  if (chk != PACE_OK) return chk;
   MassParams mp{};
   mp.q = q; mp.k = k; mp.lse = lse; mp.mass = mass; mp.cu = cu_seqlens;
   mp.mass_stride = N;
@@ -1221,6 +1228,30 @@ pace_status_t pace_prefill_attention_with_mass(
   const long long nkt = (max_vis_len + kMassKeys - 1) / kMassKeys;
   PACE_REQUIRE(nqt * B * Hq < (1ll << 31) && 2ll * max_seqlen * Hq * d < (1ll << 31),
                "pace_prefill_attention_with_mass: a sequence must span less than 2 GiB of q");
+  if (debug_checks()) {
+    pace_status_t chk = check_offsets(cu_seqlens, B, Ntot, max_seqlen,
+                                      "pace_prefill_attention_with_mass: cu_seqlens", stream);
+    if (chk != PACE_OK) return chk;
+    if (want_mass) {
+      std::vector<int32_t> cu(B + 1), vl(B), cv(B + 1), ms(B), ml(B);
+      if ((chk = copy_to_host(cu.data(), cu_seqlens, B + 1, stream)) != PACE_OK ||
+          (chk = copy_to_host(vl.data(), vis_len, B, stream)) != PACE_OK ||
+          (chk = copy_to_host(cv.data(), cu_vis, B + 1, stream)) != PACE_OK ||
+          (chk = copy_to_host(ms.data(), mq_start, B, stream)) != PACE_OK ||
+          (chk = copy_to_host(ml.data(), mq_len, B, stream)) != PACE_OK)
+        return chk;
+      PACE_REQUIRE(cv[0] == 0 && cv[B] <= nvis_total, "pace_prefill_attention_with_mass: cu_vis range");
+      for (int b = 0; b < B; ++b) {
+        const int L = cu[b + 1] - cu[b];
+        PACE_REQUIRE(vl[b] >= 0 && vl[b] <= L && vl[b] <= max_vis_len && cv[b + 1] - cv[b] == vl[b],
+                     "pace_prefill_attention_with_mass: sequence %d: vis_len %d, cu_vis step %d, length %d", b,
+                     vl[b], cv[b + 1] - cv[b], L);
+        PACE_REQUIRE(ms[b] >= 0 && ml[b] >= 0 && ml[b] <= max_mq_len && ms[b] + ml[b] <= L,
+                     "pace_prefill_attention_with_mass: sequence %d: query rows [%d, %d + %d) outside [0, %d]",
+                     b, ms[b], ms[b], ml[b], L);
+      }
+    }
+  }
   float* lse_buf = lse;
   if (lse == nullptr) {
     const size_t need = pace_prefill_attention_workspace_size(Ntot, Hq);

@@ -19,6 +19,8 @@
 // from memory in every pass) and gather_rows.
 #include <math.h>
 
+#include <vector>
+
 #include "pace_internal.h"
 
 namespace pace {
@@ -797,6 +799,15 @@ pace_status_t pace_ddae_select_varlen(const float* vis_mass, int Hv, int merge,
   if (workspace == nullptr || workspace_bytes < need)
     return set_error(PACE_ERR_WORKSPACE, "pace_ddae_select: workspace %zu < %zu bytes",
                      workspace_bytes, need);
+  if (vis_perm != nullptr && debug_checks()) {
+    std::vector<int32_t> perm(nv_total);
+    pace_status_t chk = copy_to_host(perm.data(), vis_perm, nv_total, stream);
+    if (chk != PACE_OK) return chk;
+    for (int b = 0; b < B; ++b)
+      for (int i = p.cu_nv[b]; i < p.cu_nv[b + 1]; ++i)
+        PACE_REQUIRE(perm[i] >= 0 && perm[i] < nv_host[b],
+                     "pace_ddae_select: vis_perm[%d] = %d outside [0, %d) for image %d", i, perm[i], nv_host[b], b);
+  }
   Carver c(workspace, workspace_bytes);
   p.part = c.take<MapPartial>((nv_total + kMapTokens - 1) / kMapTokens + B);
   p.vraw = c.take<float>(nv_total);

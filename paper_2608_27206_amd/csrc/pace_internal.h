@@ -14,6 +14,21 @@ namespace pace {
 pace_status_t set_error(pace_status_t st, const char* fmt, ...);
 pace_status_t check_launch(const char* what);
 
+// Validation of device-side metadata, done only when the environment variable PACE_DEBUG
+// is "1" (it copies the arrays to the host and synchronises the stream).  Each returns
+// PACE_OK when checks are off or pass, PACE_ERR_INVALID_ARG with a message otherwise.
+bool debug_checks();
+// Segment offsets cu [n + 1]: cu[0] = 0, nondecreasing, cu[n] <= total, every segment at
+// most max_len long.
+pace_status_t check_offsets(const int32_t* cu, int n, long long total, int max_len, const char* what,
+                            hipStream_t stream);
+// Per-segment values v [n] within [lo, hi_b] where hi_b = upper[b] (or hi when upper is null)
+// and at most vmax.
+pace_status_t check_values(const int32_t* v, int n, const int32_t* upper_host, int lo, int vmax,
+                           const char* what, hipStream_t stream);
+// Copies n ints from the device (synchronous on the stream).
+pace_status_t copy_to_host(int32_t* dst, const int32_t* src, int n, hipStream_t stream);
+
 #define PACE_REQUIRE(cond, ...)                                   \
   do {                                                            \
     if (!(cond)) return ::pace::set_error(PACE_ERR_INVALID_ARG, __VA_ARGS__); \
