@@ -14,8 +14,10 @@ Modules:
              per-key attention mass that Section 3.3 reads out as S_vis / S_llm.
   ddae       Section 3.3 (Extract): min-max maps, std confidences, softmax
              fusion, top-K ranking and the gather of the kept tokens.
+  preview    Section 3.2's shallow feature preview: one vision-encoder block (patch
+             embedding, window attention, SwiGLU MLP) with seeded weights.
 
 Every function is pinned by the CPU tests (tests/test_oracle_*.py) against
 closed forms, invariants, brute force on tiny inputs or library routines.
 """
-from . import apc, attention, ddae  # noqa: F401
+from . import apc, attention, ddae, preview  # noqa: F401

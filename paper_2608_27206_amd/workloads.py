@@ -273,6 +273,30 @@ def random_bf16(seed: int, shape, scale: float = 1.0) -> np.ndarray:
     return f32_to_bf16_bits(_normal_bf16(1000 + seed, 0, shape, scale))
 
 
+def preview_weights(seed: int, dim: int = 1280, ffn: int = 3420, patch: int = 14) -> dict:
+    """Seeded weights of a vision-encoder block of Qwen2.5-VL-7B's shapes (the APC preview):
+    bf16 bit arrays for the matrices (N(0,1)/sqrt(fan_in)), fp32 for biases (N(0, 0.02)) and
+    RMSNorm gains (1 + N(0, 0.1)).  Only random numbers, no arithmetic of the method."""
+    g = np.random.default_rng([seed, 77])
+    kin = 3 * patch * patch
+
+    def mat(n, k):
+        return f32_to_bf16_bits((g.standard_normal((n, k)) / np.sqrt(k)).astype(np.float32))
+
+    def vec(n, scale):
+        return (g.standard_normal(n) * scale).astype(np.float32)
+
+    w = {"pe": mat(dim, kin), "g1": (1.0 + vec(dim, 0.1)).astype(np.float32)}
+    for name in ("q", "k", "v", "o"):
+        w["w" + name] = mat(dim, dim)
+        w["b" + name] = vec(dim, 0.02)
+    w["g2"] = (1.0 + vec(dim, 0.1)).astype(np.float32)
+    w["wg"], w["bg"] = mat(ffn, dim), vec(ffn, 0.02)
+    w["wu"], w["bu"] = mat(ffn, dim), vec(ffn, 0.02)
+    w["wd"], w["bd"] = mat(dim, ffn), vec(dim, 0.02)
+    return w
+
+
 def _hidden(config_id: int, nv: int) -> np.ndarray:
     return f32_to_bf16_bits(_normal_bf16(config_id, S_HIDDEN, (nv, HIDDEN)))
 
