@@ -190,6 +190,7 @@ def main():
             per[n] += ev[n][0].elapsed_time(ev[n][1])
     per = {n: v / a.steps for n, v in per.items()}
     nxt = measure_next(pace, pq, pk, pv, p_cu, S, p_vis, p_cuv, Nv, T, idx, K, stream)
+    nxt["preview_block"] = measure_preview(pace, wl, img, L, stream)
 
     # algorithmic work
     win_sizes = np.diff(vit.cu_windows).astype(np.float64)
@@ -302,6 +303,48 @@ def measure_next(pace, pq, pk, pv, p_cu, S, p_vis, p_cuv, Nv, T, idx, K, stream,
                                "tflops_post": round(flop_post / (t_post * 1e-3) / 1e12, 1) if t_post > 0 else None,
                                "tflops_full": round(flop_full / (t_full * 1e-3) / 1e12, 1) if t_full > 0 else None},
     }
+
+
+def measure_preview(pace, wl, img, L, stream, reps=3):
+    """Outside the timed step: APC's shallow preview (the vision encoder's first block with seeded
+    weights, at the original resolution) on the same image, then the density of its embeddings."""
+    import numpy as np
+    import torch
+
+    dev = img.device
+    w = wl.preview_weights(3)
+    wdev = pace.preview_weights_to_device(w, dev)
+    f_alg = int(w["wg"].shape[0])   # hidden units of the block (the device copy pads to a multiple of 8)
+    order = torch.from_numpy(L.order.astype(np.int32)).to(dev)
+    cu = torch.from_numpy(L.cu_windows.astype(np.int32)).to(dev)
+    maxw = int(np.max(L.window_sizes))
+    N = int(L.order.shape[0])
+    D, F = wdev["dim"], wdev["ffn"]
+    out = torch.empty((N, D), dtype=torch.bfloat16, device=dev)
+    ws = torch.empty(pace.lib().pace_apc_preview_workspace_size(N, D, F, 14), dtype=torch.uint8, device=dev)
+    rho = torch.empty(4, dtype=torch.float32, device=dev)
+    dd = torch.empty(N, dtype=torch.float32, device=dev)
+    wsd = torch.empty(pace.lib().pace_apc_density_features_workspace_size(N, D), dtype=torch.uint8, device=dev)
+
+    def timed(fn):
+        fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps
+
+    t_block = timed(lambda: pace.apc_preview(img, 14, order, cu, maxw, wdev, out=out, workspace=ws))
+    t_dens = timed(lambda: pace.apc_density_features(out, d_out=dd, rho_out=rho, workspace=wsd))
+    win = np.diff(L.cu_windows).astype(np.float64)
+    flop = 2.0 * N * D * (3 * 14 * 14 + 4 * D + 3 * f_alg) + 4.0 * 80 * (D // 80) * float(np.sum(win ** 2))
+    return {"ms": round(t_block, 4), "tflops": round(flop / (t_block * 1e-3) / 1e12, 1), "patches": N,
+            "dim": D, "ffn": F, "density_features_ms": round(t_dens, 4),
+            "note": "seeded-weight first vision block at the original resolution (patch embedding, "
+                    "window attention, SwiGLU MLP) + APC density of its embeddings"}
 
 
 def cpu_baseline(vit, budget_s: float):

@@ -135,6 +135,64 @@ pace_status_t pace_apc_density_features(const uint16_t* feat, int N, int D, doub
                                         void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
+ * Weights of the APC preview block (caller-owned device memory; bf16 matrices are row-major
+ * [out, in], fp32 vectors).  dim D is a multiple of 80 (heads of 80 values); ffn F a multiple
+ * of 8 (pad with zero hidden units: zero gate/up rows and zero down columns leave the block
+ * unchanged).
+ */
+typedef struct pace_preview_weights {
+  const uint16_t* pe;             /* [D, Kp] patch embedding, Kp = 3*patch^2 rounded up to a
+                                     multiple of 8 (zero columns past 3*patch^2) */
+  const float* g1;                /* [D] first RMSNorm gain */
+  const uint16_t* wq, *wk, *wv;   /* [D, D] */
+  const float* bq, *bk, *bv;      /* [D] or NULL */
+  const uint16_t* wo;             /* [D, D] */
+  const float* bo;                /* [D] or NULL */
+  const float* g2;                /* [D] second RMSNorm gain */
+  const uint16_t* wgu;            /* [2F, D]: rows 2f and 2f+1 are hidden unit f's gate and up rows */
+  const float* bgu;               /* [2F] or NULL, same interleaving */
+  const uint16_t* wd;             /* [D, F] */
+  const float* bd;                /* [D] or NULL */
+  int dim, ffn;                   /* D and F */
+} pace_preview_weights;
+
+/* Workspace bytes for pace_apc_preview (N patches). */
+size_t pace_apc_preview_workspace_size(int N, int dim, int ffn, int patch);
+
+/*
+ * APC's shallow feature preview (Section 3.2: the vision encoder's initial block, K = 1, at the
+ * original resolution), the embeddings that pace_apc_density_features scores:
+ *   h0  = X W_pe^T, X the patch pixels mapped to x/127.5 - 1 (component order: patch row,
+ *         pixel column, channel), one row per token;
+ *   h1  = h0 + W_o A(RMSNorm_1(h0)) + b_o, A = softmax attention inside each window, heads of
+ *         80 values, scale 1/sqrt(80), q/k/v = W_{q,k,v} RMSNorm_1(h0) + b_{q,k,v};
+ *   out = h1 + W_d (silu(gate) * up) + b_d, (gate, up) = W_gu RMSNorm_2(h1) + b_gu;
+ *   RMSNorm(x) = x / sqrt(mean(x^2) + 1e-6) * g.  No rotary position encoding.
+ * Activations are stored in bf16 between the steps; products accumulate in fp32.
+ *   img         uint8 [H, W, 3]; H and W multiples of patch (1..16); N = (H/patch)*(W/patch).
+ *   token_patch int32 [N] (device): raster index of the patch that token t holds (the encoder's
+ *               window-major order); cu_windows int32 [nwin+1] (device): windows as
+ *               consecutive token ranges, each at most max_window tokens.
+ *   out         bf16 [N, D], 16-byte aligned.
+ */
+pace_status_t pace_apc_preview(const uint8_t* img, int H, int W, int patch, const int32_t* token_patch,
+                               const int32_t* cu_windows, int nwin, int max_window,
+                               const pace_preview_weights* w, uint16_t* out, void* workspace,
+                               size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * The preview's dense products (exposed for reuse and testing): C = A B^T with A bf16 [M, K],
+ * B bf16 [N, K] (row-major, 16-byte aligned, K a positive multiple of 8, each under 1 GiB),
+ * fp32 accumulation,
+ * bf16 out, and one fused epilogue:
+ *   0: C [M, N] = A B^T + bias (bias fp32 [N] or NULL)
+ *   1: C [M, N] = A B^T + bias + residual (residual bf16 [M, N])
+ *   2: C [M, N/2]: column f = silu(g) * u with g, u = columns 2f, 2f+1 of A B^T + bias (N even)
+ */
+pace_status_t pace_gemm_bf16(const uint16_t* A, const uint16_t* B, const float* bias, const uint16_t* residual,
+                             uint16_t* C, int M, int N, int K, int epilogue, hipStream_t stream);
+
+/*
  * APC resize (Appendix implementation details: bicubic resize of both sides).
  *   src uint8 [H, W, 3] -> dst uint8 [oH, oW, 3], with 1 <= oH <= H and 1 <= oW <= W.
  * Separable Keys cubic (a = -0.5); when shrinking, the kernel is stretched by the

@@ -17,7 +17,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "libpace.so")
 BUILD = os.path.join(HERE, "_build")
-SOURCES = ["abi.cpp", "apc.hip", "attention.hip", "ddae.hip"]
+SOURCES = ["abi.cpp", "apc.hip", "attention.hip", "ddae.hip", "preview.hip"]
 ARCH = "gfx950"
 # Packed-FP32 instructions are switched off for all device code.
 DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]

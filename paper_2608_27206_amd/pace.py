@@ -39,6 +39,10 @@ _PROTOS = {
     "pace_apc_density_features": (c_int, [c_void, c_int, c_int, c_double, c_float, c_float, c_void,
                                           c_void, c_void, c_size, c_void]),
     "pace_apc_downsample": (c_int, [c_void, c_int, c_int, c_void, c_int, c_int, c_void]),
+    "pace_apc_preview_workspace_size": (c_size, [c_int, c_int, c_int, c_int]),
+    "pace_apc_preview": (c_int, [c_void, c_int, c_int, c_int, c_void, c_void, c_int, c_int, c_void, c_void,
+                                 c_void, c_size, c_void]),
+    "pace_gemm_bf16": (c_int, [c_void, c_void, c_void, c_void, c_void, c_int, c_int, c_int, c_int, c_void]),
     "pace_vit_attention_workspace_size": (c_size, [c_int, c_int]),
     "pace_vit_attention": (c_int, [c_void, c_void, c_void, c_int, c_int, c_int, c_void, c_int, c_int,
                                    c_float, c_void, c_void, c_void, c_void, c_size, c_void]),
@@ -163,6 +167,83 @@ def apc_density_features(feat: torch.Tensor, tail_frac: float = 0.10, alpha: flo
                                            float(gamma), _ptr(d_out), _ptr(rho_out), _ptr(workspace),
                                            workspace.numel(), _stream()), "pace_apc_density_features")
     return rho_out, d_out
+
+
+class PreviewWeights(ctypes.Structure):
+    """Mirror of pace_preview_weights (include/pace.h)."""
+    _fields_ = [("pe", c_void), ("g1", c_void), ("wq", c_void), ("wk", c_void), ("wv", c_void),
+                ("bq", c_void), ("bk", c_void), ("bv", c_void), ("wo", c_void), ("bo", c_void),
+                ("g2", c_void), ("wgu", c_void), ("bgu", c_void), ("wd", c_void), ("bd", c_void),
+                ("dim", c_int), ("ffn", c_int)]
+
+
+def preview_weights_to_device(w: dict, device) -> dict:
+    """Device copies of preview-block weights in the layout pace_apc_preview reads: bf16 bit
+    arrays (uint16) and fp32 vectors as given; the patch embedding zero-padded to a multiple of
+    8 columns, the hidden units zero-padded to a multiple of 8, gate and up rows interleaved.
+    (Marshalling only: zero padding and row order leave the block's function unchanged.)"""
+    import numpy as np
+
+    def bf(a):
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).to(device)
+
+    def f32(a):
+        return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(device)
+
+    D, kin = w["pe"].shape
+    F = w["wg"].shape[0]
+    kp = (kin + 7) // 8 * 8
+    F8 = (F + 7) // 8 * 8
+    pe = np.zeros((D, kp), np.uint16)
+    pe[:, :kin] = w["pe"]
+    wgu = np.zeros((2 * F8, D), np.uint16)
+    wgu[0:2 * F:2] = w["wg"]
+    wgu[1:2 * F:2] = w["wu"]
+    bgu = np.zeros(2 * F8, np.float32)
+    bgu[0:2 * F:2] = w["bg"]
+    bgu[1:2 * F:2] = w["bu"]
+    wd = np.zeros((D, F8), np.uint16)
+    wd[:, :F] = w["wd"]
+    out = {"pe": bf(pe), "wgu": bf(wgu), "bgu": f32(bgu), "wd": bf(wd), "dim": D, "ffn": F8}
+    for k in ("wq", "wk", "wv", "wo"):
+        out[k] = bf(w[k])
+    for k in ("g1", "g2", "bq", "bk", "bv", "bo", "bd"):
+        out[k] = f32(w[k])
+    return out
+
+
+def apc_preview(img: torch.Tensor, patch: int, token_patch: torch.Tensor, cu_windows: torch.Tensor,
+                max_window: int, wdev: dict, out: Optional[torch.Tensor] = None,
+                workspace: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """The preview block's token embeddings, bf16 [N, D]; wdev from preview_weights_to_device."""
+    H, W, _ = img.shape
+    N = (H // patch) * (W // patch)
+    D, F = wdev["dim"], wdev["ffn"]
+    dev = img.device
+    if out is None:
+        out = torch.empty((N, D), dtype=torch.bfloat16, device=dev)
+    if workspace is None:
+        workspace = _ws(lib().pace_apc_preview_workspace_size(N, D, F, patch), dev)
+    pw = PreviewWeights(*(_ptr(wdev[k]) for k in ("pe", "g1", "wq", "wk", "wv", "bq", "bk", "bv", "wo", "bo",
+                                                  "g2", "wgu", "bgu", "wd", "bd")), D, F)
+    nwin = cu_windows.numel() - 1
+    _check(lib().pace_apc_preview(_ptr(img), H, W, patch, _ptr(token_patch), _ptr(cu_windows), nwin,
+                                  int(max_window), ctypes.byref(pw), _ptr(out), _ptr(workspace),
+                                  workspace.numel(), _stream()), "pace_apc_preview")
+    return out
+
+
+def gemm_bf16(a: torch.Tensor, b: torch.Tensor, bias: Optional[torch.Tensor] = None,
+              residual: Optional[torch.Tensor] = None, epilogue: int = 0,
+              out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """C = a b^T (+ bias, + residual, or SwiGLU of interleaved columns); a [M, K], b [N, K] bf16."""
+    M, K = a.shape
+    N = b.shape[0]
+    if out is None:
+        out = torch.empty((M, N // 2 if epilogue == 2 else N), dtype=torch.bfloat16, device=a.device)
+    _check(lib().pace_gemm_bf16(_ptr(a), _ptr(b), _ptr(bias), _ptr(residual), _ptr(out), M, N, K, int(epilogue),
+                                _stream()), "pace_gemm_bf16")
+    return out
 
 
 def apc_downsample(src: torch.Tensor, oH: int, oW: int, dst: Optional[torch.Tensor] = None):
