@@ -202,3 +202,42 @@ def test_topk_many_rows_per_workgroup():
     S = rs.random(16000).astype(np.float32)
     S[5000:9000] = 0.5   # a long run of ties at the threshold
     _topk_case(S, 8000, wl.random_bf16(21, (16000, 48)))
+
+
+def test_per_tile_and_global_selection():
+    """InternVL-style tiles (the cross-model study): "-T" keeps ceil(ratio * n) tokens inside
+    each tile (one segment per tile), "-G" keeps the same total over all tiles' tokens at once
+    (one segment).  Both against the oracle rule."""
+    from paper_2608_27206_amd import pace
+    import torch
+    rs = np.random.default_rng(31)
+    tiles = [256] * 6 + [256]          # six 448x448 tiles and the thumbnail, 256 tokens each
+    nt = sum(tiles)
+    vis = rs.gamma(0.5, size=(16, nt)).astype(np.float32)
+    llm = rs.gamma(0.3, size=(28, nt)).astype(np.float32)
+    hidden = wl.random_bf16(31, (nt, 128))
+    per = [oddae.keep_count(0.1, n) for n in tiles]
+    idx_t, sc_t, _, out_t = pace.ddae_select(dev_f32(vis), 1, None, dev_f32(llm), tiles, per,
+                                             hidden=dev_bf16(hidden))
+    idx_g, sc_g, _, out_g = pace.ddae_select(dev_f32(vis), 1, None, dev_f32(llm), [nt], [sum(per)],
+                                             hidden=dev_bf16(hidden))
+    torch.cuda.synchronize()
+    # -T: every tile keeps exactly its own share, chosen by its own normalised scores
+    got_t = host(idx_t)
+    off = koff = 0
+    for n, K in zip(tiles, per):
+        S_ref, _ = oddae.fuse(vis[:, off:off + n].astype(np.float64), llm[:, off:off + n].astype(np.float64), 1,
+                              None, 0)
+        part = got_t[koff:koff + K] - off
+        assert np.all((part >= 0) & (part < n))
+        ok, msg = kept_sets_agree(part, oddae.topk_indices(S_ref, K), S_ref)
+        assert ok, msg
+        off += n
+        koff += K
+    # -G: one ranking over all tiles; the per-tile counts follow the scores
+    S_g, _ = oddae.fuse(vis.astype(np.float64), llm.astype(np.float64), 1, None, 0)
+    ok, msg = kept_sets_agree(host(idx_g), oddae.topk_indices(S_g, sum(per)), S_g)
+    assert ok, msg
+    import torch as t
+    np.testing.assert_array_equal(out_t.view(t.int16).cpu().numpy().view(np.uint16), hidden[got_t])
+    np.testing.assert_array_equal(out_g.view(t.int16).cpu().numpy().view(np.uint16), hidden[host(idx_g)])
