@@ -151,6 +151,97 @@ def embedding_density(x: np.ndarray, tail_frac: float = TAIL_FRAC, alpha: float 
             "d_top": d_top, "c_hat": c_hat}
 
 
+# ---------------------------------------------------------------- pixel-statistic previews
+# The preview ablation replaces the shallow ViT feature with four training-free pixel statistics
+# (RGB statistics, colour entropy, edge density, Laplacian) without defining them.  Readings
+# (listed in the design notes): each is a vector per patch, so that the cosine-based density
+# steps apply unchanged (a scalar per patch would make every cosine +-1):
+#   0 RGB statistics  mean and population std of each channel of x/255      (6 values)
+#   1 colour entropy  -p_k ln p_k for the 64 colours of 4 levels per channel (64 values; their
+#                     sum is the patch's colour entropy)
+#   2 edge density    Sobel gradient magnitude of the grey image summed per orientation octant,
+#                     divided by 255 * patch^2                             (8 values)
+#   3 Laplacian       the 4-neighbour Laplacian of the grey image / 255     (patch^2 values)
+# Grey = (299 R + 587 G + 114 B) / 1000; gradients and the Laplacian take neighbours across patch
+# borders, with the image edge clamped.  The octant of a gradient (gx, gy) is decided exactly
+# from integers: 0 for angles in [0, 45) degrees, 1 for [45, 90), ..., counter-clockwise with
+# y pointing down the image rows; the zero gradient falls in octant 0 with magnitude 0.
+PIXEL_FEATURE_DIMS = {0: lambda P: 6, 1: lambda P: 64, 2: lambda P: 8, 3: lambda P: P * P}
+
+
+def _grey1000(img: np.ndarray) -> np.ndarray:
+    """1000 x the grey value: the exact integer 299 R + 587 G + 114 B."""
+    x = img.astype(np.int64)
+    return 299 * x[..., 0] + 587 * x[..., 1] + 114 * x[..., 2]
+
+
+def _octant(gx: np.ndarray, gy: np.ndarray) -> np.ndarray:
+    """Octant index 0..7 of the angle atan2(gy, gx) in [0, 360) degrees, from exact comparisons."""
+    ax, ay = np.abs(gx), np.abs(gy)
+    oct_ = np.zeros(gx.shape, dtype=np.int64)
+    up = gy >= 0
+    # quadrant I (gx > 0, gy >= 0): 0 if ay < ax else 1; II (gx <= 0, gy > 0): 2 if ax <= ay else 3;
+    # III (gx < 0, gy <= 0): 4 if ay < ax else 5; IV (gx >= 0, gy < 0): 6 if ax <= ay else 7
+    q1 = (gx > 0) & up
+    q2 = (gx <= 0) & (gy > 0)
+    q3 = (gx < 0) & (gy <= 0)
+    q4 = (gx >= 0) & (gy < 0)
+    oct_[q1] = np.where(ay[q1] < ax[q1], 0, 1)
+    oct_[q2] = np.where(ax[q2] <= ay[q2], 2, 3)
+    oct_[q3] = np.where(ay[q3] < ax[q3], 4, 5)
+    oct_[q4] = np.where(ax[q4] <= ay[q4], 6, 7)
+    return oct_
+
+
+def pixel_statistic_features(img: np.ndarray, patch: int, kind: int) -> np.ndarray:
+    """Per-patch pixel-statistic feature vectors [N, dim], patches in raster order."""
+    H, W, _ = img.shape
+    gh, gw = H // patch, W // patch
+    img = img[: gh * patch, : gw * patch]
+    N = gh * gw
+
+    def per_patch(a):   # [H, W, ...] -> [N, patch*patch, ...]
+        a = a.reshape((gh, patch, gw, patch) + a.shape[2:])
+        a = np.moveaxis(a, 2, 1)
+        return a.reshape((N, patch * patch) + a.shape[4:])
+
+    if kind == 0:
+        x = per_patch(img.astype(np.float64) / 255.0)          # [N, P*P, 3]
+        return np.concatenate([x.mean(axis=1), x.std(axis=1)], axis=1)
+    if kind == 1:
+        q = img.astype(np.int64) // 64                          # 4 levels per channel
+        colour = per_patch(q[..., 0] * 16 + q[..., 1] * 4 + q[..., 2])
+        feats = np.zeros((N, 64))
+        for i in range(N):
+            p = np.bincount(colour[i], minlength=64) / float(patch * patch)
+            nz = p > 0
+            feats[i, nz] = -p[nz] * np.log(p[nz])
+        return feats
+    # gradients and the Laplacian on 1000 x grey: exact integers, so the octants are exact
+    pi = np.pad(_grey1000(img), 1, mode="edge")
+    if kind == 3:
+        lap = 4 * pi[1:-1, 1:-1] - pi[:-2, 1:-1] - pi[2:, 1:-1] - pi[1:-1, :-2] - pi[1:-1, 2:]
+        return per_patch(lap / 255000.0)
+    if kind == 2:
+        gx = (pi[:-2, 2:] + 2 * pi[1:-1, 2:] + pi[2:, 2:]) - (pi[:-2, :-2] + 2 * pi[1:-1, :-2] + pi[2:, :-2])
+        gy = (pi[2:, :-2] + 2 * pi[2:, 1:-1] + pi[2:, 2:]) - (pi[:-2, :-2] + 2 * pi[:-2, 1:-1] + pi[:-2, 2:])
+        mag = np.sqrt(gx.astype(np.float64) ** 2 + gy.astype(np.float64) ** 2) / 1000.0
+        o = per_patch(_octant(gx, gy))
+        m = per_patch(mag)
+        feats = np.zeros((N, 8))
+        for k in range(8):
+            feats[:, k] = np.where(o == k, m, 0.0).sum(axis=1)
+        return feats / (255.0 * patch * patch)
+    raise ValueError(f"unknown pixel statistic {kind}")
+
+
+def pixel_density(img: np.ndarray, patch: int, kind: int, tail_frac: float = TAIL_FRAC,
+                  alpha: float = ALPHA, gamma: float = GAMMA) -> dict:
+    """APC scores with a pixel-statistic preview: the density steps of embedding_density over
+    pixel_statistic_features (a zero feature vector is a zero direction)."""
+    return embedding_density(pixel_statistic_features(img, patch, kind), tail_frac, alpha, gamma)
+
+
 def apc_density(img: np.ndarray, patch: int = 14, tail_frac: float = TAIL_FRAC,
                 alpha: float = ALPHA, gamma: float = GAMMA) -> dict:
     """APC density of a uint8 HWC image, with the pixel stand-in feature."""

@@ -209,3 +209,71 @@ def test_embedding_density_opposite_rows_and_zero_row():
     # identical rows: phi = 1 and every distance is 0
     s = apc.embedding_density(np.tile(rs.normal(size=(1, 16)), (20, 1)))
     assert abs(s["phi"] - 1.0) < 1e-12 and np.max(s["d"]) < 1e-7
+
+
+# ---------------------------------------------------------------- pixel-statistic previews
+def test_pixel_statistics_shapes_and_closed_forms():
+    rs = np.random.default_rng(9)
+    img = rs.integers(0, 256, size=(28, 42, 3), dtype=np.uint8)
+    for kind, dim in ((0, 6), (1, 64), (2, 8), (3, 196)):
+        f = apc.pixel_statistic_features(img, 14, kind)
+        assert f.shape == (6, dim)
+    # RGB statistics: a patch of one colour has that colour's mean and zero spread
+    flat = np.zeros((14, 14, 3), np.uint8)
+    flat[...] = (10, 200, 255)
+    f = apc.pixel_statistic_features(flat, 14, 0)
+    np.testing.assert_allclose(f[0], [10 / 255, 200 / 255, 1.0, 0, 0, 0], atol=1e-14)
+    # colour entropy: the terms of a patch sum to its entropy; half black half white -> ln 2
+    half = np.zeros((14, 14, 3), np.uint8)
+    half[:7] = 255
+    e = apc.pixel_statistic_features(half, 14, 1)[0]
+    assert abs(e.sum() - math.log(2)) < 1e-15 and np.count_nonzero(e) == 2
+    # one colour: zero entropy; Laplacian and edges vanish on a constant image
+    assert np.all(apc.pixel_statistic_features(flat, 14, 1) == 0)
+    assert np.all(apc.pixel_statistic_features(flat, 14, 3) == 0)
+    assert np.all(apc.pixel_statistic_features(flat, 14, 2) == 0)
+
+
+def test_pixel_statistics_edges_and_laplacian_by_hand():
+    """A vertical step edge: Sobel gx = 4 * step at the two columns beside it (grey scaled by
+    1000), gy = 0, so all magnitude lands in octant 0 (gradient pointing +x) and the octant-0
+    total is 2 columns * 14 rows * 4 * step / (255 * 196).  The Laplacian is +-step/255 beside
+    the edge."""
+    img = np.zeros((14, 14, 3), np.uint8)
+    img[:, 7:] = 100                       # grey 100 on the right
+    e = apc.pixel_statistic_features(img, 14, 2)[0]
+    assert abs(e[0] - 2 * 14 * 4 * 100 / (255 * 196)) < 1e-12 and np.all(e[1:] == 0)
+    lap = apc.pixel_statistic_features(img, 14, 3)[0].reshape(14, 14)
+    np.testing.assert_allclose(lap[:, 6], -100 / 255, atol=1e-12)
+    np.testing.assert_allclose(lap[:, 7], 100 / 255, atol=1e-12)
+    assert np.all(lap[:, :6] == 0) and np.all(lap[:, 8:] == 0)
+    # the mirrored edge points the other way: octant 4
+    e2 = apc.pixel_statistic_features(img[:, ::-1].copy(), 14, 2)[0]
+    assert e2[4] > 0 and np.count_nonzero(e2) == 1
+
+
+def test_pixel_statistics_octants_against_atan2():
+    rs = np.random.default_rng(10)
+    gx = rs.integers(-50, 51, size=5000)
+    gy = rs.integers(-50, 51, size=5000)
+    o = apc._octant(gx, gy)
+    ang = np.degrees(np.arctan2(gy, gx)) % 360.0
+    away = np.abs(ang / 45.0 - np.round(ang / 45.0)) > 1e-9     # not on a boundary
+    np.testing.assert_array_equal(o[away], np.floor(ang[away] / 45.0).astype(np.int64))
+    assert apc._octant(np.array([0]), np.array([0]))[0] == 0
+
+
+def test_pixel_density_special_cases():
+    """A tiling of one patch makes every preview vector equal: phi = 1, rho_g = 0 and every
+    d_i = 0 (for kinds whose vector is not zero).  A flat image has zero edge and Laplacian
+    vectors: every direction is zero, so phi = 0 and rho_g = 1."""
+    rs = np.random.default_rng(11)
+    tile = rs.integers(0, 256, size=(14, 14, 3), dtype=np.uint8)
+    img = np.tile(tile, (3, 4, 1))
+    for kind in (0, 1):
+        r = apc.pixel_density(img, 14, kind)
+        assert abs(r["phi"] - 1.0) < 1e-12 and np.max(r["d"]) < 1e-7
+    flat = np.full((28, 28, 3), 77, np.uint8)
+    for kind in (2, 3):
+        r = apc.pixel_density(flat, 14, kind)
+        assert r["phi"] == 0.0 and r["rho_g"] == 1.0
