@@ -341,10 +341,18 @@ def measure_preview(pace, wl, img, L, stream, reps=3):
     t_dens = timed(lambda: pace.apc_density_features(out, d_out=dd, rho_out=rho, workspace=wsd))
     win = np.diff(L.cu_windows).astype(np.float64)
     flop = 2.0 * N * D * (3 * 14 * 14 + 4 * D + 3 * f_alg) + 4.0 * 80 * (D // 80) * float(np.sum(win ** 2))
+    H, W = int(img.shape[0]), int(img.shape[1])
+    pixel_ms = {}
+    for name, kind in pace.PIXEL_STATISTICS.items():
+        wsp = torch.empty(pace.lib().pace_apc_pixel_density_workspace_size(H, W, 14, kind), dtype=torch.uint8,
+                          device=dev)
+        pixel_ms[name] = round(timed(lambda: pace.apc_pixel_density(img, kind, 14, d_out=dd, rho_out=rho,
+                                                                    workspace=wsp)), 4)
     return {"ms": round(t_block, 4), "tflops": round(flop / (t_block * 1e-3) / 1e12, 1), "patches": N,
-            "dim": D, "ffn": F, "density_features_ms": round(t_dens, 4),
+            "dim": D, "ffn": F, "density_features_ms": round(t_dens, 4), "pixel_statistic_density_ms": pixel_ms,
             "note": "seeded-weight first vision block at the original resolution (patch embedding, "
-                    "window attention, SwiGLU MLP) + APC density of its embeddings"}
+                    "window attention, SwiGLU MLP) + APC density of its embeddings; the four "
+                    "training-free pixel-statistic previews with their densities"}
 
 
 def cpu_baseline(vit, budget_s: float):

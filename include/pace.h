@@ -135,6 +135,38 @@ pace_status_t pace_apc_density_features(const uint16_t* feat, int N, int D, doub
                                         void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
+ * Pixel-statistic preview vectors (the training-free previews of the preview-network ablation
+ * in Section 4; the paper names them without formulas, so each is read as one vector per
+ * patch that the density steps consume like an embedding).
+ *   img     uint8 [H, W, 3] HWC; H, W positive multiples of patch, patch 1..16.
+ *   kind    0 RGB statistics: mean and population std of each channel of x/255, dim 6
+ *           1 colour entropy: -p_k ln p_k for the 64 colours of 4 levels per channel, dim 64
+ *           2 edge density: Sobel magnitude of the grey image summed per 45-degree
+ *             orientation octant, / (255 * patch^2), dim 8
+ *           3 Laplacian: 4-neighbour Laplacian of the grey image / 255, dim patch^2
+ *           grey = (299 R + 587 G + 114 B) / 1000; neighbours cross patch borders and the image
+ *           edge is clamped.
+ *   out     fp32 [N, dim] row-major, caller-owned, N = (H/patch)*(W/patch), patches in raster
+ *           order; kind 3 components in pixel raster order within the patch.
+ * INVALID_ARG on null pointers, a kind outside 0..3, or bad sizes.  Asynchronous on `stream`.
+ */
+pace_status_t pace_apc_pixel_features(const uint8_t* img, int H, int W, int patch, int kind,
+                                      float* out, hipStream_t stream);
+
+/* Workspace bytes for pace_apc_pixel_density (0 for invalid arguments). */
+size_t pace_apc_pixel_density_workspace_size(int H, int W, int patch, int kind);
+
+/*
+ * APC density with a pixel-statistic preview: pace_apc_pixel_features into the workspace,
+ * then the arithmetic of pace_apc_density_features on those fp32 rows (a zero row is a zero
+ * direction).  Arguments as in pace_apc_pixel_features and pace_apc_density.
+ */
+pace_status_t pace_apc_pixel_density(const uint8_t* img, int H, int W, int patch, int kind,
+                                     double tail_frac, float alpha, float gamma, float* d_out,
+                                     float* rho_out, void* workspace, size_t workspace_bytes,
+                                     hipStream_t stream);
+
+/*
  * Weights of the APC preview block (caller-owned device memory; bf16 matrices are row-major
  * [out, in], fp32 vectors).  dim D is a multiple of 80 (heads of 80 values); ffn F a multiple
  * of 8 (pad with zero hidden units: zero gate/up rows and zero down columns leave the block

@@ -27,6 +27,7 @@ constexpr int kMaxPatch = 16;
 struct DensityParams {
   const uint8_t* img;
   const uint16_t* feat;   // caller-supplied embeddings, bf16 [N, D] (feature entry point)
+  const float* featf;     // fp32 [N, D] (pixel-statistic previews)
   int H, W, P;            // image and patch size
   int gh, gw, N;          // patch grid
   int D;                  // 3 * P * P
@@ -194,23 +195,28 @@ __device__ __forceinline__ float bf16_hi(uint32_t u) { return __uint_as_float(u 
 
 struct FeatAdd { __device__ float operator()(float a, float b) const { return a + b; } };
 
-// VEC: rows are read as 16-byte chunks of 8 values (D a multiple of 8, aligned rows);
-// otherwise value by value.
-template <int PASS, bool VEC>
+// Element access: kFeatBf16Vec reads bf16 rows as 16-byte chunks of 8 values (D a multiple of
+// 8, aligned rows); kFeatBf16 and kFeatF32 read value by value.
+constexpr int kFeatBf16 = 0, kFeatBf16Vec = 1, kFeatF32 = 2;
+
+template <int PASS, int MODE>
 __global__ __launch_bounds__(256) void apc_feat_pass(const DensityParams p) {
+  constexpr bool VEC = MODE == kFeatBf16Vec;
   __shared__ float inv[kFeatRows];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int nchunk = p.D / 8;
-  auto bf = [](uint16_t b) { return __uint_as_float(static_cast<uint32_t>(b) << 16); };
+  auto at = [&](long long idx) -> float {
+    if constexpr (MODE == kFeatF32) return p.featf[idx];
+    else return __uint_as_float(static_cast<uint32_t>(p.feat[idx]) << 16);
+  };
   if (PASS == 0) {
     const int r0 = blockIdx.x * kFeatRows;
     for (int rr = w; rr < kFeatRows; rr += 4) {
       const int i = r0 + rr;
       float ss = 0.f;
       if (i < p.N) {
-        const uint16_t* rowp = p.feat + static_cast<long long>(i) * p.D;
         if constexpr (VEC) {
-          const uint4* row = reinterpret_cast<const uint4*>(rowp);
+          const uint4* row = reinterpret_cast<const uint4*>(p.feat + static_cast<long long>(i) * p.D);
           for (int c = lane; c < nchunk; c += 64) {
             const uint4 v = row[c];
             const float a[8] = {bf16_lo(v.x), bf16_hi(v.x), bf16_lo(v.y), bf16_hi(v.y),
@@ -220,7 +226,7 @@ __global__ __launch_bounds__(256) void apc_feat_pass(const DensityParams p) {
           }
         } else {
           for (int e = lane; e < p.D; e += 64) {
-            const float a = bf(rowp[e]);
+            const float a = at(static_cast<long long>(i) * p.D + e);
             ss += a * a;
           }
         }
@@ -235,12 +241,11 @@ __global__ __launch_bounds__(256) void apc_feat_pass(const DensityParams p) {
     __syncthreads();
     // block partial of sum_i T_i, rows added in index order
     const int nrows = min(kFeatRows, p.N - r0);
-    const uint16_t* blk = p.feat + static_cast<long long>(r0) * p.D;
     float* part = p.partial + static_cast<long long>(blockIdx.x) * p.D;
     if constexpr (VEC) {
       for (int c = threadIdx.x; c < nchunk; c += 256) {
         float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-        const uint4* col = reinterpret_cast<const uint4*>(blk) + c;
+        const uint4* col = reinterpret_cast<const uint4*>(p.feat + static_cast<long long>(r0) * p.D) + c;
 #pragma unroll 4
         for (int rr = 0; rr < nrows; ++rr) {
           const uint4 v = col[static_cast<long long>(rr) * nchunk];
@@ -258,7 +263,7 @@ __global__ __launch_bounds__(256) void apc_feat_pass(const DensityParams p) {
       for (int e = threadIdx.x; e < p.D; e += 256) {
         float acc = 0.f;
 #pragma unroll 4
-        for (int rr = 0; rr < nrows; ++rr) acc += bf(blk[static_cast<long long>(rr) * p.D + e]) * inv[rr];
+        for (int rr = 0; rr < nrows; ++rr) acc += at(static_cast<long long>(r0 + rr) * p.D + e) * inv[rr];
         part[e] = acc;
       }
     }
@@ -266,10 +271,9 @@ __global__ __launch_bounds__(256) void apc_feat_pass(const DensityParams p) {
     const int i = blockIdx.x * 4 + w;
     if (i >= p.N) return;
     const float s = p.inv_norm[i];
-    const uint16_t* rowp = p.feat + static_cast<long long>(i) * p.D;
     float acc = 0.f;
     if constexpr (VEC) {
-      const uint4* row = reinterpret_cast<const uint4*>(rowp);
+      const uint4* row = reinterpret_cast<const uint4*>(p.feat + static_cast<long long>(i) * p.D);
       const float4* ch = reinterpret_cast<const float4*>(p.chat);
       for (int c = lane; c < nchunk; c += 64) {
         const uint4 v = row[c];
@@ -282,13 +286,152 @@ __global__ __launch_bounds__(256) void apc_feat_pass(const DensityParams p) {
       }
     } else {
       for (int e = lane; e < p.D; e += 64) {
-        const float a = bf(rowp[e]) * s - p.chat[e];
+        const float a = at(static_cast<long long>(i) * p.D + e) * s - p.chat[e];
         acc += a * a;
       }
     }
     acc = wave_reduce_dpp(acc, FeatAdd{});
     if (lane == 0) p.d[i] = sqrtf(acc);
   }
+}
+
+// ---------------------------------------------------------------- pixel-statistic previews
+// Training-free preview vectors per patch (the preview ablation of Section 4), one wave per
+// patch, written as fp32 rows of out [N, dim]:
+//   kind 0  RGB statistics: channel means and population std of x/255           dim 6
+//   kind 1  colour entropy terms -p_k ln p_k over 64 colours (4 levels/channel)  dim 64
+//   kind 2  Sobel magnitude of the grey image summed per orientation octant,
+//           / (255 P^2)                                                          dim 8
+//   kind 3  4-neighbour Laplacian of the grey image / 255                        dim P^2
+// Grey is held as the exact integer 1000 x grey = 299 R + 587 G + 114 B, so gradients, the
+// Laplacian and the octant decisions are exact integer arithmetic; neighbours cross patch
+// borders and the image edge is clamped.
+constexpr int kPixMaxPatch = 16;
+constexpr int kPixMaxPix = kPixMaxPatch * kPixMaxPatch / 64;   // pixels per lane
+
+struct PixelParams {
+  const uint8_t* img;
+  int H, W, P, gw, N, kind, dim;
+  float* out;
+};
+
+__host__ __device__ inline int pixel_feature_dim(int kind, int P) {
+  return kind == 0 ? 6 : kind == 1 ? 64 : kind == 2 ? 8 : P * P;
+}
+
+// Octant 0..7 of the angle of (gx, gy), 45-degree sectors counter-clockwise from +x (y down
+// the rows), decided by integer comparisons; (0, 0) is octant 0.
+__device__ __forceinline__ int sobel_octant(int gx, int gy) {
+  const int ax = abs(gx), ay = abs(gy);
+  if (gx > 0 && gy >= 0) return ay < ax ? 0 : 1;
+  if (gx <= 0 && gy > 0) return ax <= ay ? 2 : 3;
+  if (gx < 0 && gy <= 0) return ay < ax ? 4 : 5;
+  if (gx >= 0 && gy < 0) return ax <= ay ? 6 : 7;
+  return 0;
+}
+
+__global__ __launch_bounds__(64) void apc_pixel_features(const PixelParams p) {
+  __shared__ int grey[(kPixMaxPatch + 2) * (kPixMaxPatch + 2)];
+  __shared__ int hist[64];
+  const int i = blockIdx.x;
+  const int lane = threadIdx.x;
+  const int P = p.P, P2 = P * P;
+  const int y0 = (i / p.gw) * P, x0 = (i % p.gw) * P;
+  float* out = p.out + static_cast<long long>(i) * p.dim;
+  auto pixel = [&](int y, int x) -> const uint8_t* { return p.img + (static_cast<long long>(y) * p.W + x) * 3; };
+
+  if (p.kind <= 1) {
+    uint32_t px[kPixMaxPix];
+#pragma unroll
+    for (int k = 0; k < kPixMaxPix; ++k) {
+      const int t = lane + 64 * k;
+      px[k] = 0;
+      if (t < P2) {
+        const uint8_t* q = pixel(y0 + t / P, x0 + t % P);
+        px[k] = q[0] | (q[1] << 8) | (q[2] << 16);
+      }
+    }
+    if (p.kind == 0) {
+      float s[3] = {0.f, 0.f, 0.f};
+#pragma unroll
+      for (int k = 0; k < kPixMaxPix; ++k)
+        if (lane + 64 * k < P2)
+#pragma unroll
+          for (int c = 0; c < 3; ++c) s[c] += static_cast<float>((px[k] >> (8 * c)) & 255u);
+      float mean[3], v[3] = {0.f, 0.f, 0.f};
+#pragma unroll
+      for (int c = 0; c < 3; ++c) mean[c] = wave_reduce_dpp(s[c], FeatAdd{}) / static_cast<float>(P2);
+#pragma unroll
+      for (int k = 0; k < kPixMaxPix; ++k)
+        if (lane + 64 * k < P2)
+#pragma unroll
+          for (int c = 0; c < 3; ++c) {
+            const float dv = static_cast<float>((px[k] >> (8 * c)) & 255u) - mean[c];
+            v[c] += dv * dv;
+          }
+#pragma unroll
+      for (int c = 0; c < 3; ++c) v[c] = wave_reduce_dpp(v[c], FeatAdd{});
+      if (lane < 6) {
+        const int c = lane % 3;
+        const float m = c == 0 ? mean[0] : c == 1 ? mean[1] : mean[2];
+        const float vv = c == 0 ? v[0] : c == 1 ? v[1] : v[2];
+        out[lane] = lane < 3 ? m / 255.f : sqrtf(vv / static_cast<float>(P2)) / 255.f;
+      }
+    } else {
+      hist[lane] = 0;
+      __syncthreads();
+#pragma unroll
+      for (int k = 0; k < kPixMaxPix; ++k)
+        if (lane + 64 * k < P2) {
+          const uint32_t u = px[k];
+          const int colour = ((u & 255u) >> 6) * 16 + (((u >> 8) & 255u) >> 6) * 4 + (((u >> 16) & 255u) >> 6);
+          atomicAdd(&hist[colour], 1);
+        }
+      __syncthreads();
+      const int cnt = hist[lane];
+      const float pk = static_cast<float>(cnt) / static_cast<float>(P2);
+      out[lane] = cnt > 0 ? -pk * logf(pk) : 0.f;
+    }
+    return;
+  }
+
+  const int G = P + 2;
+  for (int t = lane; t < G * G; t += 64) {
+    const int y = min(max(y0 - 1 + t / G, 0), p.H - 1);
+    const int x = min(max(x0 - 1 + t % G, 0), p.W - 1);
+    const uint8_t* q = pixel(y, x);
+    grey[t] = 299 * q[0] + 587 * q[1] + 114 * q[2];
+  }
+  __syncthreads();
+  auto g = [&](int r, int c) { return grey[(r + 1) * G + (c + 1)]; };   // patch coordinates
+  if (p.kind == 3) {
+    for (int t = lane; t < P2; t += 64) {
+      const int r = t / P, c = t % P;
+      const int lap = 4 * g(r, c) - g(r - 1, c) - g(r + 1, c) - g(r, c - 1) - g(r, c + 1);
+      out[t] = static_cast<float>(lap) / 255000.f;
+    }
+    return;
+  }
+  float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  for (int t = lane; t < P2; t += 64) {
+    const int r = t / P, c = t % P;
+    const int gx = (g(r - 1, c + 1) + 2 * g(r, c + 1) + g(r + 1, c + 1)) -
+                   (g(r - 1, c - 1) + 2 * g(r, c - 1) + g(r + 1, c - 1));
+    const int gy = (g(r + 1, c - 1) + 2 * g(r + 1, c) + g(r + 1, c + 1)) -
+                   (g(r - 1, c - 1) + 2 * g(r - 1, c) + g(r - 1, c + 1));
+    const float mag = static_cast<float>(sqrt(static_cast<double>(gx) * gx + static_cast<double>(gy) * gy));
+    const int o = sobel_octant(gx, gy);
+#pragma unroll
+    for (int k = 0; k < 8; ++k) acc[k] += (o == k) ? mag : 0.f;
+  }
+  const float scale = 1.f / (1000.f * 255.f * static_cast<float>(P2));
+  float mine = 0.f;
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    const float tot = wave_reduce_dpp(acc[k], FeatAdd{});
+    if (lane == k) mine = tot * scale;
+  }
+  if (lane < 8) out[lane] = mine;
 }
 
 // Sum of the tile partials per component: 64 components per block, 16 interleaved
@@ -765,6 +908,27 @@ void size_density(Sizer& s, int H, int W, int P) {
   s.take<float>(N);                              // d (when d_out is null)
 }
 
+// The density steps over a feature matrix: pass 0 (norms and block partials), the partial
+// reduction, c and phi, pass 1 (distances) and the tail.
+pace_status_t launch_feature_density(const DensityParams& p, int mode, hipStream_t stream) {
+  const dim3 g0(p.n_tiles), g1((p.N + 3) / 4), blk(256);
+  if (mode == kFeatBf16Vec) hipLaunchKernelGGL((apc_feat_pass<0, kFeatBf16Vec>), g0, blk, 0, stream, p);
+  else if (mode == kFeatBf16) hipLaunchKernelGGL((apc_feat_pass<0, kFeatBf16>), g0, blk, 0, stream, p);
+  else hipLaunchKernelGGL((apc_feat_pass<0, kFeatF32>), g0, blk, 0, stream, p);
+  pace_status_t st = check_launch("apc_feat_pass<0>");
+  if (st != PACE_OK) return st;
+  hipLaunchKernelGGL(apc_reduce_c, dim3((p.D + 63) / 64), dim3(1024), 0, stream, p);
+  if ((st = check_launch("apc_reduce_c")) != PACE_OK) return st;
+  hipLaunchKernelGGL(apc_finalize_c, dim3(1), dim3(1024), 0, stream, p);
+  if ((st = check_launch("apc_finalize_c")) != PACE_OK) return st;
+  if (mode == kFeatBf16Vec) hipLaunchKernelGGL((apc_feat_pass<1, kFeatBf16Vec>), g1, blk, 0, stream, p);
+  else if (mode == kFeatBf16) hipLaunchKernelGGL((apc_feat_pass<1, kFeatBf16>), g1, blk, 0, stream, p);
+  else hipLaunchKernelGGL((apc_feat_pass<1, kFeatF32>), g1, blk, 0, stream, p);
+  if ((st = check_launch("apc_feat_pass<1>")) != PACE_OK) return st;
+  hipLaunchKernelGGL(apc_tail, dim3(1), dim3(1024), 0, stream, p);
+  return check_launch("apc_tail");
+}
+
 }  // namespace
 }  // namespace pace
 
@@ -874,20 +1038,80 @@ pace_status_t pace_apc_density_features(const uint16_t* feat, int N, int D, doub
   float* dws = c.take<float>(N);
   p.d = d_out ? d_out : dws;
   p.rho_out = rho_out;
-  const bool vec = D % 8 == 0 && aligned16(feat);
-  if (vec) hipLaunchKernelGGL((apc_feat_pass<0, true>), dim3(p.n_tiles), dim3(256), 0, stream, p);
-  else hipLaunchKernelGGL((apc_feat_pass<0, false>), dim3(p.n_tiles), dim3(256), 0, stream, p);
-  pace_status_t st = check_launch("apc_feat_pass<0>");
+  const int mode = (D % 8 == 0 && aligned16(feat)) ? kFeatBf16Vec : kFeatBf16;
+  return launch_feature_density(p, mode, stream);
+}
+
+size_t pace_apc_pixel_density_workspace_size(int H, int W, int patch, int kind) {
+  if (H <= 0 || W <= 0 || patch <= 0 || kind < 0 || kind > 3) return 0;
+  const int N = (H / patch) * (W / patch);
+  const int D = pixel_feature_dim(kind, patch);
+  if (N <= 0) return 0;
+  Sizer s;
+  s.take<float>(static_cast<size_t>(N) * D);          // the preview vectors
+  return align_up(s.off, 256) + pace_apc_density_features_workspace_size(N, D);
+}
+
+pace_status_t pace_apc_pixel_features(const uint8_t* img, int H, int W, int patch, int kind,
+                                      float* out, hipStream_t stream) {
+  PACE_REQUIRE(img && out, "pace_apc_pixel_features: null device pointer");
+  PACE_REQUIRE(kind >= 0 && kind <= 3, "pace_apc_pixel_features: kind=%d not in [0, 3]", kind);
+  PACE_REQUIRE(patch >= 1 && patch <= kPixMaxPatch, "pace_apc_pixel_features: patch=%d not in [1, %d]",
+               patch, kPixMaxPatch);
+  PACE_REQUIRE(H >= patch && W >= patch && H % patch == 0 && W % patch == 0,
+               "pace_apc_pixel_features: H=%d W=%d must be positive multiples of patch=%d", H, W, patch);
+  PACE_REQUIRE(static_cast<long long>(H) * W * 3 < (1ll << 31), "pace_apc_pixel_features: image too large");
+  PixelParams q{};
+  q.img = img;
+  q.H = H; q.W = W; q.P = patch;
+  q.gw = W / patch;
+  q.N = (H / patch) * q.gw;
+  q.kind = kind;
+  q.dim = pixel_feature_dim(kind, patch);
+  q.out = out;
+  hipLaunchKernelGGL(apc_pixel_features, dim3(q.N), dim3(64), 0, stream, q);
+  return check_launch("apc_pixel_features");
+}
+
+pace_status_t pace_apc_pixel_density(const uint8_t* img, int H, int W, int patch, int kind,
+                                     double tail_frac, float alpha, float gamma, float* d_out,
+                                     float* rho_out, void* workspace, size_t workspace_bytes,
+                                     hipStream_t stream) {
+  PACE_REQUIRE(img && rho_out, "pace_apc_pixel_density: null device pointer");
+  PACE_REQUIRE(tail_frac > 0 && tail_frac <= 1, "pace_apc_pixel_density: tail_frac must be in (0, 1]");
+  PACE_REQUIRE(gamma > 0.f, "pace_apc_pixel_density: gamma must be > 0");
+  PACE_REQUIRE(kind >= 0 && kind <= 3, "pace_apc_pixel_density: kind=%d not in [0, 3]", kind);
+  PACE_REQUIRE(patch >= 1 && patch <= kPixMaxPatch && H >= patch && W >= patch && H % patch == 0 &&
+                   W % patch == 0,
+               "pace_apc_pixel_density: H=%d W=%d must be positive multiples of patch=%d <= %d", H, W,
+               patch, kPixMaxPatch);
+  const size_t need = pace_apc_pixel_density_workspace_size(H, W, patch, kind);
+  if (workspace == nullptr || workspace_bytes < need)
+    return set_error(PACE_ERR_WORKSPACE, "pace_apc_pixel_density: workspace %zu < %zu bytes",
+                     workspace_bytes, need);
+  const int N = (H / patch) * (W / patch);
+  const int D = pixel_feature_dim(kind, patch);
+  Carver c(workspace, workspace_bytes);
+  float* feats = c.take<float>(static_cast<size_t>(N) * D);
+  pace_status_t st = pace_apc_pixel_features(img, H, W, patch, kind, feats, stream);
   if (st != PACE_OK) return st;
-  hipLaunchKernelGGL(apc_reduce_c, dim3((p.D + 63) / 64), dim3(1024), 0, stream, p);
-  if ((st = check_launch("apc_reduce_c")) != PACE_OK) return st;
-  hipLaunchKernelGGL(apc_finalize_c, dim3(1), dim3(1024), 0, stream, p);
-  if ((st = check_launch("apc_finalize_c")) != PACE_OK) return st;
-  if (vec) hipLaunchKernelGGL((apc_feat_pass<1, true>), dim3((N + 3) / 4), dim3(256), 0, stream, p);
-  else hipLaunchKernelGGL((apc_feat_pass<1, false>), dim3((N + 3) / 4), dim3(256), 0, stream, p);
-  if ((st = check_launch("apc_feat_pass<1>")) != PACE_OK) return st;
-  hipLaunchKernelGGL(apc_tail, dim3(1), dim3(1024), 0, stream, p);
-  return check_launch("apc_tail");
+  DensityParams p{};
+  p.featf = feats;
+  p.N = N;
+  p.D = D;
+  p.n_tiles = (N + kFeatRows - 1) / kFeatRows;
+  const int nt = pace_keep_count(tail_frac, p.N);
+  p.n_tail = nt < 1 ? 1 : nt;
+  p.alpha = alpha; p.gamma = gamma;
+  p.inv_norm = c.take<float>(N);
+  p.partial = c.take<float>(static_cast<size_t>(p.n_tiles) * D);
+  p.csum = c.take<float>(D);
+  p.chat = c.take<float>(D);
+  p.stats = c.take<float>(8);
+  float* dws = c.take<float>(N);
+  p.d = d_out ? d_out : dws;
+  p.rho_out = rho_out;
+  return launch_feature_density(p, kFeatF32, stream);
 }
 
 pace_status_t pace_apc_downsample(const uint8_t* src, int H, int W, uint8_t* dst, int oH, int oW,

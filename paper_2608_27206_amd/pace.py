@@ -39,6 +39,10 @@ _PROTOS = {
     "pace_apc_density_features": (c_int, [c_void, c_int, c_int, c_double, c_float, c_float, c_void,
                                           c_void, c_void, c_size, c_void]),
     "pace_apc_downsample": (c_int, [c_void, c_int, c_int, c_void, c_int, c_int, c_void]),
+    "pace_apc_pixel_features": (c_int, [c_void, c_int, c_int, c_int, c_int, c_void, c_void]),
+    "pace_apc_pixel_density_workspace_size": (c_size, [c_int, c_int, c_int, c_int]),
+    "pace_apc_pixel_density": (c_int, [c_void, c_int, c_int, c_int, c_int, c_double, c_float, c_float,
+                                       c_void, c_void, c_void, c_size, c_void]),
     "pace_apc_preview_workspace_size": (c_size, [c_int, c_int, c_int, c_int]),
     "pace_apc_preview": (c_int, [c_void, c_int, c_int, c_int, c_void, c_void, c_int, c_int, c_void, c_void,
                                  c_void, c_size, c_void]),
@@ -166,6 +170,50 @@ def apc_density_features(feat: torch.Tensor, tail_frac: float = 0.10, alpha: flo
     _check(lib().pace_apc_density_features(_ptr(feat), N, D, float(tail_frac), float(alpha),
                                            float(gamma), _ptr(d_out), _ptr(rho_out), _ptr(workspace),
                                            workspace.numel(), _stream()), "pace_apc_density_features")
+    return rho_out, d_out
+
+
+PIXEL_STATISTICS = {"rgb": 0, "entropy": 1, "edges": 2, "laplacian": 3}
+
+
+def pixel_feature_dim(kind: int, patch: int) -> int:
+    return (6, 64, 8, patch * patch)[kind]
+
+
+def apc_pixel_features(img: torch.Tensor, kind: int, patch: int = 14,
+                       out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """img: uint8 [H, W, 3] on the GPU.  Returns fp32 [N, dim] pixel-statistic preview vectors."""
+    if img.dtype != torch.uint8 or img.dim() != 3 or img.shape[2] != 3:
+        raise PaceError("img must be a uint8 [H, W, 3] tensor")
+    H, W, _ = img.shape
+    if not 0 <= kind <= 3:
+        raise PaceError(f"kind={kind} not in 0..3")
+    N = (H // patch) * (W // patch)
+    if out is None:
+        out = torch.empty(N, pixel_feature_dim(kind, patch), dtype=torch.float32, device=img.device)
+    _check(lib().pace_apc_pixel_features(_ptr(img), H, W, patch, kind, _ptr(out), _stream()),
+           "pace_apc_pixel_features")
+    return out
+
+
+def apc_pixel_density(img: torch.Tensor, kind: int, patch: int = 14, tail_frac: float = 0.10,
+                      alpha: float = 0.6, gamma: float = 1.5, d_out: Optional[torch.Tensor] = None,
+                      rho_out: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None):
+    """APC density with a pixel-statistic preview.  Returns (rho [4], d [N])."""
+    if img.dtype != torch.uint8 or img.dim() != 3 or img.shape[2] != 3:
+        raise PaceError("img must be a uint8 [H, W, 3] tensor")
+    H, W, _ = img.shape
+    N = (H // patch) * (W // patch)
+    dev = img.device
+    if d_out is None:
+        d_out = torch.empty(max(N, 1), dtype=torch.float32, device=dev)
+    if rho_out is None:
+        rho_out = torch.empty(4, dtype=torch.float32, device=dev)
+    if workspace is None:
+        workspace = _ws(lib().pace_apc_pixel_density_workspace_size(H, W, patch, kind), dev)
+    _check(lib().pace_apc_pixel_density(_ptr(img), H, W, patch, kind, float(tail_frac), float(alpha),
+                                        float(gamma), _ptr(d_out), _ptr(rho_out), _ptr(workspace),
+                                        workspace.numel(), _stream()), "pace_apc_pixel_density")
     return rho_out, d_out
 
 

@@ -155,3 +155,74 @@ def test_density_features_beyond_the_register_tail():
     rs = np.random.default_rng(8)
     x = rs.normal(size=(50000, 16)).astype(np.float32)
     _check_features(wl.f32_to_bf16_bits(x))
+
+
+# ---------------------------------------------------------------- pixel-statistic previews
+# Preview vectors: within rtol 1e-5 + atol 1e-6 of the float64 oracle (fp32 sums of at most 256
+# terms; the octant of each gradient is exact integer arithmetic on both sides).  Densities of
+# those vectors: the 1e-4 bar of the image path.
+@pytest.mark.parametrize("kind", [0, 1, 2, 3])
+@pytest.mark.parametrize("shape,patch", [((448, 448), 14), ((196, 308), 14), ((48, 80), 16), ((9, 12), 3)])
+def test_pixel_features_parity(kind, shape, patch):
+    from paper_2608_27206_amd import pace
+    import torch
+    img = wl.make_image(1, shape[0], shape[1])
+    say(f"pixel features kind={kind} {shape} patch={patch}")
+    got = pace.apc_pixel_features(dev_u8(img), kind, patch)
+    torch.cuda.synchronize()
+    ref = oapc.pixel_statistic_features(img, patch, kind)
+    assert got.shape == ref.shape
+    np.testing.assert_allclose(host(got), ref, rtol=1e-5, atol=1e-6)
+
+
+@pytest.mark.parametrize("kind", [0, 1, 2, 3])
+@pytest.mark.parametrize("shape", [(448, 448), (196, 308)])
+def test_pixel_density_parity(kind, shape):
+    from paper_2608_27206_amd import pace
+    import torch
+    img = wl.make_image(2, shape[0], shape[1])
+    say(f"pixel density kind={kind} {shape}")
+    rho, d = pace.apc_pixel_density(dev_u8(img), kind, 14)
+    torch.cuda.synchronize()
+    ref = oapc.pixel_density(img, 14, kind)
+    np.testing.assert_allclose(host(d), ref["d"], atol=1e-4)
+    np.testing.assert_allclose(host(rho), [ref["rho_g"], ref["rho_d"], ref["rho"], ref["phi"]], atol=1e-4)
+
+
+def test_pixel_features_full_frame():
+    """All four previews of a 2156 x 3836 frame (42,196 patches) against the oracle, element by
+    element."""
+    from paper_2608_27206_amd import pace
+    import torch
+    img = wl.make_image(1, 2156, 3836)
+    dimg = dev_u8(img)
+    for kind in range(4):
+        say(f"pixel features full frame kind={kind}")
+        got = pace.apc_pixel_features(dimg, kind, 14)
+        torch.cuda.synchronize()
+        np.testing.assert_allclose(host(got), oapc.pixel_statistic_features(img, 14, kind), rtol=1e-5, atol=1e-6)
+
+
+def test_pixel_density_flat_and_tiled():
+    """A flat image: zero edge and Laplacian vectors, so phi = 0 and rho_g = 1; a tiling of one
+    patch: equal RGB-statistic vectors, phi = 1 and every d_i = 0 (up to rounding)."""
+    from paper_2608_27206_amd import pace
+    import torch
+    flat = np.full((56, 84, 3), 77, np.uint8)
+    for kind in (2, 3):
+        rho, d = pace.apc_pixel_density(dev_u8(flat), kind, 14)
+        torch.cuda.synchronize()
+        assert host(rho)[3] == 0.0 and host(rho)[0] == 1.0 and np.all(host(d) == 0)
+    tile = np.random.default_rng(3).integers(0, 256, size=(14, 14, 3), dtype=np.uint8)
+    rho, d = pace.apc_pixel_density(dev_u8(np.tile(tile, (4, 5, 1))), 0, 14)
+    torch.cuda.synchronize()
+    assert abs(host(rho)[3] - 1.0) < 1e-5 and np.max(host(d)) < 1e-3
+
+
+def test_pixel_rejects_bad_kind_and_patch():
+    from paper_2608_27206_amd import pace
+    img = dev_u8(wl.make_image(1, 28, 28))
+    with pytest.raises(pace.PaceError, match="kind"):
+        pace.apc_pixel_features(img, 4, 14)
+    with pytest.raises(pace.PaceError, match="patch"):
+        pace.apc_pixel_features(img, 0, 28 * 0 + 17)
