@@ -131,6 +131,8 @@ def main():
     fuse = torch.empty((1, 4), **f32)
     kept = torch.empty((K, hidden.shape[1]), dtype=hidden.dtype, device=dev)
     ws_sel = torch.empty(pace.lib().pace_ddae_select_workspace_size(Nv, 1), dtype=torch.uint8, device=dev)
+    ws_vit = torch.empty(pace.lib().pace_vit_attention_workspace_size(Np, Hv, dv, 1, Np), dtype=torch.uint8,
+                         device=dev)
 
     stream = torch.cuda.current_stream()
     names = ("apc", "resize", "vit_win", "vit_fwd", "vit_mass", "prefill", "select")
@@ -153,7 +155,7 @@ def main():
         run("vit_win", lambda: pace.vit_attention(vq, vk, vv, cu_win, max_win, o=o_win, lse=lse_win,
                                                   mass=mass_win), ev)
         run("vit_fwd", lambda: pace.vit_attention(vq, vk, vv, cu_full, Np, o=o_full, lse=lse_full,
-                                                  want_mass=False), ev)
+                                                  want_mass=False, workspace=ws_vit), ev)
         run("vit_mass", lambda: pace.vit_attention_mass(vq, vk, cu_full, Np, lse_full, mass=mass_vis),
             ev)
         run("prefill", lambda: pace.prefill_attention_with_mass(

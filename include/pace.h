@@ -204,7 +204,7 @@ size_t pace_apc_preview_workspace_size(int N, int dim, int ffn, int patch);
  *   img         uint8 [H, W, 3]; H and W multiples of patch (1..16); N = (H/patch)*(W/patch).
  *   token_patch int32 [N] (device): raster index of the patch that token t holds (the encoder's
  *               window-major order); cu_windows int32 [nwin+1] (device): windows as
- *               consecutive token ranges, each at most max_window tokens.
+ *               consecutive token ranges, each at most max_window (< 1024) tokens.
  *   out         bf16 [N, D], 16-byte aligned.
  */
 pace_status_t pace_apc_preview(const uint8_t* img, int H, int W, int patch, const int32_t* token_patch,
@@ -239,8 +239,12 @@ pace_status_t pace_apc_downsample(const uint8_t* src, int H, int W, uint8_t* dst
 
 /* ---------------------------------------------------------------- attention */
 
-/* Workspace bytes for pace_vit_attention (LSE scratch when lse == NULL and mass != NULL). */
-size_t pace_vit_attention_workspace_size(int N, int H);
+/*
+ * Workspace bytes for pace_vit_attention with these arguments: LSE scratch (used when
+ * lse == NULL and mass != NULL) and, when d == 80 and max_seglen >= 1024 (the long-segment
+ * kernel), fp16 V^T tiles of H * 81 * (8 ceil(N/8) + 8 nseg) values.
+ */
+size_t pace_vit_attention_workspace_size(int N, int H, int d, int nseg, int max_seglen);
 
 /*
  * Vision-encoder self-attention with per-key mass (window attention and the
@@ -255,7 +259,11 @@ size_t pace_vit_attention_workspace_size(int N, int H);
  *   mass      fp32 [H, N]: mass[h, j] = sum over every query row i of j's segment
  *             of P_h[i, j] (column sums of the normalised probabilities), or NULL.
  * The mass pass needs the LSE: when lse is NULL and mass is not, the workspace
- * holds it.  Requires N >= 1, H >= 1, nseg >= 1.
+ * holds it.  At d == 80 with max_seglen >= 1024 the workspace is always required: the
+ * long-segment kernel runs the PV product in fp16 on V^T tiles it writes there, so V's
+ * elements must lie within fp16's range (|v| <= 65504; below 2^-14 they keep fewer bits).
+ * The workspace must be 16-byte aligned, pace_vit_attention_workspace_size bytes.
+ * Requires N >= 1, H >= 1, nseg >= 1.
  */
 pace_status_t pace_vit_attention(const uint16_t* q, const uint16_t* k, const uint16_t* v, int N,
                                  int H, int d, const int32_t* cu_seqlens, int nseg, int max_seglen,

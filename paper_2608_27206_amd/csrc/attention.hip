@@ -162,6 +162,8 @@ struct FwdParams {
   int Ntot, Hq, Hkv, group;
   int nseg, nqt;           // q tiles per segment in the grid
   float scale_log2;        // scale * log2(e)
+  const uint16_t* vt;      // fp16 V^T tiles (rotation kernel only)
+  long long vt_cols;
 };
 
 constexpr int kBM = 128;   // query rows per workgroup
@@ -456,22 +458,98 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd(const FwdParams p) {
 }
 
 // ---------------------------------------------------------------- forward, rotation
-// For long segments without a causal mask.  A workgroup = 12 waves x 32 query rows in three
-// groups of four; wave w runs on SIMD w % 4, so every SIMD holds one wave of each group.
-// Each wave processes a 64-key tile t in three phases, one per time slot:
-//   A1: row max (and rare rescale) of S^T(t), exponentials of its first 12 keys per lane;
-//   A2: the remaining 20 exponentials, row sums, bf16 packing of P^T(t), and the first
-//       half of S^T(t+1) = K(t+1) Q^T;
-//   B : the second half of S^T(t+1) and O^T += V(t)^T P^T(t).
+// For long segments without a causal mask at head dim 80.  A workgroup = 12 waves x 32 query
+// rows in three groups of four; wave w runs on SIMD w % 4, so every SIMD holds one wave of
+// each group.  Each wave processes a 64-key tile t in three phases, one per time slot:
+//   A1: row max (and rare rescale) of S^T(t), the first kA1Vals exponentials per lane;
+//   A2: the remaining exponentials and the fp16 packing of P^T(t);
+//   B : S^T(t+1) = K(t+1) Q^T and O^T += V(t)^T P^T(t), all 22 MFMAs of the tile.
 // Group g runs g slots behind group 0 and a workgroup barrier ends every slot, so in each
-// slot the three phases run side by side on every SIMD: a single wave cannot issue VALU
-// work fast enough to keep the VALU busy, two can, and MFMA work overlaps with both.
-// Group 0 also moves the data: during its phase A2 of tile t it transposes V(t) once into
-// the operand layout (transposing LDS reads are slow, so every wave then reads V^T with
-// plain 16-byte reads) and issues the DMA of K(t+2) and V(t+2), which it awaits before
-// the barrier that ends its phase A1 of tile t+1.  K and the row-major V run through three
-// LDS buffers, V^T through two; every buffer's previous tile is read for the last time
-// at least one slot before it is overwritten.
+// slot two waves per SIMD issue VALU work (a single wave cannot keep the VALU busy) while
+// the third keeps the matrix pipe busy.
+//
+// The PV product runs in fp16 on V^T tiles that attn_vt_prep writes once per call: row 80
+// of each tile is all ones, so O^T's padding row 80 accumulates the row sums of P and the
+// VALU adds no sums.  P is exp2(s * scale * log2 e - m + 7) <= 2^15 (lazy rescaling keeps
+// s * scale * log2 e - m <= 8), so it stays far from fp16's overflow and its small values
+// keep 11 significant bits down to 2^-21 of the row max; the row sums therefore carry at
+// most 2^-12 relative rounding, against 2^-9 for bf16 P.
+// K rows enter the MFMA in a permuted order (bits 2 and 3 of the row index swapped), which
+// puts each lane's keys in the order the B operand of the PV product takes them, so V^T
+// tiles are in plain key order.  Group 0 issues the DMA of K(t+2) and V^T(t+2) during its
+// phase A2 of tile t and awaits it before the barrier that ends its phase A1 of tile t+1.
+// K runs through three LDS buffers (read in phase B of the tile before), V^T through four
+// (read in phase B of its own tile, up to three slots later).
+
+// fp16 V^T tiles in the workspace, [H][kVtRows][vt_cols]: segment s owns the 16-byte aligned
+// columns [vt_start(s), vt_start(s+1)), vt_start(s) = 8 ceil(cu[s] / 8) + 8 s; column
+// vt_start(s) + j holds key j of the segment for j < L_s and zero past it (so every column
+// a tile reads is finite).  Rows 0..79 are V^T, row 80 is one for the segment's keys.
+constexpr int kVtRows = 81;
+
+__host__ __device__ inline long long vt_cols(int N, int nseg) { return 8ll * ((N + 7) / 8) + 8ll * nseg; }
+__device__ __forceinline__ int vt_start(int cu_s, int s) { return 8 * ((cu_s + 7) / 8) + 8 * s; }
+
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ f16x8 as_f16x8(uint4 u) {
+  f16x8 r;
+  __builtin_memcpy(&r, &u, 16);
+  return r;
+}
+__device__ __forceinline__ f32x16 mfma_f16(f16x8 a, f16x8 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ uint32_t pack_f16x2(float a, float b) {
+  f32x2 v = {a, b};
+  f16x2 r = __builtin_convertvector(v, f16x2);
+  uint32_t u;
+  __builtin_memcpy(&u, &r, 4);
+  return u;
+}
+
+struct VtParams {
+  const uint16_t* v;     // bf16 [N, H, 80]
+  uint16_t* vt;          // fp16 [H, kVtRows, cols]
+  const int32_t* cu;
+  int H, tiles;          // tiles: 64-column blocks per segment in the grid
+  long long cols;
+};
+
+// One workgroup per (64-column block of a segment, head): V rows in, fp16 V^T rows out.
+// bf16 -> fp16 is exact for |v| in [2^-14, 65504]; smaller values round to fp16 subnormals.
+__global__ __launch_bounds__(256) void attn_vt_prep(const VtParams p) {
+  __shared__ __align__(16) uint16_t T[kVtRows][64 + 8];
+  const int s = blockIdx.x / p.tiles, t = blockIdx.x - (blockIdx.x / p.tiles) * p.tiles;
+  const int h = blockIdx.y;
+  const int c0 = p.cu[s], L = p.cu[s + 1] - c0;
+  const int col0 = vt_start(c0, s);
+  const int width = vt_start(p.cu[s + 1], s + 1) - col0;
+  if (64 * t >= width) return;   // the whole workgroup leaves together
+  const int tid = threadIdx.x;
+  for (int c = tid; c < 64 * 10; c += 256) {
+    const int key = c / 10, ch = c - (c / 10) * 10;
+    const int j = 64 * t + key;
+    uint4 u = make_uint4(0u, 0u, 0u, 0u);
+    if (j < L) u = *reinterpret_cast<const uint4*>(p.v + (static_cast<long long>(c0 + j) * p.H + h) * 80 + ch * 8);
+    const uint32_t w4[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const uint32_t pk = pack_f16x2(__uint_as_float(w4[e] << 16), __uint_as_float(w4[e] & 0xffff0000u));
+      T[ch * 8 + 2 * e][key] = static_cast<uint16_t>(pk & 0xffffu);
+      T[ch * 8 + 2 * e + 1][key] = static_cast<uint16_t>(pk >> 16);
+    }
+  }
+  if (tid < 64) T[80][tid] = (64 * t + tid < L) ? static_cast<uint16_t>(0x3C00) : static_cast<uint16_t>(0);
+  __syncthreads();
+  for (int c = tid; c < kVtRows * 8; c += 256) {
+    const int d = c >> 3, col = 64 * t + 8 * (c & 7);
+    if (col < width)
+      *reinterpret_cast<uint4*>(p.vt + (static_cast<long long>(h) * kVtRows + d) * p.cols + col0 + col) =
+          *reinterpret_cast<const uint4*>(&T[d][col - 64 * t]);
+  }
+}
 
 // Workgroup barrier that also fences the instruction scheduler, so no computation
 // migrates between the two sides of a phase boundary.
@@ -483,16 +561,23 @@ __device__ __forceinline__ void phase_sync() {
 
 constexpr int kRotWaves = 12;
 constexpr int kRotThreads = 64 * kRotWaves;
-constexpr int kRotBM = 32 * kRotWaves;   // query rows per workgroup
-constexpr int kVtStride = kBN + 8;       // LDS row stride of a transposed V tile (elements)
-constexpr int kA1Vals = 12;              // exponentials per lane in phase A1 (of 32)
+constexpr int kRotBM = 32 * kRotWaves;                // query rows per workgroup
+constexpr int kVtStride = kBN + 8;                    // LDS row stride of a V^T tile (elements)
+constexpr int kVtChunks = kVtRows * (kVtStride / 8);  // 16-byte DMA chunks per V^T tile
+constexpr int kVtInst = (kVtChunks + 63) / 64;        // wave-wide DMA loads per V^T tile
+constexpr int kVtPW = (kVtInst + 3) / 4;              // per wave of group 0
+constexpr int kA1Vals = 14;                           // exponentials per lane in phase A1 (of 32)
+constexpr float kP16Shift = 7.0f;                     // log2 of P's scale factor
+
+// Row order of K in S^T = K Q^T: bits 2 and 3 of the row index swapped (an involution).
+__device__ __forceinline__ int swap_bits23(int r) { return (r & ~12) | ((r & 4) << 1) | ((r & 8) >> 1); }
 
 template <int D>
 __global__ __launch_bounds__(kRotThreads, 1) void attn_fwd_rot(const FwdParams p) {
+  static_assert(D == 80, "the rotation kernel is laid out for head dim 80");
   using C = FwdCfg<D>;
   __shared__ __align__(16) uint16_t Ks[3][kBN * C::KS];
-  __shared__ __align__(16) uint16_t Vs[3][kBN * C::VS];          // V tiles as loaded (row-major)
-  __shared__ __align__(16) uint16_t Vt[2][C::DV * kVtStride];    // the same tiles as V^T operands
+  __shared__ __align__(16) uint16_t Vt[4][C::DV * kVtStride];   // fp16 V^T tiles (rows 81.. unused)
 
   const int lb = remap_block_id(blockIdx.x, gridDim.x);
   const int per_head = p.nseg * p.nqt;
@@ -516,7 +601,8 @@ __global__ __launch_bounds__(kRotThreads, 1) void attn_fwd_rot(const FwdParams p
   const unsigned seg_bytes_kv = static_cast<unsigned>((L - 1) * kvstride + D) * 2u;
   const auto rq = make_rsrc(p.q + static_cast<long long>(s0) * qstride + h * D, seg_bytes_q);
   const auto rk = make_dma_rsrc(p.k + static_cast<long long>(s0) * kvstride + kvh * D, seg_bytes_kv);
-  const auto rv = make_dma_rsrc(p.v + static_cast<long long>(s0) * kvstride + kvh * D, seg_bytes_kv);
+  const auto rvt = make_dma_rsrc(p.vt + static_cast<long long>(kvh) * kVtRows * p.vt_cols,
+                                 static_cast<unsigned>(kVtRows * p.vt_cols * 2));
 
   bf16x8 qf[C::KC];
   {
@@ -525,42 +611,40 @@ __global__ __launch_bounds__(kRotThreads, 1) void attn_fwd_rot(const FwdParams p
     for (int c = 0; c < C::KC; ++c) qf[c] = as_bf16x8(buf_load16(rq, qoff + c * 32, 0));
   }
 
-  // DMA chunk offsets (same chunk order as attn_fwd), issued by the 4 waves of group 0
-  unsigned koff[C::KPW], voff[C::VPW];
+  // DMA chunk offsets, issued by the 4 waves of group 0
+  unsigned koff[C::KPW], vtoff[kVtPW];
   static_for<0, C::KPW>([&](auto I) __attribute__((always_inline)) {
     const int c = (wl + 4 * I) * 64 + lane;
     const int r = c / C::KROW, cc = c % C::KROW;
     koff[I] = (cc < D / 8 && wl + 4 * I < C::KINST) ? static_cast<unsigned>(r * kvstride + cc * 8) * 2u
                                                      : kOutOfRange;
   });
-  static_for<0, C::VPW>([&](auto I) __attribute__((always_inline)) {
+  const long long vcol0 = vt_start(s0, seg);
+  static_for<0, kVtPW>([&](auto I) __attribute__((always_inline)) {
     const int c = (wl + 4 * I) * 64 + lane;
-    const int r = c / C::VROW, cc = c % C::VROW;
-    voff[I] = (cc < D / 8 && wl + 4 * I < C::VINST) ? static_cast<unsigned>(r * kvstride + cc * 8) * 2u
-                                                     : kOutOfRange;
+    const int d = c / (kVtStride / 8), cc = c % (kVtStride / 8);
+    vtoff[I] = (cc < kBN / 8 && d < kVtRows && wl + 4 * I < kVtInst)
+                   ? static_cast<unsigned>((d * p.vt_cols + vcol0 + cc * 8) * 2)
+                   : kOutOfRange;
   });
   const unsigned tile_bytes = static_cast<unsigned>(kBN * kvstride) * 2u;
-  const unsigned ks_lds = lds_u32(&Ks[0][0]), vs_lds = lds_u32(&Vs[0][0]);
-  auto load_kv = [&](int t, int buf) __attribute__((always_inline)) {
+  const unsigned ks_lds = lds_u32(&Ks[0][0]), vt_lds = lds_u32(&Vt[0][0]);
+  auto load_kv = [&](int t, int kbuf, int vbuf) __attribute__((always_inline)) {
     static_for<0, C::KPW>([&](auto I) __attribute__((always_inline)) {
       if (wl + 4 * I < C::KINST)
-        dma16(rk, ks_lds + (buf * kBN * C::KS + (wl + 4 * I) * 512) * 2, koff[I] + t * tile_bytes);
+        dma16(rk, ks_lds + (kbuf * kBN * C::KS + (wl + 4 * I) * 512) * 2, koff[I] + t * tile_bytes);
     });
-    static_for<0, C::VPW>([&](auto I) __attribute__((always_inline)) {
-      if (wl + 4 * I < C::VINST)
-        dma16(rv, vs_lds + (buf * kBN * C::VS + (wl + 4 * I) * 512) * 2, voff[I] + t * tile_bytes);
+    static_for<0, kVtPW>([&](auto I) __attribute__((always_inline)) {
+      if (wl + 4 * I < kVtInst)
+        dma16(rvt, vt_lds + (vbuf * C::DV * kVtStride + (wl + 4 * I) * 512) * 2, vtoff[I] + t * (kBN * 2));
     });
   };
 
-  const int tgrp = lane >> 4, li = lane & 15;
-  const int tr_row = 4 * (tgrp >> 1) + (li >> 2);
-  const int tr_col = 16 * (tgrp & 1) + 4 * (li & 3);
-  const int tr_base = tr_row * C::VS + tr_col;
-
   f32x16 s[2];
-  // half st of S^T(tile in K buffer kb): keys 32 st .. 32 st + 31
+  const int krow = swap_bits23(c32);
+  // half st of S^T(tile in K buffer kb): key rows 32 st + swap_bits23(0..31)
   auto qk_half = [&](int kb, int st) __attribute__((always_inline)) {
-    const uint16_t* kp = &Ks[kb][(st * 32 + c32) * C::KS + g * 8];
+    const uint16_t* kp = &Ks[kb][(st * 32 + krow) * C::KS + g * 8];
     bf16x8 kf[C::KC];
 #pragma unroll
     for (int c = 0; c < C::KC; ++c) kf[c] = *reinterpret_cast<const bf16x8*>(kp + c * 16);
@@ -574,35 +658,32 @@ __global__ __launch_bounds__(kRotThreads, 1) void attn_fwd_rot(const FwdParams p
   for (int t2 = 0; t2 < C::NT; ++t2) oacc[t2] = f32x16{};
   float m_used = -INFINITY;
   float m_off = 0.f;
-  float l_part[4] = {0.f, 0.f, 0.f, 0.f};
-  uint32_t pw[2][2][4];   // packed P^T: [half][16-key chunk][bf16 pair]
+  uint32_t pw[2][2][4];   // packed fp16 P^T: [half][16-key chunk][pair]
 
-  // exponentials, row sums and packing of values [R0, R1) of the 32 per lane (pairs)
+  // exponentials and fp16 packing of values [R0, R1) of the 32 per lane (pairs)
   auto exps = [&](auto R0, auto R1) __attribute__((always_inline)) {
     static_for<decltype(R0)::value / 2, decltype(R1)::value / 2>([&](auto J) __attribute__((always_inline)) {
       constexpr int r = 2 * decltype(J)::value, st = r >> 4, rr = r & 15;
       const float e0 = fast_exp2(s[st][rr] * p.scale_log2 - m_off);
       const float e1 = fast_exp2(s[st][rr + 1] * p.scale_log2 - m_off);
-      l_part[rr & 3] += e0;
-      l_part[(rr + 1) & 3] += e1;
-      pw[st][rr >> 3][(rr & 7) >> 1] = pack_bf16x2(e0, e1);
+      pw[st][rr >> 3][(rr & 7) >> 1] = pack_f16x2(e0, e1);
       // pin the results to this phase: left alone, the compiler sinks them past the barrier
       asm volatile("" : "+v"(pw[st][rr >> 3][(rr & 7) >> 1]));
     });
-#pragma unroll
-    for (int i = 0; i < 4; ++i) asm volatile("" : "+v"(l_part[i]));
   };
 
-  // phase A1: mask, max, (rare) rescale, first exponentials
+  // Phase A1: mask keys past the segment end (only a partial last tile has any), row max,
+  // (rare) rescale, first exponentials
   auto phase_a1 = [&](int kt) __attribute__((always_inline)) {
     if (kt + kBN > L) {
+      // register r of half st holds key kt + 32 st + swap_bits23(8 (r / 4) + 4 g + r % 4),
+      // that is kt + 8 g + a constant
+      const int lim = L - kt - 8 * g;
 #pragma unroll
       for (int st = 0; st < 2; ++st)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int key = kt + st * 32 + g * 4 + 8 * (r >> 2) + (r & 3);
-          if (key >= L) s[st][r] = -INFINITY;
-        }
+        for (int r = 0; r < 16; ++r)
+          if (st * 32 + 16 * (r >> 3) + 4 * ((r >> 2) & 1) + (r & 3) >= lim) s[st][r] = -INFINITY;
     }
     float m1[11];
 #pragma unroll
@@ -614,7 +695,10 @@ __global__ __launch_bounds__(kRotThreads, 1) void attn_fwd_rot(const FwdParams p
     const float m2a = fmaxf(fmaxf(m1[0], m1[1]), m1[2]), m2b = fmaxf(fmaxf(m1[3], m1[4]), m1[5]);
     const float m2c = fmaxf(fmaxf(m1[6], m1[7]), m1[8]), m2d = fmaxf(m1[9], m1[10]);
     float mx = fmaxf(fmaxf(m2a, m2b), fmaxf(m2c, m2d));
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * p.scale_log2;
+    {   // the two half-waves hold the same query rows: exchange halves without an LDS round trip
+      const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
+      mx = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1])) * p.scale_log2;
+    }
     if (__builtin_amdgcn_ballot_w64(mx > m_used + kRescaleSlack) != 0ull) {
       const float m_new = fmaxf(m_used, mx);
       const float alpha = fast_exp2(m_used - m_new);
@@ -623,27 +707,58 @@ __global__ __launch_bounds__(kRotThreads, 1) void attn_fwd_rot(const FwdParams p
       for (int t2 = 0; t2 < C::NT; ++t2)
 #pragma unroll
         for (int r = 0; r < 16; ++r) oacc[t2][r] *= alpha;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) l_part[i] *= alpha;
     }
-    m_off = (m_used == -INFINITY) ? 0.f : m_used;
+    m_off = (m_used == -INFINITY) ? 0.f : m_used - kP16Shift;
     exps(std::integral_constant<int, 0>{}, std::integral_constant<int, kA1Vals>{});
   };
 
-  // V^T fragment (st, hh, t2) of a tile: 16 bytes per lane, the A operand of O^T += V^T P^T.
-  // Group 0 moves each V tile once from its row-major copy into Vt (3 fragments per wave).
-  auto transpose_v = [&](int vb, int tb) __attribute__((always_inline)) {
-    static_for<0, 3>([&](auto I) __attribute__((always_inline)) {
-      const int f = wl * 3 + I;
+  // Phase B: S^T(next) from K buffer kb and O^T += V^T P^T from V^T buffer vb.  The K
+  // fragments are read first and the V^T fragments while the S^T MFMAs run (the two halves'
+  // chains interleaved), a few reads ahead of their MFMAs throughout.
+  auto phase_b = [&](int kb, int vb) __attribute__((always_inline)) {
+    const uint16_t* kp = &Ks[kb][krow * C::KS + g * 8];
+    bf16x8 k0[C::KC], k1[C::KC];
+#pragma unroll
+    for (int c = 0; c < C::KC; ++c) {
+      k0[c] = *reinterpret_cast<const bf16x8*>(kp + c * 16);
+      k1[c] = *reinterpret_cast<const bf16x8*>(kp + 32 * C::KS + c * 16);
+    }
+    uint4 va[12];
+    const uint16_t* vp = &Vt[vb][c32 * kVtStride + g * 8];
+#pragma unroll
+    for (int f = 0; f < 12; ++f) {
       const int st = f / 6, hh = (f / 3) & 1, t2 = f % 3;
-      const uint16_t* vp = &Vs[vb][(st * 32 + hh * 16) * C::VS + tr_base + t2 * 32];
-      const uint2 lo = lds_read_tr16(vp);
-      const uint2 hi = lds_read_tr16(vp + 8 * C::VS);
-      *reinterpret_cast<uint4*>(&Vt[tb][(t2 * 32 + c32) * kVtStride + st * 32 + hh * 16 + g * 8]) =
-          make_uint4(lo.x, lo.y, hi.x, hi.y);
+      va[f] = *reinterpret_cast<const uint4*>(vp + t2 * 32 * kVtStride + st * 32 + hh * 16);
+    }
+    s[0] = mfma(k0[0], qf[0], f32x16{});
+    s[1] = mfma(k1[0], qf[0], f32x16{});
+#pragma unroll
+    for (int c = 1; c < C::KC; ++c) {
+      s[0] = mfma(k0[c], qf[c], s[0]);
+      s[1] = mfma(k1[c], qf[c], s[1]);
+    }
+#pragma unroll
+    for (int f = 0; f < 12; ++f) {
+      const int st = f / 6, hh = (f / 3) & 1, t2 = f % 3;
+      const uint4 bp = make_uint4(pw[st][hh][0], pw[st][hh][1], pw[st][hh][2], pw[st][hh][3]);
+      oacc[t2] = mfma_f16(as_f16x8(va[f]), as_f16x8(bp), oacc[t2]);
+    }
+    // issue order: six reads, each pair of S^T MFMAs followed by two more reads, then each
+    // PV MFMA followed by one more read (about six reads in flight throughout)
+    __builtin_amdgcn_sched_group_barrier(0x100, 6, 0);
+    static_for<0, 5>([&](auto) __attribute__((always_inline)) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
     });
+    static_for<0, 6>([&](auto) __attribute__((always_inline)) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    });
+    __builtin_amdgcn_sched_group_barrier(0x008, 6, 0);
   };
-  auto pv = [&](int tb) __attribute__((always_inline)) {
+
+  // O^T += V^T P^T alone (the last tile): A = V^T fragment, B = packed P^T
+  auto pv = [&](int vb) __attribute__((always_inline)) {
 #pragma unroll
     for (int st = 0; st < 2; ++st)
 #pragma unroll
@@ -651,16 +766,16 @@ __global__ __launch_bounds__(kRotThreads, 1) void attn_fwd_rot(const FwdParams p
 #pragma unroll
         for (int t2 = 0; t2 < C::NT; ++t2) {
           const uint4 a = *reinterpret_cast<const uint4*>(
-              &Vt[tb][(t2 * 32 + c32) * kVtStride + st * 32 + hh * 16 + g * 8]);
+              &Vt[vb][(t2 * 32 + c32) * kVtStride + st * 32 + hh * 16 + g * 8]);
           const uint4 bp = make_uint4(pw[st][hh][0], pw[st][hh][1], pw[st][hh][2], pw[st][hh][3]);
-          oacc[t2] = mfma(as_bf16x8(a), as_bf16x8(bp), oacc[t2]);
+          oacc[t2] = mfma_f16(as_f16x8(a), as_f16x8(bp), oacc[t2]);
         }
   };
 
   const int ntiles = (L + kBN - 1) / kBN;
   if (grp == 0) {
-    load_kv(0, 0);
-    if (ntiles > 1) load_kv(1, 1);
+    load_kv(0, 0, 0);
+    if (ntiles > 1) load_kv(1, 1, 1);
     wait_vmem();
   }
   phase_sync();
@@ -671,17 +786,12 @@ __global__ __launch_bounds__(kRotThreads, 1) void attn_fwd_rot(const FwdParams p
   for (; t + 1 < ntiles; ++t) {
     const int kb1 = (kb == 2) ? 0 : kb + 1, kb2 = (kb1 == 2) ? 0 : kb1 + 1;
     phase_a1(t * kBN);
-    if (grp == 0) wait_vmem();   // K(t+1) and V(t+1), issued during phase A2 of tile t-1
+    if (grp == 0) wait_vmem();   // K(t+1) and V^T(t+1), issued during phase A2 of tile t-1
     phase_sync();
     exps(std::integral_constant<int, kA1Vals>{}, std::integral_constant<int, 32>{});
-    if (grp == 0) {
-      transpose_v(kb, t & 1);
-      if (t + 2 < ntiles) load_kv(t + 2, kb2);
-    }
-    qk_half(kb1, 0);
+    if (grp == 0 && t + 2 < ntiles) load_kv(t + 2, kb2, (t + 2) & 3);
     phase_sync();
-    qk_half(kb1, 1);
-    pv(t & 1);
+    phase_b(kb1, t & 3);
     phase_sync();
     kb = kb1;
   }
@@ -689,14 +799,13 @@ __global__ __launch_bounds__(kRotThreads, 1) void attn_fwd_rot(const FwdParams p
   phase_a1(t * kBN);
   phase_sync();
   exps(std::integral_constant<int, kA1Vals>{}, std::integral_constant<int, 32>{});
-  if (grp == 0) transpose_v(kb, t & 1);
   phase_sync();
-  pv(t & 1);
+  pv(t & 3);
   phase_sync();
   for (int i = grp; i < 2; ++i) phase_sync();   // equal barrier counts in every group
 
-  const float lp = (l_part[0] + l_part[1]) + (l_part[2] + l_part[3]);
-  const float l = lp + __shfl_xor(lp, 32, 64);
+  // row 80 of O^T (register 8 of block 2 in the lanes of half 0) is the row sum of P
+  const float l = __shfl(oacc[2][8], c32, 64);
   const float inv_l = 1.f / l;
   if (qrow < L) {
     uint16_t* op = p.o + static_cast<long long>(s0 + qrow) * qstride + h * D;
@@ -714,7 +823,8 @@ __global__ __launch_bounds__(kRotThreads, 1) void attn_fwd_rot(const FwdParams p
       }
     }
     if (g == 0 && p.lse)
-      p.lse[static_cast<long long>(h) * p.Ntot + s0 + qrow] = (m_used + __builtin_amdgcn_logf(l)) * kLn2;
+      p.lse[static_cast<long long>(h) * p.Ntot + s0 + qrow] =
+          (m_off + __builtin_amdgcn_logf(l)) * kLn2;
   }
 }
 
@@ -1093,6 +1203,13 @@ pace_status_t launch_attention(FwdParams fp, bool causal, int max_seglen, const 
     fp.nqt = (max_seglen + kBM - 1) / kBM;
     hipLaunchKernelGGL((attn_fwd<D, true>), dim3(fp.nqt * fp.nseg * fp.Hq), dim3(kThreads), 0, stream, fp);
   } else if (D == 80 && max_seglen >= kRotMinSeg) {
+    VtParams vp{};
+    vp.v = fp.v; vp.vt = const_cast<uint16_t*>(fp.vt); vp.cu = fp.cu;
+    vp.H = fp.Hkv; vp.cols = fp.vt_cols;
+    vp.tiles = (max_seglen + 16 + kBN - 1) / kBN;   // a segment owns at most L + 15 columns
+    hipLaunchKernelGGL(attn_vt_prep, dim3(vp.tiles * fp.nseg, fp.Hkv), dim3(256), 0, stream, vp);
+    pace_status_t st = check_launch("attn_vt_prep");
+    if (st != PACE_OK) return st;
     fp.nqt = (max_seglen + kRotBM - 1) / kRotBM;
     hipLaunchKernelGGL((attn_fwd_rot<80>), dim3(fp.nqt * fp.nseg * fp.Hq), dim3(kRotThreads), 0, stream, fp);
   } else {
@@ -1115,9 +1232,12 @@ using namespace pace;
 
 extern "C" {
 
-size_t pace_vit_attention_workspace_size(int N, int H) {
-  if (N < 0 || H < 0) return 0;
-  return static_cast<size_t>(N) * H * sizeof(float);
+size_t pace_vit_attention_workspace_size(int N, int H, int d, int nseg, int max_seglen) {
+  if (N < 0 || H < 0 || nseg < 0) return 0;
+  size_t bytes = align_up(static_cast<size_t>(N) * H * sizeof(float), 256);
+  if (d == 80 && max_seglen >= kRotMinSeg)
+    bytes += static_cast<size_t>(H) * kVtRows * static_cast<size_t>(vt_cols(N, nseg)) * 2;
+  return bytes;
 }
 
 size_t pace_prefill_attention_workspace_size(int Ntot, int Hq) {
@@ -1144,15 +1264,25 @@ pace_status_t pace_vit_attention(const uint16_t* q, const uint16_t* k, const uin
   pace_status_t chk = check_offsets(cu_seqlens, nseg, N, max_seglen, "pace_vit_attention: cu_seqlens", stream);
   if (chk != PACE_OK) return chk;
   float* lse_buf = lse;
-  if (mass != nullptr && lse == nullptr) {
-    const size_t need = pace_vit_attention_workspace_size(N, H);
+  const bool rot = d == 80 && max_seglen >= kRotMinSeg;
+  const long long cols = vt_cols(N, nseg);
+  PACE_REQUIRE(!rot || static_cast<long long>(kVtRows) * cols * 2 < (1ll << 31),
+               "pace_vit_attention: N + 8 nseg too large for the V^T tiles");
+  if ((mass != nullptr && lse == nullptr) || rot) {
+    const size_t need = pace_vit_attention_workspace_size(N, H, d, nseg, max_seglen);
     if (workspace == nullptr || workspace_bytes < need)
       return set_error(PACE_ERR_WORKSPACE, "pace_vit_attention: workspace %zu < %zu bytes",
                        workspace_bytes, need);
-    lse_buf = static_cast<float*>(workspace);
+    PACE_REQUIRE(aligned16(workspace), "pace_vit_attention: workspace must be 16-byte aligned");
+    if (lse == nullptr && mass != nullptr) lse_buf = static_cast<float*>(workspace);
   }
   FwdParams fp{};
   fp.q = q; fp.k = k; fp.v = v; fp.o = o; fp.lse = lse_buf; fp.cu = cu_seqlens;
+  if (rot) {
+    fp.vt = reinterpret_cast<const uint16_t*>(static_cast<char*>(workspace) +
+                                              align_up(static_cast<size_t>(N) * H * sizeof(float), 256));
+    fp.vt_cols = cols;
+  }
   fp.Ntot = N; fp.Hq = H; fp.Hkv = H; fp.group = 1;
   fp.nseg = nseg; fp.nqt = static_cast<int>(nqt);
   fp.scale_log2 = scale * kLog2e;

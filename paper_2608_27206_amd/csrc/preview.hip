@@ -262,8 +262,8 @@ pace_status_t pace_apc_preview(const uint8_t* img, int H, int W, int patch, cons
   const int D = w->dim, F = w->ffn;
   PACE_REQUIRE(D >= 80 && D % 80 == 0 && F >= 8 && F % 8 == 0,
                "pace_apc_preview: dim=%d must be a multiple of 80 and ffn=%d of 8", D, F);
-  PACE_REQUIRE(nwin >= 1 && max_window >= 1 && max_window <= N, "pace_apc_preview: nwin=%d max_window=%d", nwin,
-               max_window);
+  PACE_REQUIRE(nwin >= 1 && max_window >= 1 && max_window <= N && max_window < 1024,
+               "pace_apc_preview: nwin=%d max_window=%d (windows are shorter than 1024 tokens)", nwin, max_window);
   PACE_REQUIRE(w->pe && w->g1 && w->wq && w->wk && w->wv && w->wo && w->g2 && w->wgu && w->wd,
                "pace_apc_preview: a weight pointer is null");
   PACE_REQUIRE(aligned16(out), "pace_apc_preview: out must be 16-byte aligned");

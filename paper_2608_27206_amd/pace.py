@@ -47,7 +47,7 @@ _PROTOS = {
     "pace_apc_preview": (c_int, [c_void, c_int, c_int, c_int, c_void, c_void, c_int, c_int, c_void, c_void,
                                  c_void, c_size, c_void]),
     "pace_gemm_bf16": (c_int, [c_void, c_void, c_void, c_void, c_void, c_int, c_int, c_int, c_int, c_void]),
-    "pace_vit_attention_workspace_size": (c_size, [c_int, c_int]),
+    "pace_vit_attention_workspace_size": (c_size, [c_int, c_int, c_int, c_int, c_int]),
     "pace_vit_attention": (c_int, [c_void, c_void, c_void, c_int, c_int, c_int, c_void, c_int, c_int,
                                    c_float, c_void, c_void, c_void, c_void, c_size, c_void]),
     "pace_vit_attention_mass": (c_int, [c_void, c_void, c_int, c_int, c_int, c_void, c_int, c_int,
@@ -323,8 +323,11 @@ def vit_attention(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, cu_seqlens:
         lse = None
     if not want_mass:
         mass = None
-    if mass is not None and lse is None and workspace is None:
-        workspace = _ws(lib().pace_vit_attention_workspace_size(N, H), dev)
+    nseg = cu_seqlens.numel() - 1
+    if workspace is None:
+        need = lib().pace_vit_attention_workspace_size(N, H, d, nseg, int(max_seglen))
+        if (mass is not None and lse is None) or need > N * H * 4 + 256:
+            workspace = _ws(need, dev)
     _check(lib().pace_vit_attention(_ptr(q), _ptr(k), _ptr(v), N, H, d, _ptr(cu_seqlens),
                                     cu_seqlens.numel() - 1, int(max_seglen), float(scale), _ptr(o),
                                     _ptr(lse), _ptr(mass), _ptr(workspace),

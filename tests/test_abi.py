@@ -82,6 +82,9 @@ def test_errors_before_launch():
     # mass without lse or workspace
     st = L.pace_vit_attention(fake, fake, fake, 10, 2, 80, fake, 1, 10, 0.1, fake, None, fake, None, 0, None)
     assert st == 3
+    # a long segment at head dim 80 needs the workspace for its V^T tiles
+    st = L.pace_vit_attention(fake, fake, fake, 2048, 2, 80, fake, 1, 2048, 0.1, fake, fake, None, None, 0, None)
+    assert st == 3 and "workspace" in L.pace_last_error().decode()
     # GQA heads not divisible
     st = L.pace_prefill_attention_with_mass(fake, fake, fake, 10, 6, 4, 128, fake, 1, 10, fake, fake, 5,
                                             5, fake, fake, 5, 0.1, fake, fake, fake, None, 0, None)
@@ -130,4 +133,7 @@ def test_workspace_sizes_monotone():
     L = pace.lib()
     assert L.pace_apc_density_workspace_size(2156, 3836, 14) > L.pace_apc_density_workspace_size(448, 448, 14)
     assert L.pace_ddae_select_workspace_size(10549, 1) >= 3 * 10549 * 4
-    assert L.pace_vit_attention_workspace_size(42196, 16) == 42196 * 16 * 4
+    assert L.pace_vit_attention_workspace_size(42196, 16, 80, 700, 64) == 42196 * 16 * 4
+    cols = 8 * ((42196 + 7) // 8) + 8
+    assert L.pace_vit_attention_workspace_size(42196, 16, 80, 1, 42196) == 42196 * 16 * 4 + 16 * 81 * cols * 2
+    assert L.pace_vit_attention_workspace_size(42196, 16, 128, 1, 42196) == 42196 * 16 * 4
