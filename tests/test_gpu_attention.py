@@ -94,8 +94,9 @@ def test_vit_large_logits():
 
 
 def test_vit_long_segments_d80():
-    """Segments of 1024 rows or more take the two-group (ping-pong) forward kernel at head
-    dim 80; shorter segments of the same call go through it too."""
+    """Segments of 1024 rows or more take the rotation forward kernel at head dim 80 (fp16
+    PV product on V^T tiles in the workspace); shorter segments of the same call, at offsets
+    that are not multiples of 8, go through it too."""
     sizes = [1100, 37, 1536, 300, 1]
     cu = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int32)
     q, k, v = _vit_case(21, cu, 2, 80)
@@ -109,6 +110,24 @@ def test_vit_long_segment_large_logits_d80():
     k = wl.random_bf16(32, (N, H, d), 2.5)
     v = wl.random_bf16(33, (N, H, d))
     _check_vit(q, k, v, cu, d)
+
+
+@pytest.mark.parametrize("vscale", [300.0, 1e-5])
+def test_vit_long_segment_value_range_d80(vscale):
+    """The rotation kernel converts V to fp16: large values (well inside fp16's range) and
+    tiny ones (fp16 subnormals) keep O within 2e-2 of its largest magnitude."""
+    sizes = [1030, 70]
+    cu = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int32)
+    N, H, d = int(cu[-1]), 2, 80
+    q = wl.random_bf16(41, (N, H, d))
+    k = wl.random_bf16(42, (N, H, d))
+    v = wl.random_bf16(43, (N, H, d), vscale)
+    say(f"vit long segment, V scale {vscale}")
+    o, lse, _ = _run_vit(q, k, v, cu, int(max(sizes)))
+    Or, Lr, _ = oatt.vit_attention(wl.bf16_bits_to_f64(q), wl.bf16_bits_to_f64(k), wl.bf16_bits_to_f64(v),
+                                   cu, 1 / math.sqrt(d), with_mass=False)
+    assert np.max(np.abs(o - Or)) <= O_TOL * np.max(np.abs(Or))
+    assert np.max(np.abs(lse - Lr)) <= LSE_TOL
 
 
 def _run_prefill(p, d_override=None):
