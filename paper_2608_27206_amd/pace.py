@@ -325,8 +325,11 @@ def vit_attention(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, cu_seqlens:
         mass = None
     nseg = cu_seqlens.numel() - 1
     if workspace is None:
+        # the library needs a workspace for LSE scratch (mass without lse) and for the fp16 V^T
+        # tiles of the long-segment kernel; the size says which applies
         need = lib().pace_vit_attention_workspace_size(N, H, d, nseg, int(max_seglen))
-        if (mass is not None and lse is None) or need > N * H * 4 + 256:
+        lse_scratch = (N * H * 4 + 255) // 256 * 256
+        if (mass is not None and lse is None) or need > lse_scratch:
             workspace = _ws(need, dev)
     _check(lib().pace_vit_attention(_ptr(q), _ptr(k), _ptr(v), N, H, d, _ptr(cu_seqlens),
                                     cu_seqlens.numel() - 1, int(max_seglen), float(scale), _ptr(o),
