@@ -853,9 +853,12 @@ __global__ __launch_bounds__(kWinThreads) void attn_window(const FwdParams p, fl
   uint16_t* Vs = lds + kBN * C::KS;
   float* Pb = reinterpret_cast<float*>(lds);
 
+  // window-major order: the heads of a window are neighbours in the logical order, hence on
+  // the same XCD at about the same time, so the cache lines holding a token's rows of all
+  // heads (160 bytes per head) are fetched from HBM once and served from L2 for the others
   const int lb = remap_block_id(blockIdx.x, gridDim.x);
-  const int h = lb / p.nseg;
-  const int seg = lb - h * p.nseg;
+  const int seg = lb / p.Hq;
+  const int h = lb - seg * p.Hq;
   const int s0 = p.cu[seg];
   const int L = p.cu[seg + 1] - s0;
   if (L <= 0) return;   // the whole workgroup leaves together
