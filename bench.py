@@ -70,7 +70,7 @@ def parse():
 def main():
     a = parse()
     if a.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1 "
+        print(json.dumps({"error": "the benchmark runs on one GPU only; --gpus must be 1 "
                           "(multi-GPU sharding is described in the design notes, not built)"}))
         sys.exit(2)
     import numpy as np
