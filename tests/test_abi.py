@@ -95,6 +95,12 @@ def test_errors_before_launch():
     st = L.pace_ddae_select_varlen(fake, 1, 1, None, fake, 1, 1, nv, kk, 0, 0.5, 0.5, None, 0, fake,
                                    None, None, None, fake, 1 << 20, None)
     assert st == 1 and "K=11" in L.pace_last_error().decode()
+    # an image without tokens
+    nv0 = (ctypes.c_int * 1)(0)
+    k0 = (ctypes.c_int * 1)(0)
+    st = L.pace_ddae_select_varlen(fake, 1, 1, None, fake, 1, 1, nv0, k0, 0, 0.5, 0.5, None, 0, fake,
+                                   None, None, None, fake, 1 << 20, None)
+    assert st == 1 and "0 tokens" in L.pace_last_error().decode()
     # bad mode, tau
     kk[0] = 3
     st = L.pace_ddae_select_varlen(fake, 1, 1, None, fake, 1, 1, nv, kk, 2, 0.5, 0.5, None, 0, fake,

@@ -130,6 +130,17 @@ def test_vit_long_segment_value_range_d80(vscale):
     assert np.max(np.abs(lse - Lr)) <= LSE_TOL
 
 
+@pytest.mark.parametrize("sizes,d", [([0, 64, 0, 17, 0], 80),              # windows, fused mass
+                                     ([1100, 0, 0, 37, 1030, 0], 80),     # long-segment kernel
+                                     ([0, 300, 0, 129], 128)])            # general kernel
+def test_vit_empty_segments(sizes, d):
+    """Empty segments (equal neighbouring offsets) are skipped: the other segments' outputs,
+    LSE and mass match the oracle and every row's mass still sums over its own segment."""
+    cu = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int32)
+    q, k, v = _vit_case(51, cu, 2, d)
+    _check_vit(q, k, v, cu, d)
+
+
 def _run_prefill(p, d_override=None):
     from paper_2608_27206_amd import pace
     import torch
