@@ -141,6 +141,15 @@ def test_vit_empty_segments(sizes, d):
     _check_vit(q, k, v, cu, d)
 
 
+@pytest.mark.parametrize("sizes", [[1023], [1024], [1025, 63], [1087, 64, 1], [1152, 1151, 5]])
+def test_vit_long_segment_tile_boundaries_d80(sizes):
+    """Lengths around the long-segment kernel's threshold (1024 rows) and last tiles holding
+    1, 63 or 64 keys, with short segments in the same call."""
+    cu = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int32)
+    q, k, v = _vit_case(61 + len(sizes), cu, 2, 80)
+    _check_vit(q, k, v, cu, 80)
+
+
 def _run_prefill(p, d_override=None):
     from paper_2608_27206_amd import pace
     import torch
