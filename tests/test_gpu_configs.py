@@ -1,0 +1,93 @@
+"""GPU parity of the whole hot path on the 448 x 448 and 1344 x 1344 workloads, against the
+float64 oracle, element by element: APC density and distances, the window attention (O, LSE,
+mass), the full attention of the image (forward, then the mass pass, as bench.py runs them;
+at 1344 x 1344 four of the sixteen heads), the causal prefill with the text-query mass of every
+visual key, and the DDAE selection fed the GPU's own masses (fused scores, kept set, gathered
+rows).  Bars as in the other parity tests: O 2e-2, LSE 1e-3, mass 1e-3 relative, APC 1e-4,
+fused scores 1e-5, kept sets equal up to swaps inside a 1e-3 score band, gather bitwise."""
+import math
+
+import numpy as np
+import pytest
+
+from oracle import apc as oapc
+from oracle import attention as oatt
+from oracle import ddae as oddae
+from paper_2608_27206_amd import workloads as wl
+from tests.gpu_util import (dev_bf16, dev_i32, dev_u8, host, host_bf16_to_f64, kept_sets_agree,
+                            mass_ok, say)
+
+pytestmark = pytest.mark.gpu
+
+O_TOL, LSE_TOL = 2e-2, 1e-3
+
+
+def _f64(bits):
+    return wl.bf16_bits_to_f64(bits)
+
+
+@pytest.mark.parametrize("config_id,heads", [(1, list(range(16))), (2, [0, 5, 10, 15])])
+def test_hot_path_end_to_end(config_id, heads):
+    from paper_2608_27206_amd import pace
+    import torch
+    w = wl.make_workload(config_id)
+    vit, pre, L = w.vit, w.prefill, w.layouts[0]
+    N = vit.q.shape[0]
+    say(f"config {config_id}: {N} patches, {L.n_vis} visual tokens, prefill {pre.q.shape[0]}")
+
+    # a1: APC density
+    rho, d = pace.apc_density(dev_u8(w.images[0]), 14, 0.10, 0.6, 1.5)
+    torch.cuda.synchronize()
+    ref = oapc.apc_density(w.images[0])
+    np.testing.assert_allclose(host(d), ref["d"], atol=1e-4)
+    np.testing.assert_allclose(host(rho), [ref["rho_g"], ref["rho_d"], ref["rho"], ref["phi"]], atol=1e-4)
+
+    Q, K, V = dev_bf16(vit.q), dev_bf16(vit.k), dev_bf16(vit.v)
+    # a3: windows, one pass with the mass
+    cw = vit.cu_windows
+    ow, lw, mw = pace.vit_attention(Q, K, V, dev_i32(cw), int(np.diff(cw).max()))
+    torch.cuda.synchronize()
+    Or, Lr, Mr = oatt.vit_attention(_f64(vit.q), _f64(vit.k), _f64(vit.v), cw, 1 / math.sqrt(80))
+    assert np.max(np.abs(host_bf16_to_f64(ow) - Or)) <= O_TOL
+    assert np.max(np.abs(host(lw) - Lr)) <= LSE_TOL
+    err, rel = mass_ok(host(mw), Mr, 64)
+    assert err <= 0, rel
+
+    # a4: full attention of the image, forward then the mass pass
+    cf = dev_i32(vit.cu_full)
+    of, lf, _ = pace.vit_attention(Q, K, V, cf, N, want_mass=False)
+    mf = pace.vit_attention_mass(Q, K, cf, N, lf)
+    torch.cuda.synchronize()
+    of, lf, mf = host_bf16_to_f64(of), host(lf), host(mf)
+    hs = np.asarray(heads)
+    Or, Lr, Mr = oatt.vit_attention(_f64(vit.q[:, hs]), _f64(vit.k[:, hs]), _f64(vit.v[:, hs]), vit.cu_full,
+                                    1 / math.sqrt(80))
+    assert np.max(np.abs(of[:, hs] - Or)) <= O_TOL
+    assert np.max(np.abs(lf[hs] - Lr)) <= LSE_TOL
+    err, rel = mass_ok(mf[hs], Mr, N)
+    assert err <= 0, rel
+
+    # a5: causal prefill and the text-query mass of every visual key
+    nv, nt = int(pre.vis_len[0]), int(pre.text_len[0])
+    S = nv + nt
+    _, _, ml = pace.prefill_attention_with_mass(
+        dev_bf16(pre.q), dev_bf16(pre.k), dev_bf16(pre.v), dev_i32(pre.cu_seqlens), S, dev_i32(pre.vis_len),
+        dev_i32(pre.cu_vis), nv, nv, dev_i32(pre.mq_start), dev_i32(pre.mq_len), nt)
+    torch.cuda.synchronize()
+    ml_h = host(ml)
+    _, _, Ml = oatt.prefill_attention(_f64(pre.q), _f64(pre.k), _f64(pre.v), pre.cu_seqlens, pre.vis_len,
+                                      pre.mq_start, pre.mq_len, 1 / math.sqrt(pre.q.shape[2]))
+    err, rel = mass_ok(ml_h, Ml[:, :nv], nt)
+    assert err <= 0, rel
+
+    # a6-a8: the selection on the GPU's own masses, against the oracle fed the same masses
+    Kk = oddae.keep_count(w.keep_ratio, nv)
+    idx, sc, fz, out = pace.ddae_select(torch.from_numpy(mf).cuda(), 4, dev_i32(L.vis_perm), ml, [nv], [Kk],
+                                        mode=w.fusion_mode, tau=w.tau, hidden=dev_bf16(w.hidden))
+    torch.cuda.synchronize()
+    S_ref, st = oddae.fuse(mf.astype(np.float64), ml_h.astype(np.float64), 4, L.vis_perm, w.fusion_mode, w.tau)
+    np.testing.assert_allclose(host(sc), S_ref, atol=1e-5)
+    np.testing.assert_allclose(host(fz)[0], st, atol=1e-5)
+    ok, msg = kept_sets_agree(host(idx), oddae.topk_indices(S_ref, Kk), S_ref)
+    assert ok, msg
+    np.testing.assert_array_equal(out.view(torch.int16).cpu().numpy().view(np.uint16), w.hidden[host(idx)])
