@@ -248,11 +248,37 @@ def main():
             "density_gbs": round(bytes_apc / (per["apc"] * 1e-3) / 1e9, 1) if per["apc"] > 0 else None,
             "resize_gbs": round(bytes_resize / (per["resize"] * 1e-3) / 1e9, 1) if per["resize"] > 0 else None,
         },
+        # every step of the path against the roofline that bounds it (algorithmic work per step)
+        "steps": {
+            "apc_density": _hbm_row(bytes_apc, per["apc"]),
+            "apc_downsample": _hbm_row(bytes_resize, per["resize"]),
+            "vit_window_attention": _hbm_row(bytes_win, per["vit_win"]),
+            "vit_full_attention_fwd": _mfma_row(flop_full, per["vit_fwd"]),
+            "vit_full_attention_fwd_plus_mass": _mfma_row(flop_full, per["vit_fwd"] + per["vit_mass"]),
+            "prefill_attention_with_mass": _mfma_row(flop_pre, per["prefill"]),
+            "ddae_select_gather": _hbm_row(bytes_sel, per["select"]),
+        },
         "next": nxt,
     }
     if a.cpu_seconds > 0:
         result["cpu_baseline"] = cpu_baseline(vit, a.cpu_seconds)
     print(json.dumps(result), flush=True)
+
+
+def _hbm_row(nbytes, ms):
+    if ms <= 0:
+        return None
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    return {"bound": "hbm", "ms": round(ms, 4), "algorithmic_bytes": int(nbytes), "achieved": round(gbs, 1),
+            "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4)}
+
+
+def _mfma_row(flop, ms):
+    if ms <= 0:
+        return None
+    tf = flop / (ms * 1e-3) / 1e12
+    return {"bound": "mfma", "ms": round(ms, 4), "algorithmic_flop": float(flop), "achieved": round(tf, 1),
+            "unit": "TFLOP/s", "frac": round(tf / PEAK_BF16_TFLOPS, 4)}
 
 
 def measure_next(pace, pq, pk, pv, p_cu, S, p_vis, p_cuv, Nv, T, idx, K, stream, reps=5):
