@@ -1130,7 +1130,9 @@ pace_status_t pace_apc_downsample(const uint8_t* src, int H, int W, uint8_t* dst
   // guard tap on each side)
   p.ntx = static_cast<int>(ceil(4.0 * (sx > 1 ? sx : 1))) + 4;
   p.nty = static_cast<int>(ceil(4.0 * (sy > 1 ? sy : 1))) + 4;
-  int ty = 16, tx = 64;
+  // 16 x 32 output pixels per workgroup: small enough LDS for three or more workgroups per CU
+  // (the image latency of one is hidden by the others), large enough to amortise the taps' halo
+  int ty = 16, tx = 32;
   auto plan = [&](int t_y, int t_x, ResizeParams& q) {
     q.ty = t_y; q.tx = t_x;
     q.rows_cap = static_cast<int>(ceil((t_y - 1) * sy)) + q.nty + 1;
