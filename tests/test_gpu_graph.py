@@ -1,0 +1,112 @@
+"""The hot path captured in a HIP graph (torch.cuda.CUDAGraph around the C-ABI calls on the
+capturing stream): every replay must reproduce the eager results bit for bit.  The kernels use
+fixed reduction orders and no float atomics, and with caller-provided workspaces the library
+neither allocates nor records memset or copy nodes, so a replay repeats the same computation.  The
+graph is replayed three times, with the program's own eager work and synchronisations between the
+replays, and every replay is checked."""
+import numpy as np
+import pytest
+
+from paper_2608_27206_amd import workloads as wl
+from tests.gpu_util import dev_bf16, dev_i32, dev_u8, say
+
+pytestmark = pytest.mark.gpu
+
+
+def _path(pace, inp, out):
+    """One pass of the whole path into preallocated outputs."""
+    pace.apc_density(inp["img"], 14, 0.10, 0.6, 1.5, d_out=out["d"], rho_out=out["rho"], workspace=inp["ws_apc"])
+    pace.apc_downsample(inp["img"], 224, 224, dst=out["small"])
+    pace.vit_attention(inp["q"], inp["k"], inp["v"], inp["cu_win"], inp["max_win"], o=out["o_win"],
+                       lse=out["lse_win"], mass=out["mass_win"])
+    pace.vit_attention(inp["q"], inp["k"], inp["v"], inp["cu_full"], inp["N"], o=out["o_full"],
+                       lse=out["lse_full"], want_mass=False, workspace=inp["ws_vit"])
+    pace.vit_attention_mass(inp["q"], inp["k"], inp["cu_full"], inp["N"], out["lse_full"], mass=out["mass_vis"])
+    pace.prefill_attention_with_mass(inp["pq"], inp["pk"], inp["pv"], inp["p_cu"], inp["S"], inp["p_vis"],
+                                     inp["p_cuv"], inp["nv"], inp["nv"], inp["p_mqs"], inp["p_mql"], inp["T"],
+                                     o=out["o_pre"], lse=out["lse_pre"], mass=out["mass_llm"])
+    pace.ddae_select(out["mass_vis"], 4, inp["perm"], out["mass_llm"], [inp["nv"]], [inp["K"]],
+                     mode=inp["mode"], tau=inp["tau"], hidden=inp["hidden"], idx_out=out["idx"],
+                     score_out=out["scores"], fuse_out=out["fuse"], out=out["kept"], workspace=inp["ws_sel"])
+
+
+def _outputs(torch, inp):
+    dev = inp["q"].device
+    N, nv, K = inp["N"], inp["nv"], inp["K"]
+    H, Hq, Ntot = inp["q"].shape[1], inp["pq"].shape[1], inp["pq"].shape[0]
+    f32 = dict(dtype=torch.float32, device=dev)
+    return {
+        "d": torch.empty(N, **f32), "rho": torch.empty(4, **f32),
+        "small": torch.empty((224, 224, 3), dtype=torch.uint8, device=dev),
+        "o_win": torch.empty_like(inp["q"]), "lse_win": torch.empty((H, N), **f32),
+        "mass_win": torch.empty((H, N), **f32),
+        "o_full": torch.empty_like(inp["q"]), "lse_full": torch.empty((H, N), **f32),
+        "mass_vis": torch.empty((H, N), **f32),
+        "o_pre": torch.empty_like(inp["pq"]), "lse_pre": torch.empty((Hq, Ntot), **f32),
+        "mass_llm": torch.empty((Hq, nv), **f32),
+        "idx": torch.empty(K, dtype=torch.int32, device=dev), "scores": torch.empty(nv, **f32),
+        "fuse": torch.empty((1, 4), **f32),
+        "kept": torch.empty((K,) + tuple(inp["hidden"].shape[1:]), dtype=torch.bfloat16, device=dev),
+    }
+
+
+def _bitwise_equal(torch, a, b):
+    view = {torch.float32: torch.int32, torch.bfloat16: torch.int16}.get(a.dtype)
+    if view is not None:
+        a, b = a.view(view), b.view(view)
+    return bool(torch.equal(a, b))
+
+
+def test_graph_replays_match_eager():
+    from paper_2608_27206_amd import pace
+    import torch
+    dev = torch.device("cuda")
+    w = wl.make_workload(1)
+    vit, pre, L = w.vit, w.prefill, w.layouts[0]
+    N, nv, T = vit.q.shape[0], int(pre.vis_len[0]), int(pre.text_len[0])
+    inp = {"img": dev_u8(w.images[0]), "q": dev_bf16(vit.q), "k": dev_bf16(vit.k), "v": dev_bf16(vit.v),
+           "cu_win": dev_i32(vit.cu_windows), "max_win": int(np.diff(vit.cu_windows).max()),
+           "cu_full": dev_i32(vit.cu_full), "N": N,
+           "pq": dev_bf16(pre.q), "pk": dev_bf16(pre.k), "pv": dev_bf16(pre.v), "p_cu": dev_i32(pre.cu_seqlens),
+           "p_vis": dev_i32(pre.vis_len), "p_cuv": dev_i32(pre.cu_vis), "p_mqs": dev_i32(pre.mq_start),
+           "p_mql": dev_i32(pre.mq_len), "S": nv + T, "T": T, "nv": nv, "perm": dev_i32(L.vis_perm),
+           "K": pace.keep_count(w.keep_ratio, nv), "mode": w.fusion_mode, "tau": w.tau,
+           "hidden": dev_bf16(w.hidden)}
+    lib = pace.lib()
+    H, W = w.images[0].shape[:2]
+    inp["ws_apc"] = torch.empty(lib.pace_apc_density_workspace_size(H, W, 14), dtype=torch.uint8, device=dev)
+    inp["ws_vit"] = torch.empty(lib.pace_vit_attention_workspace_size(N, vit.q.shape[1], vit.q.shape[2], 1, N),
+                                dtype=torch.uint8, device=dev)
+    inp["ws_sel"] = torch.empty(lib.pace_ddae_select_workspace_size(nv, 1), dtype=torch.uint8, device=dev)
+
+    say(f"graph test: {H}x{W} image, {N} patches, {nv} visual tokens, keep {inp['K']}")
+    eager = _outputs(torch, inp)
+    _path(pace, inp, eager)
+    torch.cuda.synchronize()
+
+    cap = _outputs(torch, inp)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        _path(pace, inp, cap)            # a warm-up pass on a side stream before capture
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        _path(pace, inp, cap)
+    torch.cuda.synchronize()
+    say("captured")
+
+    other = _outputs(torch, inp)
+    for rep in range(3):
+        for t in cap.values():
+            t.fill_(7)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for name, ref in eager.items():
+            assert _bitwise_equal(torch, cap[name], ref), f"replay {rep}: {name} differs from the eager pass"
+        say(f"replay {rep} matches")
+        _path(pace, inp, other)          # the program's own eager work between replays
+        torch.cuda.synchronize()
+        assert _bitwise_equal(torch, other["idx"], eager["idx"])
