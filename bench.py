@@ -64,7 +64,33 @@ def parse():
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="before warm-up, copy this many MiB device to device once (a plain copy "
                          "of known size that calibrates the HBM byte counters of a profile run)")
+    ap.add_argument("--no-graph", dest="graph", action="store_false",
+                    help="skip timing the step captured in a HIP graph and replayed")
     return ap.parse_args()
+
+
+def time_graph_replays(torch, step, stream, steps):
+    """The same step captured once in a HIP graph and replayed `steps` times (after the timed eager
+    steps, outside their region): the per-step time without host launch overhead."""
+    side = torch.cuda.Stream()
+    side.wait_stream(stream)
+    with torch.cuda.stream(side):
+        step(None)
+    stream.wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        step(None)
+    g.replay()
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(steps):
+        g.replay()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / steps
 
 
 def main():
@@ -191,6 +217,7 @@ def main():
         for n in names:
             per[n] += ev[n][0].elapsed_time(ev[n][1])
     per = {n: v / a.steps for n, v in per.items()}
+    graph_ms = time_graph_replays(torch, step, stream, a.steps) if a.graph else None
     nxt = measure_next(pace, pq, pk, pv, p_cu, S, p_vis, p_cuv, Nv, T, idx, K, stream)
     nxt["preview_block"] = measure_preview(pace, wl, img, L, stream)
 
@@ -231,6 +258,7 @@ def main():
                      "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
                      "traffic": measured_traffic()},
         "breakdown_ms": {n: round(v, 4) for n, v in per.items()},
+        "graph_ms_per_step": None if graph_ms is None else round(graph_ms, 4),
         "attention": {
             "vit_full_fwd_tflops": round(achieved, 2),
             "vit_full_fwd_plus_mass_tflops": round(flop_full / ((per["vit_fwd"] + per["vit_mass"]) * 1e-3) / 1e12, 2)
