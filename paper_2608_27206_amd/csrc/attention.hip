@@ -81,6 +81,15 @@ __device__ __forceinline__ bf16x8 pack_bf16x8(const float* x) {
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// max of three floats in one instruction.  fmaxf on values fresh from an MFMA costs an extra
+// canonicalising v_max per operand; the inputs here are finite or -inf, never NaN, so the
+// plain instruction gives the same result.
+__device__ __forceinline__ float vmax3(float a, float b, float c) {
+  float r;
+  asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+  return r;
+}
+
 // Buffer resource over `bytes` bytes from `base`: loads at offsets past the end return 0
 // (the hardware range check), so tile loads need neither branches nor clamps.  The whole
 // offset always goes in the VGPR operand, which the range check covers.
@@ -120,6 +129,17 @@ __device__ __forceinline__ void dma16(i32x4 r, unsigned lds, unsigned voff) {
                :: "s"(m0), "v"(voff), "s"(r) : "memory", "m0");
 }
 __device__ __forceinline__ void wait_vmem() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+// The same resource moved `bytes` forward (base up, size down by the same amount): an offset v
+// into the result reads what v + bytes reads from the original, range check included.  Scalar
+// arithmetic only, so a loop that walks tiles keeps its per-lane offsets constant.
+__device__ __forceinline__ i32x4 rsrc_advance(i32x4 r, unsigned bytes) {
+  const unsigned long long a =
+      ((static_cast<unsigned long long>(static_cast<unsigned>(r.y)) & 0xffffull) << 32 | static_cast<unsigned>(r.x)) + bytes;
+  r.x = static_cast<int>(a & 0xffffffffull);
+  r.y = (r.y & ~0xffff) | static_cast<int>((a >> 32) & 0xffffull);
+  r.z = static_cast<int>(static_cast<unsigned>(r.z) - bytes);
+  return r;
+}
 // As dma16 with 4 bytes per lane (lds + 4 * lane).
 __device__ __forceinline__ void dma4(i32x4 r, unsigned lds, unsigned voff) {
   const unsigned m0 = __builtin_amdgcn_readfirstlane(lds);
@@ -566,7 +586,7 @@ constexpr int kVtStride = kBN + 8;                    // LDS row stride of a V^T
 constexpr int kVtChunks = kVtRows * (kVtStride / 8);  // 16-byte DMA chunks per V^T tile
 constexpr int kVtInst = (kVtChunks + 63) / 64;        // wave-wide DMA loads per V^T tile
 constexpr int kVtPW = (kVtInst + 3) / 4;              // per wave of group 0
-constexpr int kA1Vals = 14;                           // exponentials per lane in phase A1 (of 32)
+constexpr int kA1Vals = 16;                           // exponentials per lane in phase A1 (of 32)
 constexpr float kP16Shift = 7.0f;                     // log2 of P's scale factor
 
 // Row order of K in S^T = K Q^T: bits 2 and 3 of the row index swapped (an involution).
@@ -629,14 +649,17 @@ __global__ __launch_bounds__(kRotThreads, 1) void attn_fwd_rot(const FwdParams p
   });
   const unsigned tile_bytes = static_cast<unsigned>(kBN * kvstride) * 2u;
   const unsigned ks_lds = lds_u32(&Ks[0][0]), vt_lds = lds_u32(&Vt[0][0]);
+  // tile t of K and V^T: the resources move to the tile (scalar work), the lane offsets stay
   auto load_kv = [&](int t, int kbuf, int vbuf) __attribute__((always_inline)) {
+    const i32x4 rkt = rsrc_advance(rk, static_cast<unsigned>(t) * tile_bytes);
+    const i32x4 rvtt = rsrc_advance(rvt, static_cast<unsigned>(t) * (kBN * 2));
     static_for<0, C::KPW>([&](auto I) __attribute__((always_inline)) {
       if (wl + 4 * I < C::KINST)
-        dma16(rk, ks_lds + (kbuf * kBN * C::KS + (wl + 4 * I) * 512) * 2, koff[I] + t * tile_bytes);
+        dma16(rkt, ks_lds + (kbuf * kBN * C::KS + (wl + 4 * I) * 512) * 2, koff[I]);
     });
     static_for<0, kVtPW>([&](auto I) __attribute__((always_inline)) {
       if (wl + 4 * I < kVtInst)
-        dma16(rvt, vt_lds + (vbuf * C::DV * kVtStride + (wl + 4 * I) * 512) * 2, vtoff[I] + t * (kBN * 2));
+        dma16(rvtt, vt_lds + (vbuf * C::DV * kVtStride + (wl + 4 * I) * 512) * 2, vtoff[I]);
     });
   };
 
@@ -657,7 +680,8 @@ __global__ __launch_bounds__(kRotThreads, 1) void attn_fwd_rot(const FwdParams p
 #pragma unroll
   for (int t2 = 0; t2 < C::NT; ++t2) oacc[t2] = f32x16{};
   float m_used = -INFINITY;
-  float m_off = 0.f;
+  float m_thresh = -INFINITY;   // m_used + kRescaleSlack
+  float m_off = 0.f;            // m_used - kP16Shift (set at the first tile, whose max is finite)
   uint32_t pw[2][2][4];   // packed fp16 P^T: [half][16-key chunk][pair]
 
   // exponentials and fp16 packing of values [R0, R1) of the 32 per lane (pairs)
@@ -678,37 +702,39 @@ __global__ __launch_bounds__(kRotThreads, 1) void attn_fwd_rot(const FwdParams p
     if (kt + kBN > L) {
       // register r of half st holds key kt + 32 st + swap_bits23(8 (r / 4) + 4 g + r % 4),
       // that is kt + 8 g + a constant
-      const int lim = L - kt - 8 * g;
+      const int lim = __builtin_amdgcn_readfirstlane(L - kt) - 8 * g;
 #pragma unroll
       for (int st = 0; st < 2; ++st)
 #pragma unroll
         for (int r = 0; r < 16; ++r)
           if (st * 32 + 16 * (r >> 3) + 4 * ((r >> 2) & 1) + (r & 3) >= lim) s[st][r] = -INFINITY;
     }
-    float m1[11];
+    // 32 values in 16 three-way maxima: 10 triples, the last pair folded into the first
+    float m1[10];
 #pragma unroll
     for (int i = 0; i < 10; ++i) {
       const int a = 3 * i;
-      m1[i] = fmaxf(fmaxf(s[a >> 4][a & 15], s[(a + 1) >> 4][(a + 1) & 15]), s[(a + 2) >> 4][(a + 2) & 15]);
+      m1[i] = vmax3(s[a >> 4][a & 15], s[(a + 1) >> 4][(a + 1) & 15], s[(a + 2) >> 4][(a + 2) & 15]);
     }
-    m1[10] = fmaxf(s[1][14], s[1][15]);
-    const float m2a = fmaxf(fmaxf(m1[0], m1[1]), m1[2]), m2b = fmaxf(fmaxf(m1[3], m1[4]), m1[5]);
-    const float m2c = fmaxf(fmaxf(m1[6], m1[7]), m1[8]), m2d = fmaxf(m1[9], m1[10]);
-    float mx = fmaxf(fmaxf(m2a, m2b), fmaxf(m2c, m2d));
+    m1[0] = vmax3(m1[0], s[1][14], s[1][15]);
+    const float m2a = vmax3(m1[0], m1[1], m1[2]), m2b = vmax3(m1[3], m1[4], m1[5]);
+    const float m2c = vmax3(m1[6], m1[7], m1[8]);
+    float mx = vmax3(vmax3(m2a, m2b, m2c), m1[9], m1[9]);
     {   // the two half-waves hold the same query rows: exchange halves without an LDS round trip
       const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
-      mx = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1])) * p.scale_log2;
+      mx = vmax3(__uint_as_float(sw[0]), __uint_as_float(sw[1]), __uint_as_float(sw[1])) * p.scale_log2;
     }
-    if (__builtin_amdgcn_ballot_w64(mx > m_used + kRescaleSlack) != 0ull) {
+    if (__builtin_amdgcn_ballot_w64(mx > m_thresh) != 0ull) {
       const float m_new = fmaxf(m_used, mx);
       const float alpha = fast_exp2(m_used - m_new);
       m_used = m_new;
+      m_thresh = m_new + kRescaleSlack;
+      m_off = m_new - kP16Shift;
 #pragma unroll
       for (int t2 = 0; t2 < C::NT; ++t2)
 #pragma unroll
         for (int r = 0; r < 16; ++r) oacc[t2][r] *= alpha;
     }
-    m_off = (m_used == -INFINITY) ? 0.f : m_used - kP16Shift;
     exps(std::integral_constant<int, 0>{}, std::integral_constant<int, kA1Vals>{});
   };
 
