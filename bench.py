@@ -277,7 +277,7 @@ def main():
             "resize_gbs": round(bytes_resize / (per["resize"] * 1e-3) / 1e9, 1) if per["resize"] > 0 else None,
         },
         # every step of the path against the roofline that bounds it (algorithmic work per step)
-        "steps": {
+        "step_roofline": {
             "apc_density": _hbm_row(bytes_apc, per["apc"]),
             "apc_downsample": _hbm_row(bytes_resize, per["resize"]),
             "vit_window_attention": _hbm_row(bytes_win, per["vit_win"]),
