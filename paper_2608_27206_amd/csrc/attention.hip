@@ -339,19 +339,22 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd(const FwdParams p) {
           if (!ok) s[st][r] = -INFINITY;
         }
     }
-    // max over the 32 in-lane values as a shallow tree of three-input maxima, then across
-    // the half-waves
-    float m1[11];
+    // max over the 32 in-lane values in 16 three-input maxima (10 triples, the last pair folded
+    // into the first), then across the half-waves, which hold the same query rows
+    float m1[10];
 #pragma unroll
     for (int i = 0; i < 10; ++i) {
       const int a = 3 * i;
-      m1[i] = fmaxf(fmaxf(s[a >> 4][a & 15], s[(a + 1) >> 4][(a + 1) & 15]), s[(a + 2) >> 4][(a + 2) & 15]);
+      m1[i] = vmax3(s[a >> 4][a & 15], s[(a + 1) >> 4][(a + 1) & 15], s[(a + 2) >> 4][(a + 2) & 15]);
     }
-    m1[10] = fmaxf(s[1][14], s[1][15]);
-    const float m2a = fmaxf(fmaxf(m1[0], m1[1]), m1[2]), m2b = fmaxf(fmaxf(m1[3], m1[4]), m1[5]);
-    const float m2c = fmaxf(fmaxf(m1[6], m1[7]), m1[8]), m2d = fmaxf(m1[9], m1[10]);
-    float mx = fmaxf(fmaxf(m2a, m2b), fmaxf(m2c, m2d));
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * p.scale_log2;
+    m1[0] = vmax3(m1[0], s[1][14], s[1][15]);
+    const float m2a = vmax3(m1[0], m1[1], m1[2]), m2b = vmax3(m1[3], m1[4], m1[5]);
+    const float m2c = vmax3(m1[6], m1[7], m1[8]);
+    float mx = vmax3(vmax3(m2a, m2b, m2c), m1[9], m1[9]);
+    {
+      const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
+      mx = vmax3(__uint_as_float(sw[0]), __uint_as_float(sw[1]), __uint_as_float(sw[1])) * p.scale_log2;
+    }
     // lazy rescale: only when some row's max moved up by more than the slack
     if (__builtin_amdgcn_ballot_w64(mx > m_used + kRescaleSlack) != 0ull) {
       const float m_new = fmaxf(m_used, mx);
