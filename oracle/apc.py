@@ -152,8 +152,9 @@ def embedding_density(x: np.ndarray, tail_frac: float = TAIL_FRAC, alpha: float 
 
 
 # ---------------------------------------------------------------- pixel-statistic previews
-# The preview ablation replaces the shallow ViT feature with four training-free pixel statistics
-# (RGB statistics, colour entropy, edge density, Laplacian) without defining them.  Readings
+# Pixel-statistic previews of the preview-signal study (Appendix, shallow feature preview
+# ablation): RGB statistics, colour entropy, edge density and a Laplacian, named there as
+# weight-free stand-ins for the first encoder block but not given as formulas.  Readings
 # (listed in the design notes): each is a vector per patch, so that the cosine-based density
 # steps apply unchanged (a scalar per patch would make every cosine +-1):
 #   0 RGB statistics  mean and population std of each channel of x/255      (6 values)

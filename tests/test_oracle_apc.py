@@ -223,6 +223,16 @@ def test_pixel_statistics_shapes_and_closed_forms():
     flat[...] = (10, 200, 255)
     f = apc.pixel_statistic_features(flat, 14, 0)
     np.testing.assert_allclose(f[0], [10 / 255, 200 / 255, 1.0, 0, 0, 0], atol=1e-14)
+    # population std (ddof 0): half the pixels 0 and half 255 give mean 0.5 and std 0.5 in every
+    # channel; a quarter at 255 gives mean 1/4 and std sqrt(1/4 * 3/4) (ddof 1 would scale the
+    # spread by sqrt(196/195))
+    split = np.zeros((14, 14, 3), np.uint8)
+    split[:, :7] = 255
+    np.testing.assert_allclose(apc.pixel_statistic_features(split, 14, 0)[0], [0.5] * 6, atol=1e-14)
+    quarter = np.zeros((14, 14, 3), np.uint8)
+    quarter[:7, :7] = 255
+    np.testing.assert_allclose(apc.pixel_statistic_features(quarter, 14, 0)[0],
+                               [0.25] * 3 + [math.sqrt(3) / 4] * 3, atol=1e-14)
     # colour entropy: the terms of a patch sum to its entropy; half black half white -> ln 2
     half = np.zeros((14, 14, 3), np.uint8)
     half[:7] = 255

@@ -168,3 +168,52 @@ def test_rows_subset_matches_full():
     o2, l2 = oatt.attention_rows(q, k, v, 0, 30, rows, True, 0.3)
     np.testing.assert_allclose(o2, O[rows], atol=1e-14)
     np.testing.assert_allclose(l2, L[:, rows], atol=1e-14)
+
+
+def test_chunked_rows_match_brute_force():
+    """The oracle walks query rows in chunks and adds each chunk's column sums into the mass;
+    with a chunk of 4 rows over segments of 11 and 13 tokens (three and four chunks, ragged last
+    ones) O, LSE and the mass must still equal the pure-Python brute force, so a chunk that
+    overwrote instead of adding, or an offset slip between chunks, fails here."""
+    rs = np.random.default_rng(11)
+    q = rs.standard_normal((24, 2, 3))
+    k = rs.standard_normal((24, 2, 3))
+    v = rs.standard_normal((24, 2, 4))
+    segs = [(0, 11), (11, 24)]
+    for causal in (False, True):
+        for a, b in segs:
+            O, L, M = oatt.attention_segment(q[a:b], k[a:b], v[a:b], causal, 0.6,
+                                             mass_rows=np.arange(b - a), chunk=4)
+            Ob, Lb, Mb = _brute(q[a:b], k[a:b], v[a:b], [(0, b - a)], causal, 0.6, lambda x, y: range(x, y))
+            np.testing.assert_allclose(O, Ob, atol=1e-12)
+            np.testing.assert_allclose(L, Lb, atol=1e-12)
+            np.testing.assert_allclose(M, Mb, atol=1e-12)
+    # a subset of rows, and mass rows that start inside a chunk and span three of them
+    rows = [1, 2, 7, 10]
+    O, L, M = oatt.attention_segment(q[:11], k[:11], v[:11], True, 0.6, rows=rows,
+                                     mass_rows=np.arange(2, 11), chunk=4)
+    Ob, Lb, Mb = _brute(q[:11], k[:11], v[:11], [(0, 11)], True, 0.6, lambda x, y: range(2, 11))
+    np.testing.assert_allclose(O, Ob[rows], atol=1e-12)
+    np.testing.assert_allclose(L, Lb[:, rows], atol=1e-12)
+    np.testing.assert_allclose(M, Mb, atol=1e-12)
+
+
+def test_default_chunk_past_one_chunk():
+    """More rows than the default chunk (600 > 512): O and LSE against torch's float64 SDPA, and
+    each head's mass against the closed total (every row's probabilities sum to one) and a
+    direct float64 column sum of the full probability matrix."""
+    torch = pytest.importorskip("torch")
+    import torch.nn.functional as F
+    rs = np.random.default_rng(12)
+    n, h, d = 600, 2, 8
+    q = rs.standard_normal((n, h, d))
+    k = rs.standard_normal((n, h, d))
+    v = rs.standard_normal((n, h, d))
+    O, L, M = oatt.attention_segment(q, k, v, False, 1 / math.sqrt(d), mass_rows=np.arange(n))
+    qt, kt, vt = (torch.from_numpy(x).permute(1, 0, 2).contiguous() for x in (q, k, v))
+    ref = F.scaled_dot_product_attention(qt, kt, vt).permute(1, 0, 2).numpy()
+    np.testing.assert_allclose(O, ref, atol=1e-12)
+    S = torch.einsum("qhd,khd->hqk", torch.from_numpy(q), torch.from_numpy(k)) / math.sqrt(d)
+    np.testing.assert_allclose(L, torch.logsumexp(S, dim=2).numpy(), atol=1e-12)
+    np.testing.assert_allclose(M, torch.softmax(S, dim=2).sum(dim=1).numpy(), atol=1e-10)
+    np.testing.assert_allclose(M.sum(axis=1), n, rtol=1e-12)
