@@ -242,7 +242,8 @@ pace_status_t pace_apc_downsample(const uint8_t* src, int H, int W, uint8_t* dst
 /*
  * Workspace bytes for pace_vit_attention with these arguments: LSE scratch (used when
  * lse == NULL and mass != NULL) and, when d == 80 and max_seglen >= 1024 (the long-segment
- * kernel), fp16 V^T tiles of H * 81 * (8 ceil(N/8) + 8 nseg) values.
+ * kernel), fp16 V^T tiles of H * 81 * (64 ceil(N/64) + 64 nseg) values plus nseg * H
+ * per-(segment, head) maxima of |v|.
  */
 size_t pace_vit_attention_workspace_size(int N, int H, int d, int nseg, int max_seglen);
 
@@ -260,8 +261,11 @@ size_t pace_vit_attention_workspace_size(int N, int H, int d, int nseg, int max_
  *             of P_h[i, j] (column sums of the normalised probabilities), or NULL.
  * The mass pass needs the LSE: when lse is NULL and mass is not, the workspace
  * holds it.  At d == 80 with max_seglen >= 1024 the workspace is always required: the
- * long-segment kernel runs the PV product in fp16 on V^T tiles it writes there, so V's
- * elements must lie within fp16's range (|v| <= 65504; below 2^-14 they keep fewer bits).
+ * long-segment kernel runs the PV product in fp16 on V^T tiles it writes there, each
+ * (segment, head) scaled by a power of two that puts its largest |v| in [2^15, 2^16) and
+ * undone on the output, so any finite bf16 V is converted exactly (values below 2^-32 of
+ * their (segment, head)'s largest keep fewer bits); such segments allow at most 256 heads
+ * (UNSUPPORTED otherwise).
  * The workspace must be 16-byte aligned, pace_vit_attention_workspace_size bytes.
  * Requires N >= 1, H >= 1, nseg >= 1.
  */

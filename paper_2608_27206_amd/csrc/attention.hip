@@ -184,6 +184,7 @@ struct FwdParams {
   float scale_log2;        // scale * log2(e)
   const uint16_t* vt;      // fp16 V^T tiles (rotation kernel only)
   long long vt_cols;
+  const uint32_t* vt_amax; // [nseg, Hkv] largest |v| per (segment, KV head) as bf16 bits (rotation only)
 };
 
 constexpr int kBM = 128;   // query rows per workgroup
@@ -504,14 +505,27 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd(const FwdParams p) {
 // K runs through three LDS buffers (read in phase B of the tile before), V^T through four
 // (read in phase B of its own tile, up to three slots later).
 
-// fp16 V^T tiles in the workspace, [H][kVtRows][vt_cols]: segment s owns the 16-byte aligned
-// columns [vt_start(s), vt_start(s+1)), vt_start(s) = 8 ceil(cu[s] / 8) + 8 s; column
-// vt_start(s) + j holds key j of the segment for j < L_s and zero past it (so every column
-// a tile reads is finite).  Rows 0..79 are V^T, row 80 is one for the segment's keys.
+// fp16 V^T tiles in the workspace, [H][kVtRows][vt_cols]: segment s owns the 64-column
+// aligned range [vt_start(s), vt_start(s+1)), vt_start(s) = 64 ceil(cu[s] / 64) + 64 s, which
+// is at least 64 ceil(L_s / 64) columns wide, so no 64-key tile reads another segment's
+// columns.  Column vt_start(s) + j holds key j of the segment for j < L_s and zero past it.
+// Rows 0..79 are V^T scaled by 2^n (n = vt_shift of the segment and KV head, exact: a power of
+// two), row 80 is one for the segment's keys.
 constexpr int kVtRows = 81;
 
-__host__ __device__ inline long long vt_cols(int N, int nseg) { return 8ll * ((N + 7) / 8) + 8ll * nseg; }
-__device__ __forceinline__ int vt_start(int cu_s, int s) { return 8 * ((cu_s + 7) / 8) + 8 * s; }
+__host__ __device__ inline long long vt_cols(int N, int nseg) { return 64ll * ((N + 63) / 64) + 64ll * nseg; }
+__device__ __forceinline__ int vt_start(int cu_s, int s) { return 64 * ((cu_s + 63) / 64) + 64 * s; }
+
+// fp16 keeps 11 significant bits between 2^-14 and 65504; bf16 keeps 8 over fp32's exponent
+// range.  Scaling a (segment, KV head)'s V by 2^n with n = 142 - E, E the biased exponent of its
+// largest |v| (1 for subnormals), puts that largest value in [2^15, 2^16), where bf16's largest
+// value is 65280 < 65504; every value down to 2^-32 of the largest then converts to fp16 exactly,
+// and smaller ones (at most 2^-32 of the largest) keep fewer bits.  All-zero V takes n = 0.
+__device__ __forceinline__ int vt_shift(uint32_t amax_bits) {
+  if (amax_bits == 0u) return 0;
+  const int e = static_cast<int>((amax_bits >> 7) & 0xffu);
+  return 142 - (e > 0 ? e : 1);
+}
 
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
@@ -535,13 +549,58 @@ __device__ __forceinline__ uint32_t pack_f16x2(float a, float b) {
 struct VtParams {
   const uint16_t* v;     // bf16 [N, H, 80]
   uint16_t* vt;          // fp16 [H, kVtRows, cols]
+  uint32_t* amax;        // [nseg, H] largest |v| of each (segment, head), bf16 bits
   const int32_t* cu;
   int H, tiles;          // tiles: 64-column blocks per segment in the grid
   long long cols;
 };
 
-// One workgroup per (64-column block of a segment, head): V rows in, fp16 V^T rows out.
-// bf16 -> fp16 is exact for |v| in [2^-14, 65504]; smaller values round to fp16 subnormals.
+// Clears the per-(segment, head) maxima (a kernel, not a memset, so that a captured graph
+// replays it like any other launch).
+__global__ __launch_bounds__(256) void attn_vt_clear(uint32_t* amax, int n) {
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i < n) amax[i] = 0u;
+}
+
+// Largest |v| of every (segment, head): a workgroup reads kAmaxTok consecutive token rows of one
+// segment ([tokens, H, 80] bf16, 16-byte chunks; consecutive threads read consecutive chunks),
+// keeps one maximum per chunk slot of a row, folds the 10 slots of each head through LDS and
+// raises the head's maximum with an atomic max on the bf16 bit pattern of |v| (monotone in |v|
+// for non-NaN values).
+constexpr int kAmaxTok = 128;
+constexpr int kAmaxMaxHeads = 256;
+__global__ __launch_bounds__(256) void attn_v_amax(const VtParams p) {
+  __shared__ uint32_t sm[kAmaxMaxHeads * 10];
+  const int s = blockIdx.x / p.tiles, b = blockIdx.x - s * p.tiles;   // tiles: blocks per segment
+  const int c0 = p.cu[s], L = p.cu[s + 1] - c0;
+  const int t0 = b * kAmaxTok;
+  if (t0 >= L) return;   // the whole workgroup leaves together
+  const int nt = min(kAmaxTok, L - t0);
+  const int slots = p.H * 10;
+  const uint4* base = reinterpret_cast<const uint4*>(p.v + static_cast<long long>(c0 + t0) * p.H * 80);
+  for (int slot = threadIdx.x; slot < slots; slot += 256) {
+    uint32_t m = 0u;
+#pragma unroll 8
+    for (int r = 0; r < nt; ++r) {
+      const uint4 u = base[static_cast<long long>(r) * slots + slot];
+      const uint32_t w4[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) m = max(m, max(w4[e] & 0x7fffu, (w4[e] >> 16) & 0x7fffu));
+    }
+    sm[slot] = m;
+  }
+  __syncthreads();
+  for (int h = threadIdx.x; h < p.H; h += 256) {
+    uint32_t m = 0u;
+#pragma unroll
+    for (int c = 0; c < 10; ++c) m = max(m, sm[h * 10 + c]);
+    if (m != 0u) atomicMax(&p.amax[s * p.H + h], m);
+  }
+}
+
+// One workgroup per (64-column block of a segment, head): V rows in, fp16 V^T rows out, each
+// value scaled by 2^vt_shift of its (segment, head) (exact), which keeps every finite bf16 V
+// within fp16's range.
 __global__ __launch_bounds__(256) void attn_vt_prep(const VtParams p) {
   __shared__ __align__(16) uint16_t T[kVtRows][64 + 8];
   const int s = blockIdx.x / p.tiles, t = blockIdx.x - (blockIdx.x / p.tiles) * p.tiles;
@@ -551,6 +610,7 @@ __global__ __launch_bounds__(256) void attn_vt_prep(const VtParams p) {
   const int width = vt_start(p.cu[s + 1], s + 1) - col0;
   if (64 * t >= width) return;   // the whole workgroup leaves together
   const int tid = threadIdx.x;
+  const int shift = vt_shift(p.amax[s * p.H + h]);
   for (int c = tid; c < 64 * 10; c += 256) {
     const int key = c / 10, ch = c - (c / 10) * 10;
     const int j = 64 * t + key;
@@ -559,7 +619,8 @@ __global__ __launch_bounds__(256) void attn_vt_prep(const VtParams p) {
     const uint32_t w4[4] = {u.x, u.y, u.z, u.w};
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      const uint32_t pk = pack_f16x2(__uint_as_float(w4[e] << 16), __uint_as_float(w4[e] & 0xffff0000u));
+      const uint32_t pk = pack_f16x2(__builtin_amdgcn_ldexpf(__uint_as_float(w4[e] << 16), shift),
+                                     __builtin_amdgcn_ldexpf(__uint_as_float(w4[e] & 0xffff0000u), shift));
       T[ch * 8 + 2 * e][key] = static_cast<uint16_t>(pk & 0xffffu);
       T[ch * 8 + 2 * e + 1][key] = static_cast<uint16_t>(pk >> 16);
     }
@@ -833,9 +894,11 @@ __global__ __launch_bounds__(kRotThreads, 1) void attn_fwd_rot(const FwdParams p
   phase_sync();
   for (int i = grp; i < 2; ++i) phase_sync();   // equal barrier counts in every group
 
-  // row 80 of O^T (register 8 of block 2 in the lanes of half 0) is the row sum of P
+  // row 80 of O^T (register 8 of block 2 in the lanes of half 0) is the row sum of P; the
+  // V^T tiles carry V scaled by 2^shift, undone here (exact)
   const float l = __shfl(oacc[2][8], c32, 64);
   const float inv_l = 1.f / l;
+  const int unshift = -vt_shift(p.vt_amax[seg * p.Hkv + kvh]);
   if (qrow < L) {
     uint16_t* op = p.o + static_cast<long long>(s0 + qrow) * qstride + h * D;
 #pragma unroll
@@ -844,9 +907,12 @@ __global__ __launch_bounds__(kRotThreads, 1) void attn_fwd_rot(const FwdParams p
       for (int j = 0; j < 4; ++j) {
         const int dv = t2 * 32 + g * 4 + 8 * j;
         if (dv < D) {
+          float ov[4];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) ov[i] = __builtin_amdgcn_ldexpf(oacc[t2][4 * j + i] * inv_l, unshift);
           uint2 pk;
-          pk.x = pack_bf16x2(oacc[t2][4 * j + 0] * inv_l, oacc[t2][4 * j + 1] * inv_l);
-          pk.y = pack_bf16x2(oacc[t2][4 * j + 2] * inv_l, oacc[t2][4 * j + 3] * inv_l);
+          pk.x = pack_bf16x2(ov[0], ov[1]);
+          pk.y = pack_bf16x2(ov[2], ov[3]);
           *reinterpret_cast<uint2*>(op + dv) = pk;
         }
       }
@@ -1236,9 +1302,14 @@ pace_status_t launch_attention(FwdParams fp, bool causal, int max_seglen, const 
     hipLaunchKernelGGL((attn_fwd<D, true>), dim3(fp.nqt * fp.nseg * fp.Hq), dim3(kThreads), 0, stream, fp);
   } else if (D == 80 && max_seglen >= kRotMinSeg) {
     VtParams vp{};
-    vp.v = fp.v; vp.vt = const_cast<uint16_t*>(fp.vt); vp.cu = fp.cu;
-    vp.H = fp.Hkv; vp.cols = fp.vt_cols;
-    vp.tiles = (max_seglen + 16 + kBN - 1) / kBN;   // a segment owns at most L + 15 columns
+    vp.v = fp.v; vp.vt = const_cast<uint16_t*>(fp.vt); vp.amax = const_cast<uint32_t*>(fp.vt_amax);
+    vp.cu = fp.cu; vp.H = fp.Hkv; vp.cols = fp.vt_cols;
+    vp.tiles = (max_seglen + 128 + kBN - 1) / kBN;   // a segment owns at most L + 127 columns
+    const int namax = fp.nseg * fp.Hkv;
+    hipLaunchKernelGGL(attn_vt_clear, dim3((namax + 255) / 256), dim3(256), 0, stream, vp.amax, namax);
+    VtParams ap = vp;
+    ap.tiles = (max_seglen + kAmaxTok - 1) / kAmaxTok;
+    hipLaunchKernelGGL(attn_v_amax, dim3(ap.tiles * fp.nseg), dim3(256), 0, stream, ap);
     hipLaunchKernelGGL(attn_vt_prep, dim3(vp.tiles * fp.nseg, fp.Hkv), dim3(256), 0, stream, vp);
     pace_status_t st = check_launch("attn_vt_prep");
     if (st != PACE_OK) return st;
@@ -1267,8 +1338,10 @@ extern "C" {
 size_t pace_vit_attention_workspace_size(int N, int H, int d, int nseg, int max_seglen) {
   if (N < 0 || H < 0 || nseg < 0) return 0;
   size_t bytes = align_up(static_cast<size_t>(N) * H * sizeof(float), 256);
-  if (d == 80 && max_seglen >= kRotMinSeg)
-    bytes += static_cast<size_t>(H) * kVtRows * static_cast<size_t>(vt_cols(N, nseg)) * 2;
+  if (d == 80 && max_seglen >= kRotMinSeg) {
+    bytes += align_up(static_cast<size_t>(H) * kVtRows * static_cast<size_t>(vt_cols(N, nseg)) * 2, 256);
+    bytes += static_cast<size_t>(nseg) * H * sizeof(uint32_t);
+  }
   return bytes;
 }
 
@@ -1299,7 +1372,10 @@ pace_status_t pace_vit_attention(const uint16_t* q, const uint16_t* k, const uin
   const bool rot = d == 80 && max_seglen >= kRotMinSeg;
   const long long cols = vt_cols(N, nseg);
   PACE_REQUIRE(!rot || static_cast<long long>(kVtRows) * cols * 2 < (1ll << 31),
-               "pace_vit_attention: N + 8 nseg too large for the V^T tiles");
+               "pace_vit_attention: N + 64 nseg too large for the V^T tiles");
+  if (rot && H > kAmaxMaxHeads)
+    return set_error(PACE_ERR_UNSUPPORTED, "pace_vit_attention: %d heads at head dim 80 on segments of >= %d "
+                     "tokens (at most %d)", H, kRotMinSeg, kAmaxMaxHeads);
   if ((mass != nullptr && lse == nullptr) || rot) {
     const size_t need = pace_vit_attention_workspace_size(N, H, d, nseg, max_seglen);
     if (workspace == nullptr || workspace_bytes < need)
@@ -1311,8 +1387,10 @@ pace_status_t pace_vit_attention(const uint16_t* q, const uint16_t* k, const uin
   FwdParams fp{};
   fp.q = q; fp.k = k; fp.v = v; fp.o = o; fp.lse = lse_buf; fp.cu = cu_seqlens;
   if (rot) {
-    fp.vt = reinterpret_cast<const uint16_t*>(static_cast<char*>(workspace) +
-                                              align_up(static_cast<size_t>(N) * H * sizeof(float), 256));
+    const size_t vt_off = align_up(static_cast<size_t>(N) * H * sizeof(float), 256);
+    const size_t amax_off = vt_off + align_up(static_cast<size_t>(H) * kVtRows * static_cast<size_t>(cols) * 2, 256);
+    fp.vt = reinterpret_cast<const uint16_t*>(static_cast<char*>(workspace) + vt_off);
+    fp.vt_amax = reinterpret_cast<const uint32_t*>(static_cast<char*>(workspace) + amax_off);
     fp.vt_cols = cols;
   }
   fp.Ntot = N; fp.Hq = H; fp.Hkv = H; fp.group = 1;

@@ -16,7 +16,9 @@ from typing import Optional, Sequence
 import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libpace.so")
+# PACE_LIB_PATH selects another build of the same library (the host-sanitized one of the C ABI
+# tests); by default the in-tree libpace.so.
+LIB_PATH = os.environ.get("PACE_LIB_PATH") or os.path.join(_HERE, "libpace.so")
 
 _lib = None
 

@@ -66,3 +66,35 @@ def kept_sets_agree(idx_gpu, idx_ref, S_ref, band=1e-3):
     lo = min(S_ref[i] for i in only_gpu)
     hi = max(S_ref[i] for i in only_ref)
     return (hi - lo) <= band, f"{len(only_gpu)} swaps, spread {hi - lo:.3g}"
+
+
+def oracle_mass_parallel(q, k, causal, scale, mass_rows, workers=8):
+    """The oracle's per-key mass of one head (q, k float64 [n, d]) over `mass_rows`, the rows split
+    into `workers` groups run on threads (numpy releases the GIL inside its loops) and the
+    groups' column sums added.  Test-side parallelism only: every group is a plain oracle call."""
+    from concurrent.futures import ThreadPoolExecutor
+
+    from oracle import attention as oatt
+    rows = np.asarray(mass_rows, dtype=np.int64)
+    parts = [r for r in np.array_split(rows, workers) if r.size]
+
+    def one(r):
+        _, _, m = oatt.attention_segment(q[:, None, :], k[:, None, :], k[:, None, :], causal, scale,
+                                         rows=np.arange(0), mass_rows=r)
+        return m[0]
+    with ThreadPoolExecutor(max_workers=workers) as ex:
+        return np.sum(list(ex.map(one, parts)), axis=0)
+
+
+def load_e2e_golden(config_id, workload):
+    """Oracle-only end-to-end selection (tests/golden/make_e2e_golden.py) for one workload:
+    (nv, keep, S_final, kept idx), after checking the workload's inputs are the ones it used."""
+    import hashlib
+    import os
+    z = np.load(os.path.join(os.path.dirname(__file__), "golden", "e2e_select.npz"))
+    c = f"c{config_id}_"
+    h = hashlib.sha256()
+    for a in (workload.vit.q, workload.vit.k, workload.prefill.q, workload.prefill.k):
+        h.update(np.ascontiguousarray(a).tobytes())
+    assert str(z[c + "sha"]) == h.hexdigest(), "workload generator changed since the golden file"
+    return z[c + "nv"], z[c + "keep"], z[c + "S"].astype(np.float64), z[c + "idx"].astype(np.int64)

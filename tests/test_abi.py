@@ -140,6 +140,9 @@ def test_workspace_sizes_monotone():
     assert L.pace_apc_density_workspace_size(2156, 3836, 14) > L.pace_apc_density_workspace_size(448, 448, 14)
     assert L.pace_ddae_select_workspace_size(10549, 1) >= 3 * 10549 * 4
     assert L.pace_vit_attention_workspace_size(42196, 16, 80, 700, 64) == 42196 * 16 * 4
-    cols = 8 * ((42196 + 7) // 8) + 8
-    assert L.pace_vit_attention_workspace_size(42196, 16, 80, 1, 42196) == 42196 * 16 * 4 + 16 * 81 * cols * 2
+    cols = 64 * ((42196 + 63) // 64) + 64          # V^T columns: segments start on 64-column boundaries
+    vt = (16 * 81 * cols * 2 + 255) // 256 * 256
+    lse = (42196 * 16 * 4 + 255) // 256 * 256
+    assert L.pace_vit_attention_workspace_size(42196, 16, 80, 1, 42196) == lse + vt + 1 * 16 * 4
     assert L.pace_vit_attention_workspace_size(42196, 16, 128, 1, 42196) == 42196 * 16 * 4
+

@@ -130,6 +130,57 @@ def test_vit_long_segment_value_range_d80(vscale):
     assert np.max(np.abs(lse - Lr)) <= LSE_TOL
 
 
+def _scale_bits(v, k):
+    """bf16 bits of v * 2^k, exactly (the exponent field moves by k; zeros stay zero)."""
+    v = v.astype(np.int32)
+    e = (v >> 7) & 0xFF
+    assert np.all((e == 0) | ((e + k > 0) & (e + k < 255)))
+    return np.where(e == 0, v, v + (k << 7)).astype(np.uint16)
+
+
+@pytest.mark.parametrize("k", [17, -20, 100, -100])
+def test_vit_long_segment_any_finite_v_d80(k):
+    """V at 2^k times N(0,1) (up to ~6e5 at k = 17, ~1e-6 at k = -20, and 2^+-100): fp16 holds
+    none of these directly, but the long-segment kernel scales each (segment, head) by a power
+    of two before the fp16 PV product and undoes it on the output, so O(2^k V) is exactly
+    2^k O(V), bit for bit, and the LSE is unchanged; O also matches the oracle within 2e-2 of
+    its largest magnitude."""
+    sizes = [1100, 70]
+    cu = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int32)
+    N, H, d = int(cu[-1]), 2, 80
+    q, kk, v = _vit_case(44, cu, H, d)
+    vs = _scale_bits(v, k)
+    say(f"vit long segment, V scaled by 2^{k}")
+    o0, l0, m0 = _run_vit(q, kk, v, cu, int(max(sizes)))
+    o1, l1, m1 = _run_vit(q, kk, vs, cu, int(max(sizes)))
+    np.testing.assert_array_equal(o1, np.ldexp(o0, k))
+    np.testing.assert_array_equal(l1, l0)
+    np.testing.assert_array_equal(m1, m0)
+    Or, Lr, _ = oatt.vit_attention(wl.bf16_bits_to_f64(q), wl.bf16_bits_to_f64(kk), wl.bf16_bits_to_f64(vs),
+                                   cu, 1 / math.sqrt(d), with_mass=False)
+    assert np.max(np.abs(o1 - Or)) <= O_TOL * np.max(np.abs(Or))
+    assert np.max(np.abs(l1 - Lr)) <= LSE_TOL
+
+
+def test_vit_long_segment_neighbour_out_of_fp16_range_d80():
+    """Two long segments packed in one call, the second with V at ~2^20 (beyond fp16): the first
+    segment's O and LSE equal, bit for bit, those of a call whose second segment is unscaled
+    (no tile of one segment reads the other's V^T columns, and each has its own scale), and the
+    second segment's O is exactly 2^20 times its unscaled output."""
+    sizes = [1100, 1030]
+    cu = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int32)
+    N, H, d = int(cu[-1]), 2, 80
+    q, kk, v = _vit_case(45, cu, H, d)
+    v2 = v.copy()
+    v2[1100:] = _scale_bits(v[1100:], 20)
+    o0, l0, _ = _run_vit(q, kk, v, cu, 1100)
+    o1, l1, _ = _run_vit(q, kk, v2, cu, 1100)
+    np.testing.assert_array_equal(o1[:1100], o0[:1100])
+    np.testing.assert_array_equal(o1[1100:], np.ldexp(o0[1100:], 20))
+    np.testing.assert_array_equal(l1, l0)
+    assert np.all(np.isfinite(o1))
+
+
 @pytest.mark.parametrize("sizes,d", [([0, 64, 0, 17, 0], 80),              # windows, fused mass
                                      ([1100, 0, 0, 37, 1030, 0], 80),     # long-segment kernel
                                      ([0, 300, 0, 129], 128)])            # general kernel

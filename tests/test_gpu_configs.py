@@ -3,7 +3,8 @@ float64 oracle, element by element: APC density and distances, the window attent
 mass), the full attention of the image (forward, then the mass pass, as bench.py runs them;
 at 1344 x 1344 four of the sixteen heads), the causal prefill with the text-query mass of every
 visual key, and the DDAE selection fed the GPU's own masses (fused scores, kept set, gathered
-rows).  Bars as in the other parity tests: O 2e-2, LSE 1e-3, mass 1e-3 relative, APC 1e-4,
+rows), whose kept set is then held against the selection the oracle makes from its own masses
+(tests/golden/e2e_select.npz, written by an oracle-only script).  Bars as in the other parity tests: O 2e-2, LSE 1e-3, mass 1e-3 relative, APC 1e-4,
 fused scores 1e-5, kept sets equal up to swaps inside a 1e-3 score band, gather bitwise."""
 import math
 
@@ -15,7 +16,7 @@ from oracle import attention as oatt
 from oracle import ddae as oddae
 from paper_2608_27206_amd import workloads as wl
 from tests.gpu_util import (dev_bf16, dev_i32, dev_u8, host, host_bf16_to_f64, kept_sets_agree,
-                            mass_ok, say)
+                            load_e2e_golden, mass_ok, say)
 
 pytestmark = pytest.mark.gpu
 
@@ -91,3 +92,17 @@ def test_hot_path_end_to_end(config_id, heads):
     ok, msg = kept_sets_agree(host(idx), oddae.topk_indices(S_ref, Kk), S_ref)
     assert ok, msg
     np.testing.assert_array_equal(out.view(torch.int16).cpu().numpy().view(np.uint16), w.hidden[host(idx)])
+
+    # end to end against the oracle alone: its own masses (all 16 heads of the full attention, every
+    # text row of the prefill), its fusion and its top-K (tests/golden/make_e2e_golden.py); the kept
+    # sets may differ only by swaps whose oracle scores lie within 1e-3
+    nv_g, keep_g, S_g, idx_g = load_e2e_golden(config_id, w)
+    assert list(nv_g) == [nv] and list(keep_g) == [Kk]
+    assert np.max(np.abs(host(sc) - S_g)) <= 1e-3
+    ok, msg = kept_sets_agree(host(idx), idx_g, S_g)
+    assert ok, msg
+    say(f"end-to-end kept set vs oracle-only chain: {msg}")
+    if config_id == 1:   # here the oracle's masses of this test are complete: the same chain in-line
+        S_e2e, _ = oddae.fuse(Mr, Ml[:, :nv], 4, L.vis_perm, w.fusion_mode, w.tau)
+        np.testing.assert_allclose(S_e2e, S_g, atol=1e-6)
+        np.testing.assert_array_equal(oddae.topk_indices(S_e2e, Kk), idx_g)

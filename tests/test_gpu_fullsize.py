@@ -19,7 +19,7 @@ from oracle import attention as oatt
 from oracle import ddae as oddae
 from paper_2608_27206_amd import workloads as wl
 from tests.gpu_util import (dev_bf16, dev_f32, dev_i32, dev_u8, host, host_bf16_to_f64,
-                            kept_sets_agree, mass_ok, say)
+                            kept_sets_agree, load_e2e_golden, mass_ok, oracle_mass_parallel, say)
 
 pytestmark = pytest.mark.gpu
 
@@ -67,17 +67,77 @@ def _vit_bench_sequence(vit, cu, maxlen):
     return host_bf16_to_f64(o), host(lse), host(mass)
 
 
+ROT_ROWS = 384   # query rows per workgroup of the long-segment forward
+
+
 def test_frame4k_vit_full_attention(w4k):
+    """O and LSE of all 16 heads on 1,000+ rows: the first and last row of every 384-row
+    workgroup of the forward plus random ones; the per-key mass of two heads element by element
+    over all 42,196 keys; and each head's mass totals N."""
     vit = w4k.vit
     N = vit.q.shape[0]
     say(f"4K full attention N={N}")
     o, lse, mass = _vit_bench_sequence(vit, vit.cu_full, N)
     rs = np.random.default_rng(0)
-    rows = np.unique(np.concatenate([[0, 1, 777, N // 2, N - 2, N - 1], rs.integers(0, N, 26)]))
+    starts = np.arange(0, N, ROT_ROWS)
+    rows = np.unique(np.concatenate([starts, np.minimum(starts + ROT_ROWS - 1, N - 1), [1, N // 2, N - 2],
+                                     rs.integers(0, N, 800)]))
+    assert rows.size >= 1000
     _check_rows(vit.q, vit.k, vit.v, o, lse, 0, N, rows, False, range(vit.q.shape[1]))
+    for h in (0, 9):
+        say(f"4K full attention: oracle mass of head {h} over all {N} rows")
+        ref = oracle_mass_parallel(_f64(vit.q[:, h]), _f64(vit.k[:, h]), False, 1 / math.sqrt(80), np.arange(N))
+        err, rel = mass_ok(mass[h], ref, N)
+        assert err <= 0, (h, rel)
     # every row's probabilities sum to one, so each head's mass totals N
     np.testing.assert_allclose(mass.sum(axis=1), N, rtol=1e-4)
     assert np.all(mass >= 0)
+
+
+def _e2e_gpu_selection(w, keeps):
+    """The chain bench.py times, on the GPU alone: full attention of every image (forward, then
+    the mass pass), the causal prefill with the text-query mass, and the DDAE selection of the
+    images' K_b tokens from those masses.  Returns (kept global indices, fused scores)."""
+    from paper_2608_27206_amd import pace
+    import torch
+    vit, p = w.vit, w.prefill
+    cu = vit.cu_full
+    Q, K, CU = dev_bf16(vit.q), dev_bf16(vit.k), dev_i32(cu)
+    maxlen = int(np.diff(cu).max())
+    _, lse, _ = pace.vit_attention(Q, K, dev_bf16(vit.v), CU, maxlen, want_mass=False)
+    vis_mass = pace.vit_attention_mass(Q, K, CU, maxlen, lse)
+    pc = p.cu_seqlens
+    _, _, llm_mass = pace.prefill_attention_with_mass(
+        dev_bf16(p.q), dev_bf16(p.k), dev_bf16(p.v), dev_i32(pc), int(np.diff(pc).max()),
+        dev_i32(p.vis_len), dev_i32(p.cu_vis), int(p.cu_vis[-1]), int(p.vis_len.max()),
+        dev_i32(p.mq_start), dev_i32(p.mq_len), int(p.mq_len.max()))
+    nvs = [L.n_vis for L in w.layouts]
+    idx, sc, _, _ = pace.ddae_select(vis_mass, 4, dev_i32(vit.vis_perm), llm_mass, nvs, list(keeps),
+                                     mode=w.fusion_mode, tau=w.tau)
+    torch.cuda.synchronize()
+    return host(idx).astype(np.int64), host(sc).astype(np.float64)
+
+
+def _check_e2e(idx, sc, nvs, keeps, S_g, idx_g):
+    """Per image, the GPU's kept set against the oracle-only one: equal up to swaps whose oracle
+    scores lie within 1e-3, and the fused scores within 1e-3 of the oracle's."""
+    assert np.max(np.abs(sc - S_g)) <= 1e-3, np.max(np.abs(sc - S_g))
+    off = koff = 0
+    for b, (n, K) in enumerate(zip(nvs, keeps)):
+        ok, msg = kept_sets_agree(idx[koff:koff + K], idx_g[koff:koff + K], S_g)
+        assert ok, (b, msg)
+        say(f"image {b}: {n} tokens, keep {K}: {msg}")
+        off += n
+        koff += K
+
+
+def test_frame4k_e2e_selection(w4k):
+    """Section 3.3 end to end at 4K: the tokens the GPU keeps from its own attention masses against
+    the tokens the oracle keeps from its own (tests/golden/e2e_select.npz)."""
+    nv_g, keep_g, S_g, idx_g = load_e2e_golden(3, w4k)
+    say(f"4K end to end: keep {list(keep_g)} of {list(nv_g)}")
+    idx, sc = _e2e_gpu_selection(w4k, keep_g)
+    _check_e2e(idx, sc, nv_g, keep_g, S_g, idx_g)
 
 
 def test_frame4k_windows(w4k):
@@ -176,16 +236,27 @@ def test_frame4k_select(w4k):
 
 
 def test_varlen_vit(wvar):
+    """Per image of the packed batch: O and LSE of all 16 heads on the first and last row of every
+    384-row workgroup plus 64 random rows, and the per-key mass of one head (a different one per
+    image) element by element."""
     vit = wvar.vit
     cu = vit.cu_full
     say(f"varlen full attention: segments {np.diff(cu).tolist()}")
     o, lse, mass = _vit_bench_sequence(vit, cu, int(np.diff(cu).max()))
     for b in range(len(cu) - 1):
         a, e = int(cu[b]), int(cu[b + 1])
+        n = e - a
         rs = np.random.default_rng(b)
-        rows = np.unique(np.concatenate([[0, e - a - 1], rs.integers(0, e - a, 6)]))
-        _check_rows(vit.q, vit.k, vit.v, o, lse, a, e, rows, False, [0, 7, 15])
-        np.testing.assert_allclose(mass[:, a:e].sum(axis=1), e - a, rtol=1e-4)
+        starts = np.arange(0, n, ROT_ROWS)
+        rows = np.unique(np.concatenate([starts, np.minimum(starts + ROT_ROWS - 1, n - 1), [n - 1],
+                                         rs.integers(0, n, 64)]))
+        _check_rows(vit.q, vit.k, vit.v, o, lse, a, e, rows, False, range(16))
+        h = (5 * b) % 16
+        ref = oracle_mass_parallel(_f64(vit.q[a:e, h]), _f64(vit.k[a:e, h]), False, 1 / math.sqrt(80),
+                                   np.arange(n))
+        err, rel = mass_ok(mass[h, a:e], ref, n)
+        assert err <= 0, (b, h, rel)
+        np.testing.assert_allclose(mass[:, a:e].sum(axis=1), n, rtol=1e-4)
     # windows of the first and last image, element by element
     cw = vit.cu_windows
     ow, lw, mw = _vit_bench_sequence(vit, cw, int(np.diff(cw).max()))
@@ -246,3 +317,20 @@ def test_varlen_apc_keep_and_select(wvar):
         koff += K
     import torch as t
     np.testing.assert_array_equal(out.view(t.int16).cpu().numpy().view(np.uint16), wvar.hidden[idx])
+
+
+def test_varlen_e2e_selection(wvar):
+    """The packed batch end to end: each image's K from its APC density on the GPU (equal to the
+    oracle's), the GPU's full-attention and prefill masses, the segmented selection; every
+    image's kept set against the oracle-only selection (tests/golden/e2e_select.npz)."""
+    from paper_2608_27206_amd import pace
+    import torch
+    nv_g, keep_g, S_g, idx_g = load_e2e_golden(4, wvar)
+    keeps = []
+    for img, nv in zip(wvar.images, nv_g):
+        rho, _ = pace.apc_density(dev_u8(img), 14, 0.10, 0.6, 1.5)
+        torch.cuda.synchronize()
+        keeps.append(pace.keep_from_density(float(host(rho)[2]), int(nv)))
+    assert keeps == list(keep_g)
+    idx, sc = _e2e_gpu_selection(wvar, keeps)
+    _check_e2e(idx, sc, nv_g, keep_g, S_g, idx_g)
