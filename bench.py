@@ -1,16 +1,21 @@
 """PACE hot-path benchmark on one MI355X.
 
-A step is one pass of every hot-path kernel over the 4K-frame workload
-(3836x2156 RGB image, Qwen2.5-VL-7B shapes): APC density and 2x downsample of the
-image, vision-encoder window attention (700 windows of <= 64 patches, 16 heads,
-d = 80) and full attention over 42,196 patches with the per-key mass, causal GQA
-prefill over 10,549 visual + 128 text tokens (28/4 heads, d = 128) with the
-text-query mass of every visual key, and DDAE fusion + top-K (10%) + gather of the
-kept rows of a 10,549 x 3584 bf16 hidden-state matrix.  Inputs are synthetic and
-seeded, already resident in HBM when the timed region starts.
+A step is one pass of every hot-path kernel over one seeded workload (Qwen2.5-VL-7B shapes),
+inputs already resident in HBM when the timed region starts.  The default (--config 3) is
+the 4K frame (3836x2156 RGB): APC density and 2x downsample of the image, vision-encoder
+window attention (700 windows of <= 64 patches, 16 heads, d = 80) and full attention over
+42,196 patches with the per-key mass, causal GQA prefill over 10,549 visual + 128 text
+tokens (28/4 heads, d = 128) with the text-query mass of every visual key, and DDAE fusion +
+top-K (10%) + gather of the kept rows of a 10,549 x 3584 bf16 hidden-state matrix.
+--config 1 and 2 run the same step on a 448x448 and a 1344x1344 image (the resize takes APC's
+own rho within the 256..2048 x 28^2 pixel budget), --config 4 on the packed batch of eight
+images (per-image density, resize and keep count; the attention passes over cu_seqlens; one
+segmented selection), and --config 0 on the tiny prefill (prefill with mass, then fusion with
+a given vision mass, top-K and gather).  Sizes that follow rho are read back once before the
+timed steps.
 
 Prints one JSON line.  `value` is the step's algorithmic attention FLOP rate
-(all three attention passes' 4*d*(visible pairs)*heads, over the whole step time).
+(every attention pass's 4*d*(visible pairs)*heads, over the whole step time).
 """
 from __future__ import annotations
 
@@ -58,7 +63,8 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--config", type=int, default=3, help="workload id (3 = 4K frame)")
+    ap.add_argument("--config", type=int, default=3, choices=range(5),
+                    help="workload id: 0 tiny prefill, 1 448x448, 2 1344x1344, 3 4K frame (default), 4 varlen batch")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="wall-clock budget of the oracle CPU baseline sample (0 = skip)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
@@ -93,6 +99,173 @@ def time_graph_replays(torch, step, stream, steps):
     return e0.elapsed_time(e1) / steps
 
 
+MIN_PIXELS = 256 * 28 * 28    # APC's dynamic budget (reading R4): the resize keeps at least this area
+MAX_PIXELS = 2048 * 28 * 28   # ... and at most this one (the paper's fixed setting of 2048 * 28 * 28)
+
+
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:  # pragma: no cover
+        pass
+    return "unknown"
+
+
+def build_workload_step(a, torch, np, pace, wl, dev):
+    """Device inputs, outputs and the ordered parts of one step of the hot path for workload
+    a.config.  Returns a dict: parts [(name, fn, side, join)], work {name: (bound, amount)},
+    config (the JSON config object), roof (name and label of the dominant kernel's part),
+    flop_attn (algorithmic attention FLOPs of the step), cpu (oracle sample closure), extra."""
+    w = wl.make_workload(a.config)
+
+    def bf(x):
+        return torch.from_numpy(np.ascontiguousarray(x).view(np.int16)).view(torch.bfloat16).to(dev)
+
+    def i32(x):
+        return torch.from_numpy(np.asarray(x, np.int32)).to(dev)
+
+    f32 = dict(dtype=torch.float32, device=dev)
+    pre = w.prefill
+    pq, pk, pv = bf(pre.q), bf(pre.k), bf(pre.v)
+    p_cu, p_vis, p_cuv = i32(pre.cu_seqlens), i32(pre.vis_len), i32(pre.cu_vis)
+    p_mqs, p_mql = i32(pre.mq_start), i32(pre.mq_len)
+    S_tot = int(pre.cu_seqlens[-1])
+    seqlens = np.diff(pre.cu_seqlens)
+    max_s = int(seqlens.max())
+    nvs = [int(x) for x in pre.vis_len]
+    Nv = int(sum(nvs))
+    Hq, Hkv, dq = pre.q.shape[1], pre.k.shape[1], pre.q.shape[2]
+    hidden = bf(w.hidden)
+    o_pre = torch.empty_like(pq)
+    lse_pre = torch.empty((Hq, S_tot), **f32)
+    mass_llm = torch.empty((Hq, max(1, Nv)), **f32)
+    parts, work = [], {}
+    flop_pre = 4.0 * dq * Hq * float(np.sum(seqlens.astype(np.float64) * (seqlens + 1) / 2.0))
+
+    def prefill():
+        pace.prefill_attention_with_mass(pq, pk, pv, p_cu, max_s, p_vis, p_cuv, Nv, int(pre.vis_len.max()), p_mqs,
+                                         p_mql, int(pre.mq_len.max()), o=o_pre, lse=lse_pre, mass=mass_llm)
+
+    cfg = {"workload": wl.CONFIG_NAMES[a.config], "prefill_tokens": S_tot, "visual_tokens": Nv,
+           "text_tokens": int(pre.text_len.sum()), "llm_heads": f"{Hq}/{Hkv}", "llm_head_dim": int(dq),
+           "hidden": int(w.hidden.shape[1])}
+    extra = {}
+    if w.vit is None:
+        # tiny DDAE prefill: the vision mass is given (Dirichlet), fixed 50/50 fusion
+        K = pace.keep_count(w.keep_ratio, Nv)
+        keeps = [K]
+        vis_mass = torch.from_numpy(w.vit_mass).to(dev)
+        merge, perm = 1, None
+        parts.append(("prefill", prefill, False, False))
+        work["prefill"] = ("mfma", flop_pre)
+        roof = ("prefill", "attn_fwd<128, true> + attn_mass<128, true> (causal GQA prefill with text-query mass)")
+        flop_attn = flop_pre
+        cfg.update({"keep": K, "fusion": "fixed 0.5/0.5"})
+    else:
+        vit = w.vit
+        vq, vk, vv = bf(vit.q), bf(vit.k), bf(vit.v)
+        cu_win, cu_full = i32(vit.cu_windows), i32(vit.cu_full)
+        max_win = int(np.diff(vit.cu_windows).max())
+        full_lens = np.diff(vit.cu_full).astype(np.float64)
+        max_full = int(full_lens.max())
+        Np, Hv, dv = vit.q.shape
+        nseg = len(full_lens)
+        perm, merge = i32(vit.vis_perm), 4
+        imgs = [torch.from_numpy(im).to(dev) for im in w.images]
+        ws_apc = [torch.empty(pace.lib().pace_apc_density_workspace_size(im.shape[0], im.shape[1], 14),
+                              dtype=torch.uint8, device=dev) for im in w.images]
+        rhos = [torch.empty(4, **f32) for _ in w.images]
+        dps = [torch.empty((im.shape[0] // 14) * (im.shape[1] // 14), **f32) for im in w.images]
+        # the resize size and the per-image K follow the density: read once from the GPU here (a caller
+        # reads rho back before sizing the resize); the timed steps reuse these sizes
+        for im, ws, r, d in zip(imgs, ws_apc, rhos, dps):
+            pace.apc_density(im, 14, 0.10, 0.6, 1.5, d_out=d, rho_out=r, workspace=ws)
+        torch.cuda.synchronize()
+        rho_h = [float(r.cpu()[2]) for r in rhos]
+        sizes = []
+        for im, rh in zip(w.images, rho_h):
+            H, W = im.shape[0], im.shape[1]
+            if w.downsample_scale:
+                sizes.append((int(round(H * w.downsample_scale)), int(round(W * w.downsample_scale))))
+            else:
+                sizes.append(pace.apc_target_size(rh, H, W, MIN_PIXELS, MAX_PIXELS, 28))
+        smalls = [torch.empty((oh, ow, 3), dtype=torch.uint8, device=dev) for oh, ow in sizes]
+        if a.config == 4:
+            keeps = [pace.keep_from_density(rh, nv) for rh, nv in zip(rho_h, nvs)]
+        else:
+            keeps = [pace.keep_count(w.keep_ratio, Nv)]
+        o_win = torch.empty_like(vq)
+        lse_win = torch.empty((Hv, Np), **f32)
+        mass_win = torch.empty((Hv, Np), **f32)
+        o_full = torch.empty_like(vq)
+        lse_full = torch.empty((Hv, Np), **f32)
+        vis_mass = torch.empty((Hv, Np), **f32)
+        ws_vit = torch.empty(pace.lib().pace_vit_attention_workspace_size(Np, Hv, dv, nseg, max_full),
+                             dtype=torch.uint8, device=dev)
+
+        def apc():
+            for im, ws, r, d in zip(imgs, ws_apc, rhos, dps):
+                pace.apc_density(im, 14, 0.10, 0.6, 1.5, d_out=d, rho_out=r, workspace=ws)
+
+        def resize():
+            for im, sm in zip(imgs, smalls):
+                pace.apc_downsample(im, sm.shape[0], sm.shape[1], dst=sm)
+
+        parts += [
+            ("apc", apc, False, False),
+            ("resize", resize, False, False),
+            ("vit_win", lambda: pace.vit_attention(vq, vk, vv, cu_win, max_win, o=o_win, lse=lse_win,
+                                                   mass=mass_win), False, False),
+            ("vit_fwd", lambda: pace.vit_attention(vq, vk, vv, cu_full, max_full, o=o_full, lse=lse_full,
+                                                   want_mass=False, workspace=ws_vit), False, False),
+            # the vision mass needs only the forward's LSE and the prefill neither (it takes the encoder's
+            # output): the mass runs on a second stream beside the prefill, the selection joins both
+            ("vit_mass", lambda: pace.vit_attention_mass(vq, vk, cu_full, max_full, lse_full, mass=vis_mass),
+             True, False),
+            ("prefill", prefill, False, False),
+        ]
+        win_sizes = np.diff(vit.cu_windows).astype(np.float64)
+        flop_full = 4.0 * dv * Hv * float(np.sum(full_lens ** 2))
+        work.update({
+            "apc": ("hbm", float(sum(im.shape[0] * im.shape[1] * 3 + 4.0 * (im.shape[0] // 14) * (im.shape[1] // 14)
+                                    for im in w.images))),
+            "resize": ("hbm", float(sum(im.shape[0] * im.shape[1] * 3 + oh * ow * 3
+                                       for im, (oh, ow) in zip(w.images, sizes)))),
+            "vit_win": ("hbm", 4.0 * Np * Hv * dv * 2 + 2.0 * Hv * Np * 4),
+            "vit_fwd": ("mfma", flop_full),
+            "vit_mass": ("mfma", 0.0),
+            "prefill": ("mfma", flop_pre),
+        })
+        flop_attn = 4.0 * dv * Hv * float(np.sum(win_sizes ** 2)) + flop_full + flop_pre
+        roof = ("vit_fwd", "pace_vit_attention call on the full-attention segments: attn_vt_clear + attn_v_amax + "
+                           f"attn_vt_prep + attn_fwd_rot<80> ({Np:,} patches in {nseg} segment(s) x {Hv} heads); "
+                           "attn_fwd_rot is 99% of it")
+        cfg.update({"images": [f"{im.shape[1]}x{im.shape[0]}" for im in w.images], "vit_patches": int(Np),
+                    "vit_heads": int(Hv), "vit_head_dim": int(dv), "vit_segments": nseg,
+                    "windows": int(len(win_sizes)), "keep": keeps if len(keeps) > 1 else keeps[0],
+                    "resize_to": [f"{ow}x{oh}" for oh, ow in sizes] if len(sizes) > 1 else f"{sizes[0][1]}x{sizes[0][0]}"})
+        extra["flop_full"] = flop_full
+        extra.update({"vq": vq, "vk": vk, "vv": vv, "img": imgs[0], "layout": w.layouts[0]})
+    ktot = int(sum(keeps))
+    idx = torch.empty(max(1, ktot), dtype=torch.int32, device=dev)
+    scores = torch.empty(max(1, Nv), **f32)
+    fuse = torch.empty((len(keeps), 4), **f32)
+    kept = torch.empty((max(1, ktot), hidden.shape[1]), dtype=hidden.dtype, device=dev)
+    ws_sel = torch.empty(pace.lib().pace_ddae_select_workspace_size(Nv, len(keeps)), dtype=torch.uint8, device=dev)
+    parts.append(("select", lambda: pace.ddae_select(vis_mass, merge, perm, mass_llm, nvs, keeps, mode=w.fusion_mode,
+                                                     tau=w.tau, w_llm_fixed=w.w_llm_fixed, hidden=hidden,
+                                                     idx_out=idx, score_out=scores, fuse_out=fuse, out=kept,
+                                                     workspace=ws_sel), False, True))
+    Hv_sel = vis_mass.shape[0]
+    work["select"] = ("hbm", float(Hv_sel * vis_mass.shape[1] * 4 + Hq * Nv * 4 + 4 * ktot
+                                   + 2.0 * ktot * hidden.shape[1] * 2))
+    extra.update({"pq": pq, "pk": pk, "pv": pv, "p_cu": p_cu, "p_vis": p_vis, "p_cuv": p_cuv, "S": S_tot, "Nv": Nv,
+                  "T": int(pre.text_len.sum()), "idx": idx, "K": ktot, "w": w})
+    return {"parts": parts, "work": work, "config": cfg, "roof": roof, "flop_attn": flop_attn, "extra": extra}
+
+
 def main():
     a = parse()
     if a.gpus != 1:
@@ -107,107 +280,35 @@ def main():
 
     torch.cuda.set_device(0)
     dev = torch.device("cuda:0")
-    w = wl.make_workload(a.config)
-    L = w.layouts[0]
-    img_np = w.images[0]
-    H, W, _ = img_np.shape
-    vit, pre = w.vit, w.prefill
-
-    def bf(x):
-        return torch.from_numpy(np.ascontiguousarray(x).view(np.int16)).view(torch.bfloat16).to(dev)
-
-    def i32(x):
-        return torch.from_numpy(np.asarray(x, np.int32)).to(dev)
-
-    img = torch.from_numpy(img_np).to(dev)
-    vq, vk, vv = bf(vit.q), bf(vit.k), bf(vit.v)
-    cu_win, cu_full = i32(vit.cu_windows), i32(vit.cu_full)
-    max_win = int(np.diff(vit.cu_windows).max())
-    Np, Hv, dv = vit.q.shape
-    pq, pk, pv = bf(pre.q), bf(pre.k), bf(pre.v)
-    p_cu, p_vis, p_cuv = i32(pre.cu_seqlens), i32(pre.vis_len), i32(pre.cu_vis)
-    p_mqs, p_mql = i32(pre.mq_start), i32(pre.mq_len)
-    S = int(pre.cu_seqlens[-1])
-    Nv = int(pre.vis_len[0])
-    T = int(pre.text_len[0])
-    Hq, Hkv, dq = pre.q.shape[1], pre.k.shape[1], pre.q.shape[2]
-    hidden = bf(w.hidden)
-    perm = i32(vit.vis_perm)
-    K = pace.keep_count(w.keep_ratio, Nv)
-    oH, oW = (int(round(H * w.downsample_scale)), int(round(W * w.downsample_scale))) \
-        if w.downsample_scale else pace.apc_target_size(0.5, H, W, 0, 1e18, 28)
-
-    # outputs and workspaces, allocated once
-    f32 = dict(dtype=torch.float32, device=dev)
-    rho = torch.empty(4, **f32)
-    dpatch = torch.empty(L.n_patches, **f32)
-    ws_apc = torch.empty(pace.lib().pace_apc_density_workspace_size(H, W, 14), dtype=torch.uint8, device=dev)
-    small = torch.empty((oH, oW, 3), dtype=torch.uint8, device=dev)
-    o_win = torch.empty_like(vq)
-    lse_win = torch.empty((Hv, Np), **f32)
-    mass_win = torch.empty((Hv, Np), **f32)
-    o_full = torch.empty_like(vq)
-    lse_full = torch.empty((Hv, Np), **f32)
-    mass_vis = torch.empty((Hv, Np), **f32)
-    o_pre = torch.empty_like(pq)
-    lse_pre = torch.empty((Hq, S), **f32)
-    mass_llm = torch.empty((Hq, Nv), **f32)
-    idx = torch.empty(K, dtype=torch.int32, device=dev)
-    scores = torch.empty(Nv, **f32)
-    fuse = torch.empty((1, 4), **f32)
-    kept = torch.empty((K, hidden.shape[1]), dtype=hidden.dtype, device=dev)
-    ws_sel = torch.empty(pace.lib().pace_ddae_select_workspace_size(Nv, 1), dtype=torch.uint8, device=dev)
-    ws_vit = torch.empty(pace.lib().pace_vit_attention_workspace_size(Np, Hv, dv, 1, Np), dtype=torch.uint8,
-                         device=dev)
-
+    B = build_workload_step(a, torch, np, pace, wl, dev)
+    parts, work, ex = B["parts"], B["work"], B["extra"]
+    names = [p[0] for p in parts]
     stream = torch.cuda.current_stream()
-    names = ("apc", "resize", "vit_win", "vit_fwd", "vit_mass", "prefill", "select")
+    side = torch.cuda.Stream()   # default priority
 
     def new_events():
-        return {n: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-                for n in names}
-
-    # The vision mass pass needs only the forward's LSE, and the LLM prefill needs neither it nor
-    # its result (it takes the vision encoder's output, which the forward has produced): the two
-    # run side by side, the mass on a second stream (default priority), and the selection waits
-    # for both.  The mass kernel's last round of workgroups leaves CUs idle that the prefill fills.
-    side = torch.cuda.Stream()
-
-    def run(name, fn, ev):
-        cur = torch.cuda.current_stream()
-        if ev is not None:
-            ev[name][0].record(cur)
-        fn()
-        if ev is not None:
-            ev[name][1].record(cur)
+        return {n: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for n in names}
 
     def step(ev, overlap=True):
-        run("apc", lambda: pace.apc_density(img, 14, 0.10, 0.6, 1.5, d_out=dpatch, rho_out=rho,
-                                            workspace=ws_apc), ev)
-        run("resize", lambda: pace.apc_downsample(img, oH, oW, dst=small), ev)
-        run("vit_win", lambda: pace.vit_attention(vq, vk, vv, cu_win, max_win, o=o_win, lse=lse_win,
-                                                  mass=mass_win), ev)
-        run("vit_fwd", lambda: pace.vit_attention(vq, vk, vv, cu_full, Np, o=o_full, lse=lse_full,
-                                                  want_mass=False, workspace=ws_vit), ev)
-        def vis_mass():
-            pace.vit_attention_mass(vq, vk, cu_full, Np, lse_full, mass=mass_vis)
-
-        def prefill():
-            pace.prefill_attention_with_mass(pq, pk, pv, p_cu, S, p_vis, p_cuv, Nv, Nv, p_mqs, p_mql, T,
-                                             o=o_pre, lse=lse_pre, mass=mass_llm)
-        if overlap:
-            cur = torch.cuda.current_stream()
-            side.wait_stream(cur)
-            with torch.cuda.stream(side):
-                vis_mass()
-            prefill()
+        cur = torch.cuda.current_stream()
+        pending = False
+        for name, fn, on_side, join in parts:
+            if overlap and join and pending:
+                cur.wait_stream(side)
+                pending = False
+            if overlap and on_side:
+                side.wait_stream(cur)
+                with torch.cuda.stream(side):
+                    fn()
+                pending = True
+                continue
+            if ev is not None:
+                ev[name][0].record(cur)
+            fn()
+            if ev is not None:
+                ev[name][1].record(cur)
+        if pending:
             cur.wait_stream(side)
-        else:
-            run("vit_mass", vis_mass, ev)
-            run("prefill", prefill, ev)
-        run("select", lambda: pace.ddae_select(mass_vis, 4, perm, mass_llm, [Nv], [K], mode=w.fusion_mode,
-                                               tau=w.tau, hidden=hidden, idx_out=idx, score_out=scores,
-                                               fuse_out=fuse, out=kept, workspace=ws_sel), ev)
 
     if a.copy_calibration_mib > 0:
         nbytes = a.copy_calibration_mib << 20
@@ -245,22 +346,29 @@ def main():
             per[n] += ev[n][0].elapsed_time(ev[n][1])
     per = {n: v / a.steps for n, v in per.items()}
     graph_ms = time_graph_replays(torch, step, stream, a.steps) if a.graph else None
-    nxt = measure_next(pace, pq, pk, pv, p_cu, S, p_vis, p_cuv, Nv, T, idx, K, stream)
-    nxt["preview_block"] = measure_preview(pace, wl, img, L, stream)
+    nxt = None
+    if a.config == 3:
+        nxt = measure_next(pace, ex["pq"], ex["pk"], ex["pv"], ex["p_cu"], ex["S"], ex["p_vis"], ex["p_cuv"],
+                           ex["Nv"], ex["T"], ex["idx"], ex["K"], stream)
+        nxt["preview_block"] = measure_preview(pace, wl, ex["img"], ex["layout"], stream)
 
-    # algorithmic work
-    win_sizes = np.diff(vit.cu_windows).astype(np.float64)
-    flop_win = 4.0 * dv * Hv * float(np.sum(win_sizes ** 2))
-    flop_full = 4.0 * dv * Hv * float(Np) ** 2
-    flop_pre = 4.0 * dq * Hq * (S * (S + 1) / 2.0)
-    flop_attn = flop_win + flop_full + flop_pre
-    bytes_win = 4.0 * Np * Hv * dv * 2 + 2.0 * Hv * Np * 4
-    bytes_sel = Hv * Np * 4 + Hq * Nv * 4 + 4 * K + 2.0 * K * hidden.shape[1] * 2
-    bytes_apc = H * W * 3 + 4.0 * L.n_patches
-    bytes_resize = H * W * 3 + oH * oW * 3
-    t_fwd = per["vit_fwd"] * 1e-3
-    achieved = flop_full / t_fwd / 1e12 if t_fwd > 0 else 0.0
-    value = flop_attn / (ms_per_step * 1e-3) / 1e12
+    roof_name, roof_label = B["roof"]
+    t_roof = per[roof_name] * 1e-3
+    achieved = work[roof_name][1] / t_roof / 1e12 if t_roof > 0 else 0.0
+    value = B["flop_attn"] / (ms_per_step * 1e-3) / 1e12
+    sel_ms = per["select"]
+
+    step_roofline = {}
+    labels = {"apc": "apc_density", "resize": "apc_downsample", "vit_win": "vit_window_attention",
+              "vit_fwd": "vit_full_attention_fwd", "prefill": "prefill_attention_with_mass",
+              "select": "ddae_select_gather"}
+    for n in names:
+        if n == "vit_mass":
+            continue
+        bound, amount = work[n]
+        step_roofline[labels[n]] = _hbm_row(amount, per[n]) if bound == "hbm" else _mfma_row(amount, per[n])
+    if "vit_mass" in per:
+        step_roofline["vit_full_attention_fwd_plus_mass"] = _mfma_row(work["vit_fwd"][1], per["vit_fwd"] + per["vit_mass"])
 
     result = {
         "metric": "attn TFLOP/s (% bf16 MFMA peak) + DDAE select tokens/s (% HBM BW), 1 GPU",
@@ -275,51 +383,26 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic (seeded Qwen2.5-VL-7B-shaped inputs)",
-        "config": {"workload": wl.CONFIG_NAMES[a.config], "image": f"{W}x{H}",
-                   "vit_patches": int(Np), "vit_heads": int(Hv), "vit_head_dim": int(dv),
-                   "windows": int(len(win_sizes)), "prefill_tokens": S, "visual_tokens": Nv,
-                   "text_tokens": T, "llm_heads": f"{Hq}/{Hkv}", "llm_head_dim": int(dq),
-                   "keep": K, "hidden": int(hidden.shape[1]), "resize_to": f"{oW}x{oH}"},
-        "roofline": {"kernel": "attn_fwd_rot<80> (vision full attention, 42,196 patches x 16 heads)",
-                     "bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
+        "config": B["config"],
+        "roofline": {"kernel": roof_label, "bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-                     "traffic": measured_traffic()},
+                     "traffic": measured_traffic() if a.config == 3 else None},
         "schedule": "vision mass on a second stream beside the prefill; breakdown_ms and step_roofline "
                     "from the same steps run serially on one stream",
         "serial_ms_per_step": round(serial_ms, 4),
         "breakdown_ms": {n: round(v, 4) for n, v in per.items()},
         "graph_ms_per_step": None if graph_ms is None else round(graph_ms, 4),
-        "attention": {
-            "vit_full_fwd_tflops": round(achieved, 2),
-            "vit_full_fwd_plus_mass_tflops": round(flop_full / ((per["vit_fwd"] + per["vit_mass"]) * 1e-3) / 1e12, 2)
-            if per["vit_fwd"] + per["vit_mass"] > 0 else None,
-            "prefill_fwd_plus_mass_tflops": round(flop_pre / (per["prefill"] * 1e-3) / 1e12, 2)
-            if per["prefill"] > 0 else None,
-            "vit_window_gbs": round(bytes_win / (per["vit_win"] * 1e-3) / 1e9, 1) if per["vit_win"] > 0 else None,
-        },
         "select": {
-            "tokens_per_s": round(Nv / (per["select"] * 1e-3), 1) if per["select"] > 0 else None,
-            "gbs": round(bytes_sel / (per["select"] * 1e-3) / 1e9, 1) if per["select"] > 0 else None,
-            "hbm_frac": round(bytes_sel / (per["select"] * 1e-3) / 1e9 / PEAK_HBM_GBS, 4) if per["select"] > 0 else None,
-        },
-        "apc": {
-            "density_gbs": round(bytes_apc / (per["apc"] * 1e-3) / 1e9, 1) if per["apc"] > 0 else None,
-            "resize_gbs": round(bytes_resize / (per["resize"] * 1e-3) / 1e9, 1) if per["resize"] > 0 else None,
+            "tokens_per_s": round(ex["Nv"] / (sel_ms * 1e-3), 1) if sel_ms > 0 else None,
+            "gbs": round(work["select"][1] / (sel_ms * 1e-3) / 1e9, 1) if sel_ms > 0 else None,
+            "hbm_frac": round(work["select"][1] / (sel_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4) if sel_ms > 0 else None,
         },
         # every step of the path against the roofline that bounds it (algorithmic work per step)
-        "step_roofline": {
-            "apc_density": _hbm_row(bytes_apc, per["apc"]),
-            "apc_downsample": _hbm_row(bytes_resize, per["resize"]),
-            "vit_window_attention": _hbm_row(bytes_win, per["vit_win"]),
-            "vit_full_attention_fwd": _mfma_row(flop_full, per["vit_fwd"]),
-            "vit_full_attention_fwd_plus_mass": _mfma_row(flop_full, per["vit_fwd"] + per["vit_mass"]),
-            "prefill_attention_with_mass": _mfma_row(flop_pre, per["prefill"]),
-            "ddae_select_gather": _hbm_row(bytes_sel, per["select"]),
-        },
+        "step_roofline": step_roofline,
         "next": nxt,
     }
     if a.cpu_seconds > 0:
-        result["cpu_baseline"] = cpu_baseline(vit, a.cpu_seconds)
+        result["cpu_baseline"] = cpu_baseline(ex["w"], a.cpu_seconds)
     print(json.dumps(result), flush=True)
 
 
@@ -441,10 +524,11 @@ def measure_preview(pace, wl, img, L, stream, reps=3):
                     "training-free pixel-statistic previews with their densities"}
 
 
-def cpu_baseline(vit, budget_s: float):
-    """The float64 oracle (unchanged) on the host cores: O and LSE of query rows of the 4K
-    full attention, all 16 heads, over all 42,196 keys, in chunks of 256 rows until the time
-    budget is spent.  Reported in the metric's unit (algorithmic attention TFLOP/s)."""
+def cpu_baseline(w, budget_s: float):
+    """The float64 oracle (unchanged) on the host cores, in the metric's unit (algorithmic attention
+    TFLOP/s): O and LSE of query rows of the first image's full attention, all 16 heads, over all of
+    its keys, in chunks of 256 rows until the time budget is spent; for the tiny workload (no vision
+    encoder), the whole causal prefill, repeated until the budget is spent."""
     import numpy as np
 
     from oracle import attention as oatt
@@ -460,21 +544,36 @@ def cpu_baseline(vit, budget_s: float):
         pass
     if cores is None:
         cores = len(os.sched_getaffinity(0))
-    q = wl.bf16_bits_to_f64(vit.q)
-    k = wl.bf16_bits_to_f64(vit.k)
-    v = wl.bf16_bits_to_f64(vit.v)
-    N, H, d = q.shape
-    rows_done = 0
     t0 = time.perf_counter()
-    while time.perf_counter() - t0 < budget_s and rows_done < N:
-        rows = np.arange(rows_done, min(N, rows_done + 256))
-        oatt.attention_rows(q, k, v, 0, N, rows, False, 1 / math.sqrt(d))
-        rows_done += rows.size
-    dt = time.perf_counter() - t0
-    flops = 4.0 * d * H * rows_done * N
+    if w.vit is None:
+        p = w.prefill
+        q, k, v = (wl.bf16_bits_to_f64(x) for x in (p.q, p.k, p.v))
+        S = int(p.cu_seqlens[-1])
+        reps = 0
+        while time.perf_counter() - t0 < budget_s:
+            oatt.prefill_attention(q, k, v, p.cu_seqlens, p.vis_len, p.mq_start, p.mq_len, 1 / math.sqrt(q.shape[2]))
+            reps += 1
+        dt = time.perf_counter() - t0
+        flops = reps * 4.0 * q.shape[2] * q.shape[1] * S * (S + 1) / 2.0
+        sample = f"float64 oracle causal prefill with text-query mass ({S} tokens, {q.shape[1]} heads), {reps} runs, {dt:.1f} s wall"
+    else:
+        vit = w.vit
+        n0 = int(vit.cu_full[1])
+        q = wl.bf16_bits_to_f64(vit.q[:n0])
+        k = wl.bf16_bits_to_f64(vit.k[:n0])
+        v = wl.bf16_bits_to_f64(vit.v[:n0])
+        N, H, d = q.shape
+        rows_done = 0
+        while time.perf_counter() - t0 < budget_s and rows_done < N:
+            rows = np.arange(rows_done, min(N, rows_done + 256))
+            oatt.attention_rows(q, k, v, 0, N, rows, False, 1 / math.sqrt(d))
+            rows_done += rows.size
+        dt = time.perf_counter() - t0
+        flops = 4.0 * d * H * rows_done * N
+        sample = (f"float64 oracle attention (O, LSE) for the first {rows_done} of {N} query rows x {H} heads of "
+                  f"the first image's full attention over all {N} keys, {dt:.1f} s wall")
     return {"value": round(flops / dt / 1e12, 5), "unit": "TFLOP/s", "cores": cores, "kind": "oracle",
-            "sample": f"float64 oracle attention (O, LSE) for the first {rows_done} of {N} query rows "
-                      f"x {H} heads of the 4K full attention over all {N} keys, {dt:.1f} s wall"}
+            "cpu_model": cpu_model(), "sample": sample}
 
 
 if __name__ == "__main__":

@@ -166,7 +166,9 @@ class PrefillInputs:
     text_len: np.ndarray         # int32 [B]
     cu_vis: np.ndarray           # int32 [B+1] offsets of each sequence's visual keys in mass
     salient: List[np.ndarray]    # per sequence: visual token ids made salient
-    q_f32: Optional[np.ndarray] = None   # tiny config: pre-rounding float32 values
+    q_f32: Optional[np.ndarray] = None   # tiny config: pre-rounding float32 values of q, k, v
+    k_f32: Optional[np.ndarray] = None
+    v_f32: Optional[np.ndarray] = None
 
     @property
     def mq_start(self) -> np.ndarray:
@@ -244,7 +246,7 @@ def _prefill(config_id: int, vis_lens: List[int], text_lens: List[int], hq: int,
         q=f32_to_bf16_bits(q), k=f32_to_bf16_bits(k), v=f32_to_bf16_bits(v),
         cu_seqlens=cu, vis_len=np.asarray(vis_lens, dtype=np.int32),
         text_len=np.asarray(text_lens, dtype=np.int32), cu_vis=cuv, salient=sal_list,
-        q_f32=(q if keep_f32 else None))
+        q_f32=(q if keep_f32 else None), k_f32=(k if keep_f32 else None), v_f32=(v if keep_f32 else None))
 
 
 def _vit(config_id: int, layouts: List[VitLayout]) -> VitInputs:
