@@ -31,8 +31,10 @@
  *     the host, synchronises the stream and checks it first, returning
  *     PACE_ERR_INVALID_ARG before any launch when it is inconsistent.
  *   - The library keeps no global mutable state other than the thread-local
- *     error message, so independent calls may run concurrently on different
- *     streams.
+ *     error message and, for pace_ddae_select_varlen_noalloc only, a static per-GPU
+ *     scratch array and the table of its device addresses, so independent calls (other
+ *     than overlapping calls of that entry point on one GPU) may run concurrently on
+ *     different streams.
  */
 #ifndef PACE_H_
 #define PACE_H_
@@ -360,6 +362,28 @@ pace_status_t pace_ddae_select(const float* vis_mass, int Hv, int merge, const i
                                float w_llm_fixed, int K, const void* hidden, size_t row_bytes,
                                int32_t* idx_out, float* score_out, float* fuse_out, void* out,
                                void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * pace_ddae_select_varlen without a workspace argument, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation).  It allocates nothing: its scratch is a static device array of
+ * pace_ddae_select_noalloc_max_bytes() bytes (4 MiB), one per GPU, held until the process ends;
+ * its device address is looked up on the first call on each device (hipGetSymbolAddress, with
+ * that device current).  Arguments and results as in pace_ddae_select_varlen.
+ *   Returns PACE_ERR_WORKSPACE, launching nothing, when the selection needs more scratch than
+ *   that (pace_ddae_select_workspace_size(sum nv_host, B) > 4 MiB, about 300,000 tokens).
+ *   Every call on a GPU shares that GPU's scratch, so calls that overlap on one GPU (on
+ *   different streams, or from different threads without ordering) race; calls in one
+ *   stream's order do not.  With PACE_DEBUG=1 it copies and synchronises like the workspace
+ *   form (leave PACE_DEBUG unset under graph capture).
+ */
+size_t pace_ddae_select_noalloc_max_bytes(void);
+pace_status_t pace_ddae_select_varlen_noalloc(const float* vis_mass, int Hv, int merge,
+                                              const int32_t* vis_perm, const float* llm_mass, int Hl,
+                                              int B, const int* nv_host, const int* keep_host, int mode,
+                                              float tau, float w_llm_fixed, const void* hidden,
+                                              size_t row_bytes, int32_t* idx_out, float* score_out,
+                                              float* fuse_out, void* out, hipStream_t stream);
 
 /*
  * The ranking and pruning steps alone (end of Section 3.3): top-K of given fp32

@@ -19,6 +19,7 @@
 // from memory in every pass) and gather_rows.
 #include <math.h>
 
+#include <mutex>
 #include <vector>
 
 #include "pace_internal.h"
@@ -747,6 +748,39 @@ void size_select(Sizer& s, int nv_total, int nseg) {
 }
 
 }  // namespace
+
+// ---------------------------------------------------------------- allocation-free selection
+// Scratch of pace_ddae_select_varlen_noalloc: a device array of fixed size, one copy per GPU
+// (each holds it until the process ends), standing in for the caller's workspace.  Nothing in
+// it must start at zero: every selection writes each value it later reads.  Host code never
+// passes the array's name to a kernel (on the host it is only a stand-in): it looks up the
+// array's device address once per device, with that device current, and passes that.
+constexpr size_t kNoAllocScratchBytes = size_t(4) << 20;
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_dev[kMaxDevices] = {};
+
+pace_status_t scratch_on_current_device(void** out) {
+  int dev = -1;
+  const hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return set_error(PACE_ERR_HIP, "hipGetDevice: %s", hipGetErrorString(e));
+  if (dev < 0 || dev >= kMaxDevices)
+    return set_error(PACE_ERR_UNSUPPORTED, "device %d: at most %d devices", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_dev[dev] == nullptr) {
+    void* ptr = nullptr;
+    const hipError_t r = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (r != hipSuccess || ptr == nullptr)
+      return set_error(PACE_ERR_HIP, "hipGetSymbolAddress(scratch) on device %d: %s", dev, hipGetErrorString(r));
+    g_scratch_dev[dev] = ptr;
+  }
+  *out = g_scratch_dev[dev];
+  return PACE_OK;
+}
+}  // namespace
 }  // namespace pace
 
 using namespace pace;
@@ -837,6 +871,37 @@ pace_status_t pace_ddae_select(const float* vis_mass, int Hv, int merge, const i
   return pace_ddae_select_varlen(vis_mass, Hv, merge, vis_perm, llm_mass, Hl, 1, nv, kk, mode, tau,
                                  w_llm_fixed, hidden, row_bytes, idx_out, score_out, fuse_out, out,
                                  workspace, workspace_bytes, stream);
+}
+
+size_t pace_ddae_select_noalloc_max_bytes(void) { return kNoAllocScratchBytes; }
+
+pace_status_t pace_ddae_select_varlen_noalloc(const float* vis_mass, int Hv, int merge,
+                                              const int32_t* vis_perm, const float* llm_mass, int Hl,
+                                              int B, const int* nv_host, const int* keep_host, int mode,
+                                              float tau, float w_llm_fixed, const void* hidden,
+                                              size_t row_bytes, int32_t* idx_out, float* score_out,
+                                              float* fuse_out, void* out, hipStream_t stream) {
+  PACE_REQUIRE(B >= 1 && B <= PACE_MAX_SEGMENTS, "pace_ddae_select_varlen_noalloc: B=%d not in [1, %d]", B,
+               PACE_MAX_SEGMENTS);
+  PACE_REQUIRE(nv_host && keep_host, "pace_ddae_select_varlen_noalloc: null host count arrays");
+  long long nv_total = 0;
+  for (int b = 0; b < B; ++b) {
+    PACE_REQUIRE(nv_host[b] >= 1, "pace_ddae_select_varlen_noalloc: image %d has %d tokens", b, nv_host[b]);
+    nv_total += nv_host[b];
+  }
+  PACE_REQUIRE(nv_total < (1ll << 30), "pace_ddae_select_varlen_noalloc: too many tokens");
+  const size_t need = pace_ddae_select_workspace_size(static_cast<int>(nv_total), B);
+  if (need > kNoAllocScratchBytes)
+    return set_error(PACE_ERR_WORKSPACE,
+                     "pace_ddae_select_varlen_noalloc: %lld tokens in %d images need %zu bytes of scratch, "
+                     "more than the %zu of the static scratch; use pace_ddae_select_varlen with a workspace",
+                     nv_total, B, need, kNoAllocScratchBytes);
+  void* ws = nullptr;
+  pace_status_t st = scratch_on_current_device(&ws);
+  if (st != PACE_OK) return st;
+  return pace_ddae_select_varlen(vis_mass, Hv, merge, vis_perm, llm_mass, Hl, B, nv_host, keep_host, mode,
+                                 tau, w_llm_fixed, hidden, row_bytes, idx_out, score_out, fuse_out, out, ws,
+                                 kNoAllocScratchBytes, stream);
 }
 
 pace_status_t pace_topk_gather(const float* scores, int N, int K, const void* hidden,

@@ -66,6 +66,10 @@ _PROTOS = {
     "pace_ddae_select": (c_int, [c_void, c_int, c_int, c_void, c_void, c_int, c_int, c_int, c_float,
                                  c_float, c_int, c_void, c_size, c_void, c_void, c_void, c_void,
                                  c_void, c_size, c_void]),
+    "pace_ddae_select_noalloc_max_bytes": (c_size, []),
+    "pace_ddae_select_varlen_noalloc": (c_int, [c_void, c_int, c_int, c_void, c_void, c_int, c_int, c_int_p,
+                                                c_int_p, c_int, c_float, c_float, c_void, c_size, c_void,
+                                                c_void, c_void, c_void, c_void]),
     "pace_topk_gather": (c_int, [c_void, c_int, c_int, c_void, c_size, c_void, c_void, c_void, c_size,
                                  c_void]),
     "pace_gather_rows": (c_int, [c_void, c_int, c_size, c_void, c_int, c_void, c_void]),
@@ -416,6 +420,36 @@ def ddae_select(vis_mass: torch.Tensor, merge: int, vis_perm: Optional[torch.Ten
         float(tau), float(w_llm_fixed), _ptr(hidden), row_bytes, _ptr(idx_out), _ptr(score_out),
         _ptr(fuse_out), _ptr(out), _ptr(workspace), workspace.numel(), _stream()),
         "pace_ddae_select_varlen")
+    return idx_out[:ktot], score_out, fuse_out, (out[:ktot] if out is not None else None)
+
+
+def ddae_select_noalloc(vis_mass: torch.Tensor, merge: int, vis_perm: Optional[torch.Tensor],
+                        llm_mass: torch.Tensor, nv: Sequence[int], keep: Sequence[int], mode: int = 0,
+                        tau: float = 0.5, w_llm_fixed: float = 0.5, hidden: Optional[torch.Tensor] = None,
+                        idx_out=None, score_out=None, fuse_out=None, out=None):
+    """pace_ddae_select_varlen_noalloc: ddae_select without a workspace (the library's static
+    per-GPU scratch); outputs are the caller's tensors, allocated here only when not given."""
+    B = len(nv)
+    dev = llm_mass.device
+    nv_total = int(sum(nv))
+    ktot = int(sum(keep))
+    if idx_out is None:
+        idx_out = torch.empty(max(1, ktot), dtype=torch.int32, device=dev)
+    if score_out is None:
+        score_out = torch.empty(nv_total, dtype=torch.float32, device=dev)
+    if fuse_out is None:
+        fuse_out = torch.empty((B, 4), dtype=torch.float32, device=dev)
+    row_bytes = 0
+    if hidden is not None:
+        row_bytes = hidden[0].numel() * hidden.element_size()
+        if out is None:
+            out = torch.empty((max(1, ktot),) + tuple(hidden.shape[1:]), dtype=hidden.dtype, device=dev)
+    nv_a = (ctypes.c_int * B)(*[int(x) for x in nv])
+    kp_a = (ctypes.c_int * B)(*[int(x) for x in keep])
+    _check(lib().pace_ddae_select_varlen_noalloc(
+        _ptr(vis_mass), vis_mass.shape[0], merge, _ptr(vis_perm), _ptr(llm_mass), llm_mass.shape[0], B, nv_a,
+        kp_a, int(mode), float(tau), float(w_llm_fixed), _ptr(hidden), row_bytes, _ptr(idx_out),
+        _ptr(score_out), _ptr(fuse_out), _ptr(out), _stream()), "pace_ddae_select_varlen_noalloc")
     return idx_out[:ktot], score_out, fuse_out, (out[:ktot] if out is not None else None)
 
 

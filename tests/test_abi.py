@@ -146,3 +146,23 @@ def test_workspace_sizes_monotone():
     assert L.pace_vit_attention_workspace_size(42196, 16, 80, 1, 42196) == lse + vt + 1 * 16 * 4
     assert L.pace_vit_attention_workspace_size(42196, 16, 128, 1, 42196) == 42196 * 16 * 4
 
+
+def test_noalloc_select_rejects_more_than_its_scratch():
+    """The allocation-free selection refuses, before touching the GPU, a batch whose scratch would
+    exceed the static 4 MiB; bad counts are refused the same way."""
+    L = pace.lib()
+    cap = L.pace_ddae_select_noalloc_max_bytes()
+    assert cap == 4 << 20
+    big = 400000
+    assert L.pace_ddae_select_workspace_size(big, 1) > cap >= L.pace_ddae_select_workspace_size(300000, 1)
+    one = (ctypes.c_int * 1)
+    null = None
+    st = L.pace_ddae_select_varlen_noalloc(null, 16, 4, null, null, 28, 1, one(big), one(10), 0, 0.5, 0.5,
+                                           null, 0, null, null, null, null, null)
+    assert st == 3 and b"static scratch" in L.pace_last_error()
+    st = L.pace_ddae_select_varlen_noalloc(null, 16, 4, null, null, 28, 1, one(0), one(0), 0, 0.5, 0.5,
+                                           null, 0, null, null, null, null, null)
+    assert st == 1
+    st = L.pace_ddae_select_varlen_noalloc(null, 16, 4, null, null, 28, 65, one(5), one(1), 0, 0.5, 0.5,
+                                           null, 0, null, null, null, null, null)
+    assert st == 1
