@@ -72,7 +72,67 @@ def parse():
                          "of known size that calibrates the HBM byte counters of a profile run)")
     ap.add_argument("--no-graph", dest="graph", action="store_false",
                     help="skip timing the step captured in a HIP graph and replayed")
+    ap.add_argument("--select-sweep", action="store_true",
+                    help="instead of the step: DDAE selection + gather over batches of 1, 4, 16 and 64 "
+                         "images of 4K-frame shapes (one JSON line per batch)")
     return ap.parse_args()
+
+
+def select_sweep(a):
+    """DDAE fuse + top-K + gather (pace_ddae_select_varlen, one call) over B images of the 4K frame's
+    shapes (16 x 42,196 vision masses, 28 x 10,549 text masses, the window-order permutation, a
+    10,549 x 3584 bf16 hidden matrix per image, K = 1,055 each), B = 1, 4, 16, 64: how the rate
+    approaches the HBM roofline once the fixed latency of the two launches is amortised.  Masses are
+    seeded Gamma draws (the selection's cost does not depend on their values)."""
+    import numpy as np
+    import torch
+
+    from paper_2608_27206_amd import pace
+    from paper_2608_27206_amd import workloads as wl
+
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda:0")
+    L = wl.vit_layout(2156 // 14, 3836 // 14)
+    nv, npatch = L.n_vis, L.n_patches
+    K = pace.keep_count(0.10, nv)
+    stream = torch.cuda.current_stream()
+    for B in (1, 4, 16, 64):
+        g = torch.Generator(device=dev)
+        g.manual_seed(1000 + B)
+        vis = torch.empty((16, B * npatch), device=dev).exponential_(generator=g)
+        llm = torch.empty((28, B * nv), device=dev).exponential_(generator=g)
+        perm = torch.from_numpy(np.tile(L.vis_perm.astype(np.int32), B)).to(dev)
+        hidden = torch.empty((B * nv, wl.HIDDEN), dtype=torch.bfloat16, device=dev).normal_(generator=g)
+        nvs, keeps = [nv] * B, [K] * B
+        idx = torch.empty(B * K, dtype=torch.int32, device=dev)
+        sc = torch.empty(B * nv, dtype=torch.float32, device=dev)
+        fz = torch.empty((B, 4), dtype=torch.float32, device=dev)
+        out = torch.empty((B * K, wl.HIDDEN), dtype=torch.bfloat16, device=dev)
+        ws = torch.empty(pace.lib().pace_ddae_select_workspace_size(B * nv, B), dtype=torch.uint8, device=dev)
+
+        def call():
+            pace.ddae_select(vis, 4, perm, llm, nvs, keeps, mode=0, tau=0.5, hidden=hidden, idx_out=idx,
+                             score_out=sc, fuse_out=fz, out=out, workspace=ws)
+        for _ in range(3):
+            call()
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(max(5, a.steps)):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            call()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1))
+        ms = sorted(ts)[len(ts) // 2]
+        nbytes = float(B) * (16 * npatch * 4 + 28 * nv * 4 + 4 * K + 2.0 * K * wl.HIDDEN * 2)
+        gbs = nbytes / (ms * 1e-3) / 1e9
+        print(json.dumps({"select_sweep": {"images": B, "tokens": B * nv, "kept": B * K, "ms": round(ms, 4),
+                                           "tokens_per_s": round(B * nv / (ms * 1e-3), 1),
+                                           "algorithmic_bytes": int(nbytes), "gbs": round(gbs, 1),
+                                           "hbm_frac": round(gbs / PEAK_HBM_GBS, 4)}}), flush=True)
+        del vis, llm, perm, hidden, out, ws
+        torch.cuda.empty_cache()
 
 
 def time_graph_replays(torch, step, stream, steps):
@@ -272,6 +332,9 @@ def main():
         print(json.dumps({"error": "the benchmark runs on one GPU only; --gpus must be 1 "
                           "(multi-GPU sharding is described in the design notes, not built)"}))
         sys.exit(2)
+    if a.select_sweep:
+        select_sweep(a)
+        return
     import numpy as np
     import torch
 

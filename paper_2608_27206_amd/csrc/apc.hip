@@ -2,8 +2,9 @@
 // the bicubic resize by sqrt(r) per side (Appendix implementation details).
 //
 // Density, five launches (all HBM/L2-bound, fixed reduction orders -> deterministic):
-//   apc_patch_pass<0>  per patch-strip tile: ||f_i|| -> 1/||f_i||, and the tile's partial
-//                      sum of T_i = f_i/||f_i|| over its patches (one 588-vector per tile)
+//   apc_patch_pass<0>  per patch-strip tile: ||f_i|| -> 1/||f_i|| (from exact integer sums of
+//                      the bytes and their squares), and the tile's partial sum of
+//                      T_i = f_i/||f_i|| over its patches (one 588-vector per tile)
 //   apc_reduce_c       sum of the tile partials per component -> sum_i T_i
 //   apc_finalize_c     c = mean T_i, phi = ||c||^2 (equal to Eq. 1's mean pairwise cosine),
 //                      rho_g = 1 - phi (Eq. 2), c_hat = c/||c||
@@ -73,11 +74,14 @@ __device__ __forceinline__ int stage_tile(const DensityParams& p, int tile, uint
   const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint8_t*>(p.img), (short)0, total, 0x00020000);
   const int nd = (row_bytes + 3) / 4 + 1;   // <= 4 * kApcThreads dwords per row
-  // four rows at a time, all sixteen loads of a thread in flight before the LDS writes
-  for (int r0 = 0; r0 < p.P; r0 += 4) {
-    uint32_t v[4][4];
+  // eight rows at a time (P <= 16: one or two batches), all of a thread's loads of a batch in
+  // flight before its LDS writes
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
+  for (int r0 = 0; r0 < kMaxPatch; r0 += 8) {
+    if (r0 >= p.P) break;
+    uint32_t v[8][4];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
       const int r = r0 + q;
       const int a0 = ((py * p.P + r) * p.W * 3 + px0 * p.P * 3) & ~3;
 #pragma unroll
@@ -87,7 +91,7 @@ __device__ __forceinline__ int stage_tile(const DensityParams& p, int tile, uint
       }
     }
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
+    for (int q = 0; q < 8; ++q) {
       const int a0 = ((py * p.P + r0 + q) * p.W * 3 + px0 * p.P * 3) & ~3;
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
@@ -96,7 +100,7 @@ __device__ __forceinline__ int stage_tile(const DensityParams& p, int tile, uint
       }
     }
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
+    for (int q = 0; q < 8; ++q) {
       const int r = r0 + q;
       if (r < p.P) {
         const int b0 = (py * p.P + r) * p.W * 3 + px0 * p.P * 3;
@@ -136,31 +140,31 @@ __global__ __launch_bounds__(kApcThreads) void apc_patch_pass(const DensityParam
   const int rb = p.row_dwords * 4;
   const int pb = 3 * p.P;                  // bytes of one patch row
   const int j = threadIdx.x >> 2, t = threadIdx.x & 3;
-  float acc = 0.f;
-  if (j < np) {
-    // the four threads of a patch take every fourth byte of each of its rows
-    float s = 0.f;
-    if (PASS == 1) s = p.inv_norm[py * p.gw + px0 + j];
-    for (int r = 0; r < p.P; ++r) {
-      const uint8_t* row = pxb + r * rb + shift[r] + j * pb;
-      const float* cr = chat + r * pb;
-#pragma unroll 4
-      for (int cb = t; cb < pb; cb += 4) {
-        const float x = feat_of(row[cb]);
-        if (PASS == 0) {
-          acc += x * x;
-        } else {
-          const float y = x * s - cr[cb];
-          acc += y * y;
+  if (PASS == 0) {
+    // ||f||^2 = sum (b/127.5 - 1)^2 = (4 sum b^2 - 1020 sum b + 65025 D) / 65025, from exact
+    // integer sums: the four threads of a patch take every fourth dword of each of its rows
+    // (bytes outside the patch masked off) and add b^2 and b with packed-byte dot products
+    uint32_t sq = 0u, sm = 0u;
+    if (j < np) {
+      for (int r = 0; r < p.P; ++r) {
+        const int o = r * rb + shift[r] + j * pb;   // first byte of the patch's row r
+        const int k0 = o >> 2, k1 = (o + pb - 1) >> 2;
+        for (int k = k0 + t; k <= k1; k += 4) {
+          const int lo = max(o - 4 * k, 0), hi = min(o + pb - 4 * k, 4);
+          const uint32_t keep = (hi >= 4 ? 0xffffffffu : ((1u << (8 * hi)) - 1u)) & ~((1u << (8 * lo)) - 1u);
+          const uint32_t w = px[k] & keep;
+          sq = __builtin_amdgcn_udot4(w, w, sq, false);
+          sm = __builtin_amdgcn_udot4(w, 0x01010101u, sm, false);
         }
       }
     }
-  }
-  acc += __shfl_xor(acc, 1, 64);
-  acc += __shfl_xor(acc, 2, 64);
-  if (PASS == 0) {
+    sq += __shfl_xor(sq, 1, 64);
+    sq += __shfl_xor(sq, 2, 64);
+    sm += __shfl_xor(sm, 1, 64);
+    sm += __shfl_xor(sm, 2, 64);
     if (j < np && t == 0) {
-      const float in = 1.0f / sqrtf(acc);
+      const int num = 4 * static_cast<int>(sq) - 1020 * static_cast<int>(sm) + 65025 * p.D;
+      const float in = 255.0f / sqrtf(static_cast<float>(num));
       inv[j] = in;
       p.inv_norm[py * p.gw + px0 + j] = in;
     }
@@ -175,6 +179,22 @@ __global__ __launch_bounds__(kApcThreads) void apc_patch_pass(const DensityParam
       p.partial[static_cast<long long>(tile) * p.D + e] = sum;
     }
   } else {
+    float acc = 0.f;
+    if (j < np) {
+      // the four threads of a patch take every fourth byte of each of its rows
+      const float s = p.inv_norm[py * p.gw + px0 + j];
+      for (int r = 0; r < p.P; ++r) {
+        const uint8_t* row = pxb + r * rb + shift[r] + j * pb;
+        const float* cr = chat + r * pb;
+#pragma unroll 4
+        for (int cb = t; cb < pb; cb += 4) {
+          const float y = feat_of(row[cb]) * s - cr[cb];
+          acc += y * y;
+        }
+      }
+    }
+    acc += __shfl_xor(acc, 1, 64);
+    acc += __shfl_xor(acc, 2, 64);
     if (j < np && t == 0) p.d[py * p.gw + px0 + j] = sqrtf(acc);
   }
 }

@@ -650,12 +650,18 @@ __global__ __launch_bounds__(kSelThreads) void ddae_select_gather(const SelectPa
   for (int j = 0; j < kSelR; ++j) kc += key[j];
   uint32_t tot_keep = 0;
   uint32_t pos = block_excl_scan(kc, wt[2], &tot_keep);
-  const auto ri = range_rsrc(p.idx + out0, lead ? static_cast<unsigned>(K) * 4u : 0u);
+  if (lead) {   // the kept indices (one workgroup stores them; the others only need their slice)
+    const auto ri = range_rsrc(p.idx + out0, static_cast<unsigned>(K) * 4u);
+    uint32_t ps = pos;
+#pragma unroll
+    for (int j = 0; j < kSelR; ++j) {
+      rstore_b32(ri, key[j] ? ps * 4u : kNoStore, static_cast<uint32_t>(n0 + base + j));
+      ps += key[j];
+    }
+  }
 #pragma unroll
   for (int j = 0; j < kSelR; ++j) {
-    const int src = n0 + base + j;
-    rstore_b32(ri, key[j] ? pos * 4u : kNoStore, static_cast<uint32_t>(src));
-    if (key[j] && static_cast<int>(pos) >= r0 && static_cast<int>(pos) < r1) rows_lds[pos - r0] = src;
+    if (key[j] && static_cast<int>(pos) >= r0 && static_cast<int>(pos) < r1) rows_lds[pos - r0] = n0 + base + j;
     pos += key[j];
   }
   if (p.hidden == nullptr || r1 <= r0) return;
