@@ -687,43 +687,57 @@ __device__ __forceinline__ int make_taps(int o, int n, int m, int slots, float* 
   return lo + j0;
 }
 
-// make_taps with the candidate weights in registers (slots <= kRegTaps): one LDS write per
-// weight instead of a read-modify-write sequence through LDS.  Same weights, lo and count.
+// make_taps spread over a row of 16 lanes, lane j holding candidate j (slots <= 16): every
+// lane of the row evaluates one weight, the row's sum comes from a butterfly (every lane ends
+// with the same bits) and the first and last nonzero candidates from a ballot.  The same
+// weights, lo and count as make_taps up to the order of the normalising sum.  All 64 lanes
+// of the wave must call it together (`valid` false for rows of 16 with no coordinate); the
+// distance numerator is formed in 32 bits when 2 n m fits, which makes the same float.
 constexpr int kRegTaps = 16;
-__device__ __forceinline__ int make_taps_reg(int o, int n, int m, int slots, float* w_out, int* count) {
+__device__ __forceinline__ void make_taps_row16(int o, bool valid, int n, int m, int slots, float* w_out,
+                                                int* lo_out, int* count_out) {
+  const int lane = threadIdx.x & 63, j = lane & 15;
   const float centre = (static_cast<float>(o) + 0.5f) * static_cast<float>(n) / static_cast<float>(m);
   const float support = 2.f * fmaxf(1.f, static_cast<float>(n) / static_cast<float>(m));
   const int lo = max(static_cast<int>(floorf(centre - support - 0.5f)) - 1, 0);
   const float inv_den = 1.f / static_cast<float>(2ll * (n > m ? n : m));
-  long long num = (2ll * lo + 1) * m - (2ll * o + 1) * n;
-  float w[kRegTaps];
-  float sum = 0.f;
-  int j0 = kRegTaps, j1 = 0;
-#pragma unroll
-  for (int j = 0; j < kRegTaps; ++j, num += 2ll * m) {
-    const float wt = (j < slots && lo + j < n) ? keys_cubic(static_cast<float>(num) * inv_den) : 0.f;
-    w[j] = wt;
-    sum += wt;
-    if (wt != 0.f) { j0 = min(j0, j); j1 = j; }
+  float wt = 0.f;
+  if (valid && j < slots && lo + j < n) {
+    float num;
+    if (2ll * n * m < (1ll << 31))
+      num = static_cast<float>((2 * (lo + j) + 1) * m - (2 * o + 1) * n);
+    else
+      num = static_cast<float>((2ll * (lo + j) + 1) * m - (2ll * o + 1) * n);
+    wt = keys_cubic(num * inv_den);
   }
-  if (j0 > j1) j0 = j1;
-  const float inv = 1.f / sum;
+  float sum = wt;
+  sum += dpp_f32<kDppQuadXor1>(sum);
+  sum += dpp_f32<kDppQuadXor2>(sum);
+  sum += dpp_f32<kDppRowHalfMirror>(sum);
+  sum += dpp_f32<kDppRowMirror>(sum);
+  const uint32_t bits = static_cast<uint32_t>(__ballot(wt != 0.f) >> (lane & 48)) & 0xffffu;
+  if (!valid) return;
+  const int j1 = bits ? 31 - __builtin_clz(bits) : 0;
+  const int j0 = bits ? __builtin_ctz(bits) : 0;
   const int cnt = j1 - j0 + 1;
-#pragma unroll
-  for (int j = 0; j < kRegTaps; ++j) {
-    if (j >= j0 && j <= j1) w_out[j - j0] = w[j] * inv;
-    if (j >= cnt && j < slots) w_out[j] = 0.f;
-  }
-  *count = cnt;
-  return lo + j0;
+  const float inv = 1.f / sum;
+  if (j >= j0 && j <= j1) w_out[j - j0] = wt * inv;
+  if (j >= cnt && j < slots) w_out[j] = 0.f;
+  if (j == 0) { *lo_out = lo + j0; *count_out = cnt; }
 }
 
 // The resize with taps of at most kRegTaps per axis (shrinks up to 3x per side) and
 // tx dividing the block: the horizontal pass keeps one output column per thread, its
 // weights in registers, and reads each staged row's bytes as aligned dwords; the vertical
-// pass keeps one (column, channel) per thread.  Same arithmetic, in the same order, as
-// apc_resize.
+// pass keeps one (column, channel) and half of the tile's rows per thread.  NT bounds the
+// nonzero horizontal taps: the stretched kernel is nonzero on an open interval of width 4s,
+// which holds at most ceil(4s) + 1 sample points (the extra one when rounding leaves a
+// near-zero weight at an end), so the NT-tap loop runs unpredicated, the weights past a
+// column's count being zero (adding 0 * x leaves every sum bit for bit as it was).  Same
+// arithmetic, in the same order, as apc_resize.
+template <int NT>
 __global__ __launch_bounds__(kRsThreads) void apc_resize_reg(const ResizeParams p) {
+  constexpr int ND = (3 * NT + 3) / 4 + 1;   // dwords covering 3 NT bytes at any byte shift
   extern __shared__ float sm[];
   float* wx = sm + p.o_wx;                      // [tx][ntx], ntx a multiple of 4
   float* wy = sm + p.o_wy;                      // [ty][nty]
@@ -737,11 +751,15 @@ __global__ __launch_bounds__(kRsThreads) void apc_resize_reg(const ResizeParams 
   const int tid = threadIdx.x;
   const int ox0 = blockIdx.x * p.tx, oy0 = blockIdx.y * p.ty;
   const int ncols = min(p.tx, p.oW - ox0), nrows = min(p.ty, p.oH - oy0);
-  // columns on the first waves, rows on the last wave
-  if (tid < ncols) lox[tid] = make_taps_reg(ox0 + tid, p.W, p.oW, p.ntx, wx + tid * p.ntx, &cnx[tid]);
-  if (tid >= kRsThreads - 64 && tid - (kRsThreads - 64) < nrows) {
-    const int r = tid - (kRsThreads - 64);
-    loy[r] = make_taps_reg(oy0 + r, p.H, p.oH, p.nty, wy + r * p.nty, &cny[r]);
+  // taps: 16 lanes per output coordinate, the tile's columns first, then its rows
+  for (int b = 0; b < (p.tx + p.ty) * 16; b += kRsThreads) {
+    const int item = (b + tid) >> 4;
+    if (item < p.tx)
+      make_taps_row16(ox0 + item, item < ncols, p.W, p.oW, p.ntx, wx + item * p.ntx, &lox[item], &cnx[item]);
+    else {
+      const int r = min(item - p.tx, p.ty - 1);
+      make_taps_row16(oy0 + r, item - p.tx < nrows, p.H, p.oH, p.nty, wy + r * p.nty, &loy[r], &cny[r]);
+    }
   }
   __syncthreads();
   const int xlo = lox[0], ylo = loy[0];
@@ -755,24 +773,30 @@ __global__ __launch_bounds__(kRsThreads) void apc_resize_reg(const ResizeParams 
     const int b0 = (ylo + r) * p.W * 3 + xlo * 3;
     shift[r] = b0 - (b0 & ~3);
   }
-  for (int e0 = tid; e0 < yin * nd; e0 += 8 * kRsThreads) {
-    uint32_t v[8];
-    int slot[8], addr[8];
+  // staging: wave w takes rows w, w + 4, ..., lane l dwords l, l + 64, ...; eight loads in
+  // flight per lane before their LDS writes
+  {
+    const int w = tid >> 6, l = tid & 63;
+    for (int r0 = w; r0 < yin; r0 += 8 * (kRsThreads / 64)) {
+      for (int d = l; d - l < nd; d += 64) {
+        uint32_t v[8];
+        int addr[8];
+        bool ok[8];
 #pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const int e = e0 + u * kRsThreads;
-      const int r = e / nd, d = e - r * nd;
-      const int a0 = ((ylo + r) * p.W * 3 + xlo * 3) & ~3;
-      slot[u] = (e < yin * nd) ? r * p.row_dwords + d : -1;
-      addr[u] = a0 + 4 * d;
-      v[u] = (e < yin * nd) ? load_dword(rs, addr[u]) : 0u;
+        for (int u = 0; u < 8; ++u) {
+          const int r = r0 + u * (kRsThreads / 64);
+          ok[u] = r < yin && d < nd;
+          addr[u] = (((ylo + r) * p.W + xlo) * 3 & ~3) + 4 * d;
+          v[u] = ok[u] ? load_dword(rs, addr[u]) : 0u;
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          if (ok[u] && straddles(addr[u], total)) v[u] = load_dword_bytes(rs, addr[u], total);
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          if (ok[u]) pix[(r0 + u * (kRsThreads / 64)) * p.row_dwords + d] = v[u];
+      }
     }
-#pragma unroll
-    for (int u = 0; u < 8; ++u)
-      if (slot[u] >= 0 && straddles(addr[u], total)) v[u] = load_dword_bytes(rs, addr[u], total);
-#pragma unroll
-    for (int u = 0; u < 8; ++u)
-      if (slot[u] >= 0) pix[slot[u]] = v[u];
   }
   __syncthreads();
   // horizontal pass: thread -> output column c, staged rows g, g + G, ...
@@ -786,27 +810,24 @@ __global__ __launch_bounds__(kRsThreads) void apc_resize_reg(const ResizeParams 
                                          : make_float4(0.f, 0.f, 0.f, 0.f);
         wr[4 * q] = f.x; wr[4 * q + 1] = f.y; wr[4 * q + 2] = f.z; wr[4 * q + 3] = f.w;
       }
-      const int nt = cnx[c];
       const int xoff = (lox[c] - xlo) * 3;
       for (int r = g; r < yin; r += G) {
         const int off = shift[r] + xoff;                       // byte offset in the staged row
         const uint32_t* dp = pix + r * p.row_dwords + (off >> 2);
         const uint32_t sh = static_cast<uint32_t>(off & 3);
-        uint32_t d[13];
+        uint32_t d[ND];
 #pragma unroll
-        for (int k = 0; k < 13; ++k) d[k] = dp[k];
-        uint32_t e[12];
+        for (int k = 0; k < ND; ++k) d[k] = dp[k];
+        uint32_t e[ND - 1];
 #pragma unroll
-        for (int k = 0; k < 12; ++k) e[k] = __builtin_amdgcn_alignbyte(d[k + 1], d[k], sh);
+        for (int k = 0; k < ND - 1; ++k) e[k] = __builtin_amdgcn_alignbyte(d[k + 1], d[k], sh);
         float a0 = 0.f, a1 = 0.f, a2 = 0.f;
 #pragma unroll
-        for (int j = 0; j < kRegTaps; ++j) {
-          if (j < nt) {
-            const int b = 3 * j;
-            a0 += wr[j] * static_cast<float>((e[b >> 2] >> (8 * (b & 3))) & 255u);
-            a1 += wr[j] * static_cast<float>((e[(b + 1) >> 2] >> (8 * ((b + 1) & 3))) & 255u);
-            a2 += wr[j] * static_cast<float>((e[(b + 2) >> 2] >> (8 * ((b + 2) & 3))) & 255u);
-          }
+        for (int j = 0; j < NT; ++j) {
+          const int b = 3 * j;
+          a0 += wr[j] * static_cast<float>((e[b >> 2] >> (8 * (b & 3))) & 255u);
+          a1 += wr[j] * static_cast<float>((e[(b + 1) >> 2] >> (8 * ((b + 1) & 3))) & 255u);
+          a2 += wr[j] * static_cast<float>((e[(b + 2) >> 2] >> (8 * ((b + 2) & 3))) & 255u);
         }
         float* h = hb + (r * p.tx + c) * 3;
         h[0] = a0; h[1] = a1; h[2] = a2;
@@ -814,10 +835,13 @@ __global__ __launch_bounds__(kRsThreads) void apc_resize_reg(const ResizeParams 
     }
   }
   __syncthreads();
-  // vertical pass: thread -> (column, channel), every output row of the tile
-  if (tid < 3 * ncols) {
-    const int c = tid / 3, ch = tid - 3 * c;
-    for (int r = 0; r < nrows; ++r) {
+  // vertical pass: thread -> (column, channel), half of the tile's output rows
+  if (tid < 6 * ncols) {
+    const int half = tid >= 3 * ncols ? 1 : 0;
+    const int cc = tid - half * 3 * ncols;
+    const int c = cc / 3, ch = cc - 3 * c;
+    const int rmid = (nrows + 1) / 2;
+    for (int r = half * rmid; r < (half ? nrows : rmid); ++r) {
       const float* w = wy + r * p.nty;
       const int base = loy[r] - ylo;
       const int nt = cny[r];
@@ -1176,13 +1200,18 @@ pace_status_t pace_apc_downsample(const uint8_t* src, int H, int W, uint8_t* dst
   }
   dim3 grid((oW + tx - 1) / tx, (oH + ty - 1) / ty);
   const int ntx4 = (p.ntx + 3) / 4 * 4;
-  if (ntx4 <= kRegTaps && p.nty <= kRegTaps && kRsThreads % tx == 0 && 3 * tx <= kRsThreads &&
-      (tx == 64 || tx == 32 || tx == 16)) {
+  // nonzero horizontal taps per output column: at most ceil(4 sx) + 1 (see apc_resize_reg)
+  const int nz = static_cast<int>(ceil(4.0 * (sx > 1 ? sx : 1))) + 1;
+  if (ntx4 <= kRegTaps && p.nty <= kRegTaps && kRsThreads % tx == 0 &&
+      6 * tx <= kRsThreads && (tx == 32 || tx == 16)) {
     ResizeParams q = p;
     q.ntx = ntx4;
     const size_t lds_q = plan(ty, tx, q);
     if (lds_q <= kRsMaxLds) {
-      hipLaunchKernelGGL(apc_resize_reg, grid, dim3(kRsThreads), lds_q, stream, q);
+      // ntx4 <= 16 caps ceil(4 sx) at 12, so nz <= 13
+      if (nz <= 5) hipLaunchKernelGGL(apc_resize_reg<5>, grid, dim3(kRsThreads), lds_q, stream, q);
+      else if (nz <= 9) hipLaunchKernelGGL(apc_resize_reg<9>, grid, dim3(kRsThreads), lds_q, stream, q);
+      else hipLaunchKernelGGL(apc_resize_reg<13>, grid, dim3(kRsThreads), lds_q, stream, q);
       return check_launch("apc_resize_reg");
     }
   }

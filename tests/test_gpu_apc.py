@@ -99,7 +99,8 @@ def _check_resize(img, oh, ow):
 @pytest.mark.parametrize("shape,out", [((448, 448), (224, 224)), ((448, 448), (308, 308)),
                                        ((150, 333), (149, 100)), ((96, 128), (96, 128)),
                                        ((300, 200), (37, 23)), ((64, 64), (2, 2)),
-                                       ((2156, 3836), (1078, 1918))])
+                                       ((2156, 3836), (1078, 1918)), ((250, 200), (100, 80)),
+                                       ((300, 128), (150, 128)), ((210, 330), (90, 150))])
 def test_resize_parity(shape, out):
     img = wl.make_image(3, *shape)
     _check_resize(img, *out)
