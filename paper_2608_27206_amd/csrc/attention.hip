@@ -1239,11 +1239,75 @@ __global__ __launch_bounds__(kThreads, (D == 80 && !CAUSAL) ? 3 : 2) void attn_m
   };
 
   // Three query-tile buffers: Q(t+2) and its LSE rows are loaded while Q(t) is read, into the
-  // buffer of Q(t-1) that every wave left behind at this iteration's barrier.  No software
-  // pipelining within a wave: three workgroups per CU overlap one wave's MFMAs with the
-  // others' VALU work.
+  // buffer of Q(t-1) that every wave left behind at this iteration's barrier.
   const int ntiles = (ql + kMassQ - 1) / kMassQ;
-  if (ntiles > 0) {
+  if constexpr (D == 80 && !CAUSAL) {
+    // Pipelined within the wave, one 32-key x 32-row block of S^T at a time: the tile's blocks
+    // (half u, key set ks) go in the order (0,0) (0,1) (1,0) (1,1), and the MFMAs of each block
+    // are issued among the VALU work (exponentials and sums) of the block before it; the last
+    // block's VALU work moves to the next iteration, under the first block's MFMAs (it reads
+    // no LDS, so it may cross the barrier).  Two blocks of S^T are live at a time.  Every
+    // key's sum takes its terms in the same order as in the unpipelined loop below.
+    auto chain = [&](int ks, const bf16x8* qb) __attribute__((always_inline)) {
+      f32x16 r = mfma(kf[ks][0], qb[0], f32x16{});
+#pragma unroll
+      for (int c = 1; c < C::KC; ++c) r = mfma(kf[ks][c], qb[c], r);
+      return r;
+    };
+    auto sums = [&](const f32x16& sv, float l2, int ks) __attribute__((always_inline)) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) macc[ks][r] += fast_exp2(sv[r] * p.scale_log2 - l2);
+    };
+    auto q_frags = [&](int buf, int u, bf16x8* qb) __attribute__((always_inline)) {
+      const uint16_t* qp = &Qs[buf][(u * 32 + c32) * C::QS + g * 8];
+#pragma unroll
+      for (int c = 0; c < C::KC; ++c) qb[c] = *reinterpret_cast<const bf16x8*>(qp + c * 16);
+    };
+    // one MFMA among every six VALU instructions of the block before (the MFMAs go early)
+    auto interleave = [&]() __attribute__((always_inline)) {
+      static_for<0, C::KC>([&](auto) __attribute__((always_inline)) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);
+      });
+    };
+    if (ntiles > 0) {
+      load_q(0, 0);
+      if (ntiles > 1) load_q(1, 1);
+      int buf = 0;
+      f32x16 s3 = f32x16{};    // block (1,1) of the previous tile
+      float l2p = INFINITY;    // its rows' LSE: +inf makes the first iteration's sums add zeros
+      for (int t = 0; t < ntiles; ++t) {
+        wait_vmem_upto(t + 1 < ntiles ? dma_per_tile : 0);
+        __syncthreads();
+        const float l2a = load_lse2(t, buf, 0), l2b = load_lse2(t, buf, 1);
+        const int buf2 = (buf == 0) ? 2 : buf - 1;   // (t + 2) % 3
+        if (t + 2 < ntiles) load_q(t + 2, buf2);
+        bf16x8 qa[C::KC], qc[C::KC];
+        q_frags(buf, 0, qa);
+        __builtin_amdgcn_sched_barrier(0);
+        const f32x16 s0 = chain(0, qa);
+        sums(s3, l2p, 1);
+        interleave();
+        __builtin_amdgcn_sched_barrier(0);
+        q_frags(buf, 1, qc);
+        const f32x16 s1 = chain(1, qa);
+        sums(s0, l2a, 0);
+        interleave();
+        __builtin_amdgcn_sched_barrier(0);
+        const f32x16 s2 = chain(0, qc);
+        sums(s1, l2a, 1);
+        interleave();
+        __builtin_amdgcn_sched_barrier(0);
+        s3 = chain(1, qc);
+        sums(s2, l2b, 0);
+        interleave();
+        __builtin_amdgcn_sched_barrier(0);
+        l2p = l2b;
+        buf = (buf == 2) ? 0 : buf + 1;
+      }
+      sums(s3, l2p, 1);
+    }
+  } else if (ntiles > 0) {
     load_q(0, 0);
     if (ntiles > 1) load_q(1, 1);
     int buf = 0;
