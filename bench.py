@@ -71,7 +71,8 @@ def parse():
                     help="before warm-up, copy this many MiB device to device once (a plain copy "
                          "of known size that calibrates the HBM byte counters of a profile run)")
     ap.add_argument("--no-graph", dest="graph", action="store_false",
-                    help="skip timing the step captured in a HIP graph and replayed")
+                    help="time the steps launched kernel by kernel instead of replaying the step captured "
+                         "in a HIP graph")
     ap.add_argument("--select-sweep", action="store_true",
                     help="instead of the step: DDAE selection + gather over batches of 1, 4, 16 and 64 "
                          "images of 4K-frame shapes (one JSON line per batch)")
@@ -135,9 +136,10 @@ def select_sweep(a):
         torch.cuda.empty_cache()
 
 
-def time_graph_replays(torch, step, stream, steps):
-    """The same step captured once in a HIP graph and replayed `steps` times (after the timed eager
-    steps, outside their region): the per-step time without host launch overhead."""
+def capture_step_graph(torch, step, stream):
+    """The step captured once in a HIP graph (the vision mass forks onto a second stream inside
+    the capture and joins before the selection), after one pass on a side stream and followed
+    by one replay, both outside any timed region."""
     side = torch.cuda.Stream()
     side.wait_stream(stream)
     with torch.cuda.stream(side):
@@ -149,14 +151,7 @@ def time_graph_replays(torch, step, stream, steps):
         step(None)
     g.replay()
     torch.cuda.synchronize()
-    e0 = torch.cuda.Event(enable_timing=True)
-    e1 = torch.cuda.Event(enable_timing=True)
-    e0.record(stream)
-    for _ in range(steps):
-        g.replay()
-    e1.record(stream)
-    torch.cuda.synchronize()
-    return e0.elapsed_time(e1) / steps
+    return g
 
 
 MIN_PIXELS = 256 * 28 * 28    # APC's dynamic budget (reading R4): the resize keeps at least this area
@@ -384,14 +379,23 @@ def main():
     for _ in range(a.warmup):
         step(None)
     torch.cuda.synchronize()
-    t_start = torch.cuda.Event(enable_timing=True)
-    t_end = torch.cuda.Event(enable_timing=True)
-    t_start.record(stream)
-    for i in range(a.steps):
-        step(None)
-    t_end.record(stream)
-    torch.cuda.synchronize()
-    ms_per_step = t_start.elapsed_time(t_end) / a.steps
+    graph = capture_step_graph(torch, step, stream) if a.graph else None
+
+    def timed_steps(run):
+        t0 = torch.cuda.Event(enable_timing=True)
+        t1 = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        t0.record(stream)
+        for _ in range(a.steps):
+            run()
+        t1.record(stream)
+        torch.cuda.synchronize()
+        return t0.elapsed_time(t1) / a.steps
+
+    # the timed region: K steps, each a replay of the captured step (or, with --no-graph, the
+    # step launched kernel by kernel); then the same K steps launched kernel by kernel
+    ms_per_step = timed_steps(graph.replay if graph is not None else lambda: step(None))
+    eager_ms = timed_steps(lambda: step(None))
     # per-part times from the same number of steps run serially on one stream (after the timed
     # region: the side-by-side parts would otherwise time each other's share of the GPU)
     step_events = [new_events() for _ in range(a.steps)]
@@ -408,7 +412,6 @@ def main():
         for n in names:
             per[n] += ev[n][0].elapsed_time(ev[n][1])
     per = {n: v / a.steps for n, v in per.items()}
-    graph_ms = time_graph_replays(torch, step, stream, a.steps) if a.graph else None
     nxt = None
     if a.config == 3:
         nxt = measure_next(pace, ex["pq"], ex["pk"], ex["pv"], ex["p_cu"], ex["S"], ex["p_vis"], ex["p_cuv"],
@@ -450,11 +453,14 @@ def main():
         "roofline": {"kernel": roof_label, "bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
                      "traffic": measured_traffic() if a.config == 3 else None},
-        "schedule": "vision mass on a second stream beside the prefill; breakdown_ms and step_roofline "
-                    "from the same steps run serially on one stream",
+        "schedule": ("each timed step replays the step captured once in a HIP graph" if graph is not None
+                     else "each timed step launched kernel by kernel") +
+                    " (vision mass on a second stream beside the prefill); eager_ms_per_step: the same "
+                    "steps launched kernel by kernel; breakdown_ms and step_roofline from the same steps "
+                    "run serially on one stream",
+        "eager_ms_per_step": round(eager_ms, 4),
         "serial_ms_per_step": round(serial_ms, 4),
         "breakdown_ms": {n: round(v, 4) for n, v in per.items()},
-        "graph_ms_per_step": None if graph_ms is None else round(graph_ms, 4),
         "select": {
             "tokens_per_s": round(ex["Nv"] / (sel_ms * 1e-3), 1) if sel_ms > 0 else None,
             "gbs": round(work["select"][1] / (sel_ms * 1e-3) / 1e9, 1) if sel_ms > 0 else None,
