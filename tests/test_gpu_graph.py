@@ -3,7 +3,8 @@ capturing stream): every replay must reproduce the eager results bit for bit.  T
 fixed reduction orders and no float atomics, and with caller-provided workspaces the library
 neither allocates nor records memset or copy nodes, so a replay repeats the same computation.  The
 graph is replayed three times, with the program's own eager work and synchronisations between the
-replays, and every replay is checked."""
+replays, and every replay is checked.  The forked form runs the vision mass on a second stream
+beside the prefill inside the capture, as the benchmark's step does."""
 import numpy as np
 import pytest
 
@@ -13,18 +14,27 @@ from tests.gpu_util import dev_bf16, dev_i32, dev_u8, say
 pytestmark = pytest.mark.gpu
 
 
-def _path(pace, inp, out):
-    """One pass of the whole path into preallocated outputs."""
+def _path(pace, inp, out, side=None):
+    """One pass of the whole path into preallocated outputs; with `side`, the vision mass runs on
+    that stream (forked after the full-attention forward, joined before the selection)."""
+    import torch
     pace.apc_density(inp["img"], 14, 0.10, 0.6, 1.5, d_out=out["d"], rho_out=out["rho"], workspace=inp["ws_apc"])
     pace.apc_downsample(inp["img"], 224, 224, dst=out["small"])
     pace.vit_attention(inp["q"], inp["k"], inp["v"], inp["cu_win"], inp["max_win"], o=out["o_win"],
                        lse=out["lse_win"], mass=out["mass_win"])
     pace.vit_attention(inp["q"], inp["k"], inp["v"], inp["cu_full"], inp["N"], o=out["o_full"],
                        lse=out["lse_full"], want_mass=False, workspace=inp["ws_vit"])
-    pace.vit_attention_mass(inp["q"], inp["k"], inp["cu_full"], inp["N"], out["lse_full"], mass=out["mass_vis"])
+    if side is not None:
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            pace.vit_attention_mass(inp["q"], inp["k"], inp["cu_full"], inp["N"], out["lse_full"], mass=out["mass_vis"])
+    else:
+        pace.vit_attention_mass(inp["q"], inp["k"], inp["cu_full"], inp["N"], out["lse_full"], mass=out["mass_vis"])
     pace.prefill_attention_with_mass(inp["pq"], inp["pk"], inp["pv"], inp["p_cu"], inp["S"], inp["p_vis"],
                                      inp["p_cuv"], inp["nv"], inp["nv"], inp["p_mqs"], inp["p_mql"], inp["T"],
                                      o=out["o_pre"], lse=out["lse_pre"], mass=out["mass_llm"])
+    if side is not None:
+        torch.cuda.current_stream().wait_stream(side)
     pace.ddae_select(out["mass_vis"], 4, inp["perm"], out["mass_llm"], [inp["nv"]], [inp["K"]],
                      mode=inp["mode"], tau=inp["tau"], hidden=inp["hidden"], idx_out=out["idx"],
                      score_out=out["scores"], fuse_out=out["fuse"], out=out["kept"], workspace=inp["ws_sel"])
@@ -57,7 +67,8 @@ def _bitwise_equal(torch, a, b):
     return bool(torch.equal(a, b))
 
 
-def test_graph_replays_match_eager():
+@pytest.mark.parametrize("forked", [False, True], ids=["one_stream", "mass_forked"])
+def test_graph_replays_match_eager(forked):
     from paper_2608_27206_amd import pace
     import torch
     dev = torch.device("cuda")
@@ -79,7 +90,8 @@ def test_graph_replays_match_eager():
                                 dtype=torch.uint8, device=dev)
     inp["ws_sel"] = torch.empty(lib.pace_ddae_select_workspace_size(nv, 1), dtype=torch.uint8, device=dev)
 
-    say(f"graph test: {H}x{W} image, {N} patches, {nv} visual tokens, keep {inp['K']}")
+    say(f"graph test ({'mass forked' if forked else 'one stream'}): {H}x{W} image, {N} patches, "
+        f"{nv} visual tokens, keep {inp['K']}")
     eager = _outputs(torch, inp)
     _path(pace, inp, eager)
     torch.cuda.synchronize()
@@ -87,13 +99,14 @@ def test_graph_replays_match_eager():
     cap = _outputs(torch, inp)
     side = torch.cuda.Stream()
     side.wait_stream(torch.cuda.current_stream())
+    fork = torch.cuda.Stream() if forked else None
     with torch.cuda.stream(side):
-        _path(pace, inp, cap)            # a warm-up pass on a side stream before capture
+        _path(pace, inp, cap, fork)      # a warm-up pass on a side stream before capture
     torch.cuda.current_stream().wait_stream(side)
     torch.cuda.synchronize()
     g = torch.cuda.CUDAGraph()
     with torch.cuda.graph(g):
-        _path(pace, inp, cap)
+        _path(pace, inp, cap, fork)
     torch.cuda.synchronize()
     say("captured")
 
