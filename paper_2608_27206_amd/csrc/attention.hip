@@ -3,7 +3,8 @@
 // block) and the LLM's causal grouped-query prefill attention (S_llm from the text
 // query rows).  No attention matrix is ever stored.
 //
-// Three kernels, all on bf16 MFMA (v_mfma_f32_32x32x16_bf16, fp32 accumulation):
+// The kernels (MFMA 32x32x16, bf16 inputs except the fp16 PV product of attn_fwd_rot, fp32
+// accumulation):
 //
 //  attn_fwd   query-stationary.  A workgroup = 4 waves x 32 query rows of one
 //             (segment, head).  K and V tiles of 64 keys are staged through LDS by
@@ -14,18 +15,27 @@
 //             straight from registers (no LDS round trip); V^T comes from transposing
 //             LDS reads of the row-major V tile.  For head dim 80 the PV product is
 //             padded to 96 rows.  Writes O (bf16) and the natural-log LSE (fp32).
-//             Causal segments, short segments and head dim 128.
+//             Causal segments (the prefill), short segments and head dim 128.
 //
 //  attn_fwd_rot  the same computation for long segments at head dim 80, with 12 waves
 //             per workgroup in three groups that rotate through three phases (see the
-//             kernel), so that VALU and MFMA work of different waves overlap.
+//             kernel), so that VALU and MFMA work of different waves overlap; its PV
+//             product runs in fp16 on V^T tiles that attn_v_amax + attn_vt_prep write once
+//             per call (scaled per segment and KV head into fp16's range, a row of ones
+//             for the row sums).
+//
+//  attn_window  segments of at most 64 tokens (the 8x8-patch windows): O, LSE and the
+//             per-key mass in one pass, since a window's row max and sum are final after
+//             its single key tile.
 //
 //  attn_mass  key-stationary.  A workgroup = 4 waves x 64 keys of one (segment,
 //             head); K stays in registers, query tiles of 64 rows stream through LDS
 //             (three buffers, up to three workgroups per CU).  P = exp2(S * scale * log2 e -
 //             LSE * log2 e) is the exact normalised probability; each lane accumulates
 //             column sums for its 16 keys in fp32, and one butterfly over the half-wave
-//             finishes the sum.  Writes mass[h, key] once (no atomics, deterministic).
+//             finishes the sum.  Writes mass[h, key] once (no atomics, deterministic).  At
+//             head dim 80 without a mask it is pipelined inside each wave, one 32 x 32
+//             block at a time.
 //
 // Operand layouts of v_mfma_f32_32x32x16_bf16 (wave64, lane l, g = l / 32):
 //   A (32 x 16): lane l holds A[l % 32][8g .. 8g+7]
