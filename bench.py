@@ -268,6 +268,17 @@ def build_workload_step(a, torch, np, pace, wl, dev):
             for im, sm in zip(imgs, smalls):
                 pace.apc_downsample(im, sm.shape[0], sm.shape[1], dst=sm)
 
+        # one image's density then its resize: the images are independent, so with several of them
+        # the overlapped step runs these chains side by side on a few streams
+        def image_chain(i):
+            def run():
+                pace.apc_density(imgs[i], 14, 0.10, 0.6, 1.5, d_out=dps[i], rho_out=rhos[i], workspace=ws_apc[i])
+                pace.apc_downsample(imgs[i], smalls[i].shape[0], smalls[i].shape[1], dst=smalls[i])
+            return run
+
+        if len(imgs) > 1:
+            extra["image_chains"] = [image_chain(i) for i in range(len(imgs))]
+
         parts += [
             ("apc", apc, False, False),
             ("resize", resize, False, False),
@@ -343,6 +354,10 @@ def main():
     names = [p[0] for p in parts]
     stream = torch.cuda.current_stream()
     side = torch.cuda.Stream()   # default priority
+    # several images: their density + resize chains fork onto up to four streams (default
+    # priority) in the overlapped step and join before the window attention
+    chains = ex.get("image_chains")
+    img_streams = [torch.cuda.Stream() for _ in range(min(4, len(chains)))] if chains else []
 
     def new_events():
         return {n: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for n in names}
@@ -351,6 +366,16 @@ def main():
         cur = torch.cuda.current_stream()
         pending = False
         for name, fn, on_side, join in parts:
+            if overlap and chains and name in ("apc", "resize"):
+                if name == "apc":
+                    for sm in img_streams:
+                        sm.wait_stream(cur)
+                    for i, chain in enumerate(chains):
+                        with torch.cuda.stream(img_streams[i % len(img_streams)]):
+                            chain()
+                    for sm in img_streams:
+                        cur.wait_stream(sm)
+                continue
             if overlap and join and pending:
                 cur.wait_stream(side)
                 pending = False
@@ -455,7 +480,9 @@ def main():
                      "traffic": measured_traffic() if a.config == 3 else None},
         "schedule": ("each timed step replays the step captured once in a HIP graph" if graph is not None
                      else "each timed step launched kernel by kernel") +
-                    " (vision mass on a second stream beside the prefill); eager_ms_per_step: the same "
+                    " (vision mass on a second stream beside the prefill" +
+                    ("; the images' density and resize chains on %d streams side by side" % len(img_streams)
+                     if chains else "") + "); eager_ms_per_step: the same "
                     "steps launched kernel by kernel; breakdown_ms and step_roofline from the same steps "
                     "run serially on one stream",
         "eager_ms_per_step": round(eager_ms, 4),

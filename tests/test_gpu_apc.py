@@ -227,3 +227,52 @@ def test_pixel_rejects_bad_kind_and_patch():
         pace.apc_pixel_features(img, 4, 14)
     with pytest.raises(pace.PaceError, match="patch"):
         pace.apc_pixel_features(img, 0, 28 * 0 + 17)
+
+
+def test_images_on_parallel_streams_match_serial():
+    """Independent images' density and resize chains run side by side on four streams (as the
+    benchmark's multi-image step does) give bit-identical d, rho and resized pixels to the same
+    calls in series: the calls share no state beyond their own arguments and workspaces."""
+    from paper_2608_27206_amd import pace
+    import torch
+    w = wl.make_workload(4)
+    imgs = [dev_u8(im) for im in w.images]
+    say(f"{len(imgs)} images on 4 streams: " + ", ".join(f"{im.shape[1]}x{im.shape[0]}" for im in w.images))
+    lib = pace.lib()
+
+    def buffers():
+        out = []
+        for im in w.images:
+            H, W = im.shape[:2]
+            out.append({"ws": torch.empty(lib.pace_apc_density_workspace_size(H, W, 14), dtype=torch.uint8, device="cuda"),
+                        "d": torch.empty((H // 14) * (W // 14), dtype=torch.float32, device="cuda"),
+                        "rho": torch.empty(4, dtype=torch.float32, device="cuda"),
+                        "small": torch.empty((H // 2, W // 2, 3), dtype=torch.uint8, device="cuda")})
+        return out
+
+    def chain(img, b):
+        pace.apc_density(img, 14, 0.10, 0.6, 1.5, d_out=b["d"], rho_out=b["rho"], workspace=b["ws"])
+        pace.apc_downsample(img, b["small"].shape[0], b["small"].shape[1], dst=b["small"])
+
+    serial = buffers()
+    for img, b in zip(imgs, serial):
+        chain(img, b)
+    torch.cuda.synchronize()
+    par = buffers()
+    cur = torch.cuda.current_stream()
+    streams = [torch.cuda.Stream() for _ in range(4)]
+    for rep in range(2):
+        for b in par:
+            for t in b.values():
+                t.fill_(3)
+        for s in streams:
+            s.wait_stream(cur)
+        for i, (img, b) in enumerate(zip(imgs, par)):
+            with torch.cuda.stream(streams[i % 4]):
+                chain(img, b)
+        for s in streams:
+            cur.wait_stream(s)
+        torch.cuda.synchronize()
+        for i, (a, b) in enumerate(zip(serial, par)):
+            for k in ("d", "rho", "small"):
+                assert torch.equal(a[k], b[k]), f"pass {rep}, image {i}: {k} differs from the serial calls"
