@@ -135,8 +135,8 @@ __device__ __forceinline__ unsigned lds_u32(const void* p) {
 }
 __device__ __forceinline__ void dma16(i32x4 r, unsigned lds, unsigned voff) {
   const unsigned m0 = __builtin_amdgcn_readfirstlane(lds);
-  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
-               :: "s"(m0), "v"(voff), "s"(r) : "memory", "m0");
+  asm volatile("s_nop 0\n\tbuffer_load_dwordx4 %0, %1, 0 offen lds"
+               :: "v"(voff), "s"(r), "{m0}"(m0) : "memory");
 }
 __device__ __forceinline__ void wait_vmem() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 // The same resource moved `bytes` forward (base up, size down by the same amount): an offset v
@@ -153,8 +153,8 @@ __device__ __forceinline__ i32x4 rsrc_advance(i32x4 r, unsigned bytes) {
 // As dma16 with 4 bytes per lane (lds + 4 * lane).
 __device__ __forceinline__ void dma4(i32x4 r, unsigned lds, unsigned voff) {
   const unsigned m0 = __builtin_amdgcn_readfirstlane(lds);
-  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dword %1, %2, 0 offen lds"
-               :: "s"(m0), "v"(voff), "s"(r) : "memory", "m0");
+  asm volatile("s_nop 0\n\tbuffer_load_dword %0, %1, 0 offen lds"
+               :: "v"(voff), "s"(r), "{m0}"(m0) : "memory");
 }
 // Waits until at most n (wave-uniform, <= 7) of this wave's vector memory operations are
 // outstanding: the older ones, issued first, have completed.
