@@ -644,6 +644,8 @@ struct ResizeParams {
   uint8_t* dst;
   int H, W, oH, oW;
   int ty, tx;             // output rows / columns per workgroup
+  float rx, ry;           // W / oW and H / oH (register path: per-axis constants set on the host)
+  float invdx, invdy;     // 1 / (2 max(W, oW)) and 1 / (2 max(H, oH))
   int ntx, nty;           // tap slots per output column / row (upper bound of the tap count)
   int rows_cap;           // input rows staged per workgroup
   int cols_cap;           // input columns staged per workgroup
@@ -694,13 +696,22 @@ __device__ __forceinline__ int make_taps(int o, int n, int m, int slots, float* 
 // of the wave must call it together (`valid` false for rows of 16 with no coordinate); the
 // distance numerator is formed in 32 bits when 2 n m fits, which makes the same float.
 constexpr int kRegTaps = 16;
-__device__ __forceinline__ void make_taps_row16(int o, bool valid, int n, int m, int slots, float* w_out,
-                                                int* lo_out, int* count_out) {
+// keys_cubic without branches (both pieces evaluated, then selected): the same values
+__device__ __forceinline__ float keys_cubic_sel(float x) {
+  x = fabsf(x);
+  const float a = (1.5f * x - 2.5f) * x * x + 1.f;
+  const float b = ((-0.5f * x + 2.5f) * x - 4.f) * x + 2.f;
+  return x <= 1.f ? a : (x < 2.f ? b : 0.f);
+}
+// ratio = n / m and inv_den = 1 / (2 max(n, m)) come from the host.  The first candidate lo may
+// sit one sample off the one make_taps finds (the centre rounds differently), but the 16
+// candidates still cover the support, whose weights come from the same exact numerators.
+__device__ __forceinline__ void make_taps_row16(int o, bool valid, int n, int m, int slots, float ratio,
+                                                float inv_den, float* w_out, int* lo_out, int* count_out) {
   const int lane = threadIdx.x & 63, j = lane & 15;
-  const float centre = (static_cast<float>(o) + 0.5f) * static_cast<float>(n) / static_cast<float>(m);
-  const float support = 2.f * fmaxf(1.f, static_cast<float>(n) / static_cast<float>(m));
+  const float centre = (static_cast<float>(o) + 0.5f) * ratio;
+  const float support = 2.f * fmaxf(1.f, ratio);
   const int lo = max(static_cast<int>(floorf(centre - support - 0.5f)) - 1, 0);
-  const float inv_den = 1.f / static_cast<float>(2ll * (n > m ? n : m));
   float wt = 0.f;
   if (valid && j < slots && lo + j < n) {
     float num;
@@ -708,7 +719,7 @@ __device__ __forceinline__ void make_taps_row16(int o, bool valid, int n, int m,
       num = static_cast<float>((2 * (lo + j) + 1) * m - (2 * o + 1) * n);
     else
       num = static_cast<float>((2ll * (lo + j) + 1) * m - (2ll * o + 1) * n);
-    wt = keys_cubic(num * inv_den);
+    wt = keys_cubic_sel(num * inv_den);
   }
   float sum = wt;
   sum += dpp_f32<kDppQuadXor1>(sum);
@@ -755,10 +766,12 @@ __global__ __launch_bounds__(kRsThreads) void apc_resize_reg(const ResizeParams 
   for (int b = 0; b < (p.tx + p.ty) * 16; b += kRsThreads) {
     const int item = (b + tid) >> 4;
     if (item < p.tx)
-      make_taps_row16(ox0 + item, item < ncols, p.W, p.oW, p.ntx, wx + item * p.ntx, &lox[item], &cnx[item]);
+      make_taps_row16(ox0 + item, item < ncols, p.W, p.oW, p.ntx, p.rx, p.invdx, wx + item * p.ntx, &lox[item],
+                      &cnx[item]);
     else {
       const int r = min(item - p.tx, p.ty - 1);
-      make_taps_row16(oy0 + r, item - p.tx < nrows, p.H, p.oH, p.nty, wy + r * p.nty, &loy[r], &cny[r]);
+      make_taps_row16(oy0 + r, item - p.tx < nrows, p.H, p.oH, p.nty, p.ry, p.invdy, wy + r * p.nty, &loy[r],
+                      &cny[r]);
     }
   }
   __syncthreads();
@@ -1170,6 +1183,10 @@ pace_status_t pace_apc_downsample(const uint8_t* src, int H, int W, uint8_t* dst
   ResizeParams p{};
   p.src = src; p.dst = dst;
   p.H = H; p.W = W; p.oH = oH; p.oW = oW;
+  p.rx = static_cast<float>(W) / static_cast<float>(oW);
+  p.ry = static_cast<float>(H) / static_cast<float>(oH);
+  p.invdx = 1.f / static_cast<float>(2ll * (W > oW ? W : oW));
+  p.invdy = 1.f / static_cast<float>(2ll * (H > oH ? H : oH));
   // taps of one output pixel span at most 4*s + 4 inputs (the support plus one zero-weight
   // guard tap on each side)
   p.ntx = static_cast<int>(ceil(4.0 * (sx > 1 ? sx : 1))) + 4;
