@@ -1,14 +1,15 @@
 // APC (Section 3.2, "Condense"): per-patch information density of a uint8 image and
 // the bicubic resize by sqrt(r) per side (Appendix implementation details).
 //
-// Density, five launches (all HBM/L2-bound, fixed reduction orders -> deterministic):
+// Density, four launches (all HBM/L2-bound, fixed reduction orders -> deterministic):
 //   apc_patch_pass<0>  per patch-strip tile: ||f_i|| -> 1/||f_i|| (from exact integer sums of
 //                      the bytes and their squares), and the tile's partial sum of
 //                      T_i = f_i/||f_i|| over its patches (one 588-vector per tile)
 //   apc_reduce_c       sum of the tile partials per component -> sum_i T_i
-//   apc_finalize_c     c = mean T_i, phi = ||c||^2 (equal to Eq. 1's mean pairwise cosine),
-//                      rho_g = 1 - phi (Eq. 2), c_hat = c/||c||
-//   apc_patch_pass<1>  d_i = ||T_i - c_hat|| (the image is re-read, mostly from L2/MALL)
+//   apc_patch_pass<1>  c = mean T_i, phi = ||c||^2 (equal to Eq. 1's mean pairwise cosine),
+//                      rho_g = 1 - phi (Eq. 2) and c_hat = c/||c||, recomputed by every
+//                      workgroup from the sums; then d_i = ||T_i - c_hat|| (the image is
+//                      re-read, mostly from L2/MALL)
 //   apc_tail           radix select of the n_tail-th largest d, tail mean, rho_d, rho
 //                      (up to 49,152 distances held in registers, more re-read from memory)
 //
@@ -130,12 +131,55 @@ __global__ __launch_bounds__(kApcThreads) void apc_patch_pass(const DensityParam
   float* inv = reinterpret_cast<float*>(px + p.P * p.row_dwords);  // [64]
   float* chat = inv + kPatchesPerTile;                            // [D] (pass 1)
   __shared__ int shift[kMaxPatch];
+  __shared__ float red[kApcThreads / 64];
   const int tile = blockIdx.x;
+  // pass 1: the component sums of sum_i T_i (D <= 3 * 16^2, three per thread), requested
+  // before the tile so that their loads fly with the tile's
+  constexpr int kCPer = (3 * kMaxPatch * kMaxPatch + kApcThreads - 1) / kApcThreads;
+  float cs[kCPer];
+  if (PASS == 1) {
+#pragma unroll
+    for (int k = 0; k < kCPer; ++k) {
+      const int e = static_cast<int>(threadIdx.x) + k * kApcThreads;
+      cs[k] = e < p.D ? p.csum[e] : 0.f;
+    }
+  }
   int py, px0;
   const int np = stage_tile(p, tile, px, shift, &py, &px0);
-  if (PASS == 1)
-    for (int e = threadIdx.x; e < p.D; e += kApcThreads) chat[e] = p.chat[e];
+  if (PASS == 1) {
+    // c = mean_i T_i and phi = ||c||^2 (equal to Eq. 1's mean pairwise cosine), summed by
+    // every workgroup in the same fixed order, so that all get the same c_hat
+    const float invN = 1.0f / static_cast<float>(p.N);
+    float ss = 0.f;
+#pragma unroll
+    for (int k = 0; k < kCPer; ++k) {
+      const int e = static_cast<int>(threadIdx.x) + k * kApcThreads;
+      const float c = cs[k] * invN;
+      if (e < p.D) chat[e] = c;
+      ss += c * c;
+    }
+    ss = wave_sum(ss);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
+  }
   __syncthreads();
+  if (PASS == 1) {
+    float ss = red[0];
+#pragma unroll
+    for (int i = 1; i < kApcThreads / 64; ++i) ss += red[i];
+    const float nc = sqrtf(ss);
+    const float ic = (nc > 1e-5f) ? 1.0f / nc : 0.f;   // c_hat = 0 when ||c|| is numerically zero
+#pragma unroll
+    for (int k = 0; k < kCPer; ++k) {
+      const int e = static_cast<int>(threadIdx.x) + k * kApcThreads;
+      if (e < p.D) chat[e] *= ic;
+    }
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+      p.stats[0] = ss;          // phi
+      p.stats[1] = 1.0f - ss;   // rho_g (Eq. 2)
+      p.stats[2] = nc;
+    }
+    __syncthreads();
+  }
   const uint8_t* pxb = reinterpret_cast<const uint8_t*>(px);
   const int rb = p.row_dwords * 4;
   const int pb = 3 * p.P;                  // bytes of one patch row
@@ -207,7 +251,8 @@ __global__ __launch_bounds__(kApcThreads) void apc_patch_pass(const DensityParam
 //                     when rows are 16-byte vectors) of x_i / ||x_i|| over the block's rows
 //                     (L2-resident) -> the block partial
 //   apc_feat_pass<1>  one wave per row: d_i = ||x_i / ||x_i|| - c_hat||
-// The partials then go through apc_reduce_c, apc_finalize_c and apc_tail as for images.
+// The partials then go through apc_reduce_c, apc_finalize_c (c, phi and c_hat once, as pass 1
+// here has a small workgroup per row) and apc_tail.
 constexpr int kFeatRows = 64;
 
 __device__ __forceinline__ float bf16_lo(uint32_t u) { return __uint_as_float(u << 16); }
@@ -528,7 +573,12 @@ __global__ __launch_bounds__(1024) void apc_tail(const DensityParams p) {
   int need_eq;
   float s = 0.f;
   if (p.N <= 1024 * kTailR) {
-    for (int i = tid; i < kTailBins; i += 1024) hist[i] = 0u;
+    // Slots past N read as +0 (range-checked loads), the smallest possible distance.  They
+    // are counted into bin 0 at once, not one contended atomic each, and take part in every
+    // later step as ordinary zeros: as n_tail <= N, the top n_tail values, T and the sum are
+    // those of the N distances (a tie at 0 adds 0), and no step needs a per-slot range test.
+    const uint32_t pad = static_cast<uint32_t>(1024 * kTailR - p.N);
+    for (int i = tid; i < kTailBins; i += 1024) hist[i] = i == 0 ? pad : 0u;
     rhist[tid] = 0u;
     if (tid < 8) misc[tid] = 0u;
     uint32_t key[kTailR];
@@ -537,10 +587,12 @@ __global__ __launch_bounds__(1024) void apc_tail(const DensityParams p) {
     for (int j = 0; j < kTailR; ++j)
       key[j] = __float_as_uint(rload_f32(rd, static_cast<unsigned>(j * 1024 + tid) * 4u));
     __syncthreads();
+    const int jfull = p.N >> 10;
+    const bool rem_live = tid < (p.N & 1023);
 #pragma unroll
     for (int j = 0; j < kTailR; ++j) {
       const int bin = static_cast<int>(fminf(__uint_as_float(key[j]) * 2048.f, static_cast<float>(kTailBins - 1)));
-      if (j * 1024 + tid < p.N) atomicAdd(&hist[bin], 1u);
+      if (j < jfull || (j == jfull && rem_live)) atomicAdd(&hist[bin], 1u);
     }
     __syncthreads();
     // thread t covers bins 4095 - 4t down to 4092 - 4t (descending)
@@ -564,17 +616,36 @@ __global__ __launch_bounds__(1024) void apc_tail(const DensityParams p) {
     __syncthreads();
     const int bstar = static_cast<int>(misc[0]);
     const int need = static_cast<int>(misc[1]);   // 1 <= need <= count of bin b*
+    // d * 2048 is exact, so bin b* holds exactly the keys in [b*/2048, (b*+1)/2048), the
+    // last bin everything from 4095/2048 up
+    const uint32_t lo = __float_as_uint(static_cast<float>(bstar) * (1.f / 2048.f));
+    const uint32_t span = (bstar == kTailBins - 1) ? 0xffffffffu - lo
+                          : __float_as_uint(static_cast<float>(bstar + 1) * (1.f / 2048.f)) - lo;
 #pragma unroll
     for (int j = 0; j < kTailR; ++j) {
-      const int bin = static_cast<int>(fminf(__uint_as_float(key[j]) * 2048.f, static_cast<float>(kTailBins - 1)));
-      if (j * 1024 + tid < p.N && bin == bstar) {
+      if (key[j] - lo < span) {
         const uint32_t slot = atomicAdd(&misc[2], 1u);
         if (slot < static_cast<uint32_t>(kTailCand)) { cand_key[slot] = key[j]; cand_idx[slot] = j * 1024 + tid; }
       }
     }
     __syncthreads();
     const uint32_t ncand = misc[2];
-    if (ncand <= static_cast<uint32_t>(kTailCand)) {
+    if (ncand <= 64u) {
+      // one wave ranks up to 64 candidates, one per lane, the others' keys read by lane index
+      if (w == 0) {
+        const bool mine = lane < static_cast<int>(ncand);
+        const uint32_t kt = mine ? cand_key[lane] : 0u;
+        const int it = mine ? cand_idx[lane] : 0;
+        int rank = 0, greater = 0;
+        for (uint32_t u = 0; u < ncand; ++u) {
+          const uint32_t ku = __builtin_amdgcn_readlane(kt, u);
+          const int iu = __builtin_amdgcn_readlane(it, u);
+          rank += (ku > kt || (ku == kt && iu < it)) ? 1 : 0;
+          greater += ku > kt ? 1 : 0;
+        }
+        if (mine && rank == need - 1) { misc[3] = kt; misc[4] = static_cast<uint32_t>(need - greater); }
+      }
+    } else if (ncand <= static_cast<uint32_t>(kTailCand)) {
       if (tid < static_cast<int>(ncand)) {
         const uint32_t kt = cand_key[tid];
         const int it = cand_idx[tid];
@@ -589,15 +660,12 @@ __global__ __launch_bounds__(1024) void apc_tail(const DensityParams p) {
       }
     } else {
       // many equal distances in one bin: radix select over the candidates' keys (+1, so
-      // that every candidate ranks above the non-candidates' 0)
+      // that every candidate ranks above the others' 0)
       uint32_t ck[kTailR];
 #pragma unroll
-      for (int j = 0; j < kTailR; ++j) {
-        const int bin = static_cast<int>(fminf(__uint_as_float(key[j]) * 2048.f, static_cast<float>(kTailBins - 1)));
-        ck[j] = (j * 1024 + tid < p.N && bin == bstar) ? key[j] + 1u : 0u;
-      }
+      for (int j = 0; j < kTailR; ++j) ck[j] = (key[j] - lo < span) ? key[j] + 1u : 0u;
       int ne = 0;
-      const uint32_t T1 = radix_select_prezeroed<kTailR, true>(ck, p.N, need, rhist, &misc[5], &ne);
+      const uint32_t T1 = radix_select_prezeroed<kTailR, true>(ck, 1024 * kTailR, need, rhist, &misc[5], &ne);
       if (tid == 0) { misc[3] = T1 - 1u; misc[4] = static_cast<uint32_t>(ne); }
     }
     __syncthreads();
@@ -605,7 +673,7 @@ __global__ __launch_bounds__(1024) void apc_tail(const DensityParams p) {
     need_eq = static_cast<int>(misc[4]);
 #pragma unroll
     for (int j = 0; j < kTailR; ++j)
-      if (j * 1024 + tid < p.N && key[j] > T) s += __uint_as_float(key[j]);
+      if (key[j] > T) s += __uint_as_float(key[j]);
   } else {
     int need = 0;
     T = block_radix_select(p.N, p.n_tail, [&](int i) { return __float_as_uint(p.d[i]); }, rhist, &need);
@@ -960,7 +1028,6 @@ void size_density(Sizer& s, int H, int W, int P) {
   s.take<float>(N);                              // inv_norm
   s.take<float>(static_cast<size_t>(tiles) * D); // partials
   s.take<float>(D);                              // csum
-  s.take<float>(D);                              // chat
   s.take<float>(8);                              // stats
   s.take<float>(N);                              // d (when d_out is null)
 }
@@ -1032,7 +1099,6 @@ pace_status_t pace_apc_density(const uint8_t* img, int H, int W, int patch, doub
   p.inv_norm = c.take<float>(p.N);
   p.partial = c.take<float>(static_cast<size_t>(p.n_tiles) * p.D);
   p.csum = c.take<float>(p.D);
-  p.chat = c.take<float>(p.D);
   p.stats = c.take<float>(8);
   float* dws = c.take<float>(p.N);
   p.d = d_out ? d_out : dws;
@@ -1043,8 +1109,6 @@ pace_status_t pace_apc_density(const uint8_t* img, int H, int W, int patch, doub
   if (st != PACE_OK) return st;
   hipLaunchKernelGGL(apc_reduce_c, dim3((p.D + 63) / 64), dim3(1024), 0, stream, p);
   if ((st = check_launch("apc_reduce_c")) != PACE_OK) return st;
-  hipLaunchKernelGGL(apc_finalize_c, dim3(1), dim3(1024), 0, stream, p);
-  if ((st = check_launch("apc_finalize_c")) != PACE_OK) return st;
   hipLaunchKernelGGL(apc_patch_pass<1>, dim3(p.n_tiles), dim3(kApcThreads), lds, stream, p);
   if ((st = check_launch("apc_patch_pass<1>")) != PACE_OK) return st;
   hipLaunchKernelGGL(apc_tail, dim3(1), dim3(1024), 0, stream, p);
