@@ -2,8 +2,8 @@
 // softmax(sigma / tau) fusion, top-K ranking and the gather of the kept rows.
 //
 // Two launches per call when every image has at most 16,384 tokens:
-//   ddae_token_maps      grid-wide, 64 tokens per workgroup, workgroups never straddle
-//                        two images: head sums (and 2x2 merge + permutation for S_vis) ->
+//   ddae_token_maps      grid-wide, one wave of 64 tokens (one per lane) per workgroup,
+//                        workgroups never straddle two images: head sums (and 2x2 merge + permutation for S_vis) ->
 //                        raw S_vis, S_llm per LLM visual token (HBM-bound read of the
 //                        masses), plus each workgroup's min, max and float64 sum and sum
 //                        of squares of both maps
@@ -74,83 +74,75 @@ struct MinOp { __device__ float operator()(float a, float b) const { return fmin
 struct MaxOp { __device__ float operator()(float a, float b) const { return fmaxf(a, b); } };
 struct AddOpD { __device__ double operator()(double a, double b) const { return a + b; } };
 
-constexpr int kMapTokens = 64;   // tokens per map workgroup
+constexpr int kMapTokens = 64;    // tokens per map workgroup: one wave, one token per lane
+constexpr int kMapHeadsL = 32;    // LLM heads whose loads are in flight together
+constexpr int kMapHeadsV = 16;    // vision heads likewise
 
-// Four lanes per token, each summing every fourth head; combined by shuffles in a fixed
-// order (deterministic).  Then the workgroup's partial statistics, reduced in a fixed order.
-__global__ __launch_bounds__(256) void ddae_token_maps(const SelectParams p) {
-  __shared__ float red_f[4][4];
-  __shared__ double red_d[4][4];
-  const int b = __builtin_amdgcn_readfirstlane(find_image(p.cu_mwg, p.B, blockIdx.x));
+// One token per lane: every load of a head reads that head's row over 64 consecutive tokens
+// (LLM masses) or their permuted 2x2 groups (vision masses), all heads' loads in flight
+// together.  Each sum over heads keeps four interleaved partial sums (head 4u + r into sum r,
+// u increasing), combined as (s0 + s1) + (s2 + s3).  Then the workgroup's partial
+// statistics (wave reductions in a fixed order).
+__global__ __launch_bounds__(kMapTokens) void ddae_token_maps(const SelectParams p) {
+  // XCD-contiguous logical order: the workgroups of neighbouring raster runs, which read the
+  // two halves of the same cache lines of window-ordered vision masses, share an L2
+  const int lb = remap_block_id(blockIdx.x, gridDim.x);
+  const int b = __builtin_amdgcn_readfirstlane(find_image(p.cu_mwg, p.B, lb));
   const int n0 = p.cu_nv[b];
   const int n = p.cu_nv[b + 1] - n0;
-  const int li = (blockIdx.x - p.cu_mwg[b]) * kMapTokens + (threadIdx.x >> 2);
-  const int part = threadIdx.x & 3;
+  const int li = (lb - p.cu_mwg[b]) * kMapTokens + static_cast<int>(threadIdx.x);
   const bool valid = li < n;
   const int ii = n0 + (valid ? li : 0);
-  // The LLM masses do not depend on the permutation: their loads go out first, then the
-  // permutation entry, then the vision masses it points at.
-  float lm[8];
-#pragma unroll
-  for (int u = 0; u < 8; ++u) {
-    const int h = part + 4 * u;
-    lm[u] = (valid && h < p.Hl) ? p.llm_mass[static_cast<long long>(h) * p.nv_total + ii] : 0.f;
-  }
-  float l = 0.f;
-  for (int h = part + 32; h < p.Hl; h += 4) l += valid ? p.llm_mass[static_cast<long long>(h) * p.nv_total + ii] : 0.f;
+  // the permutation entry first (the vision loads depend on it), then the LLM masses
   const int local = p.vis_perm ? p.vis_perm[ii] : (ii - n0);
+  float l4[4] = {0.f, 0.f, 0.f, 0.f};
+  for (int h0 = 0; h0 < p.Hl; h0 += kMapHeadsL) {
+    float lm[kMapHeadsL];
+    // heads past the last re-read the last one (no predicated loads); they are not added
+#pragma unroll
+    for (int u = 0; u < kMapHeadsL; ++u)
+      lm[u] = p.llm_mass[static_cast<long long>(min(h0 + u, p.Hl - 1)) * p.nv_total + ii];
+#pragma unroll
+    for (int u = 0; u < kMapHeadsL; ++u)
+      if (h0 + u < p.Hl) l4[u & 3] += lm[u];
+  }
   const long long patch0 = static_cast<long long>(n0 + local) * p.merge;
-  float v = 0.f;
-  if (valid) {
-    if (p.merge == 4) {
-#pragma unroll 4
-      for (int h = part; h < p.Hv; h += 4) {
-        const float4 m = *reinterpret_cast<const float4*>(p.vis_mass + h * p.vis_stride + patch0);
-        v += (m.x + m.y) + (m.z + m.w);
-      }
-    } else {
-      for (int h = part; h < p.Hv; h += 4) {
-        const float* row = p.vis_mass + h * p.vis_stride + patch0;
-        for (int t = 0; t < p.merge; ++t) v += row[t];
-      }
+  float v4[4] = {0.f, 0.f, 0.f, 0.f};
+  if (p.merge == 4) {
+    for (int h0 = 0; h0 < p.Hv; h0 += kMapHeadsV) {
+      float4 m[kMapHeadsV];
+#pragma unroll
+      for (int u = 0; u < kMapHeadsV; ++u)
+        m[u] = *reinterpret_cast<const float4*>(p.vis_mass + min(h0 + u, p.Hv - 1) * p.vis_stride + patch0);
+#pragma unroll
+      for (int u = 0; u < kMapHeadsV; ++u)
+        if (h0 + u < p.Hv) v4[u & 3] += (m[u].x + m[u].y) + (m[u].z + m[u].w);
+    }
+  } else {
+    for (int h = 0; h < p.Hv; ++h) {
+      const float* row = p.vis_mass + h * p.vis_stride + patch0;
+      for (int t = 0; t < p.merge; ++t) v4[h & 3] += row[t];
     }
   }
-#pragma unroll
-  for (int u = 0; u < 8; ++u) l += lm[u];
-  v += __shfl_xor(v, 1, 64);
-  l += __shfl_xor(l, 1, 64);
-  v += __shfl_xor(v, 2, 64);
-  l += __shfl_xor(l, 2, 64);
-  if (valid && part == 0) {
+  const float v = (v4[0] + v4[1]) + (v4[2] + v4[3]);
+  const float l = (l4[0] + l4[1]) + (l4[2] + l4[3]);
+  if (valid) {
     p.vraw[ii] = v;
     p.lraw[ii] = l;
   }
   if (p.part == nullptr) return;
-  // one lane per token contributes (the four lanes of a token hold the same sums)
-  const bool own = valid && part == 0;
-  const float vmin = wave_reduce_dpp(own ? v : INFINITY, MinOp{});
-  const float vmax = wave_reduce_dpp(own ? v : -INFINITY, MaxOp{});
-  const float lmin = wave_reduce_dpp(own ? l : INFINITY, MinOp{});
-  const float lmax = wave_reduce_dpp(own ? l : -INFINITY, MaxOp{});
-  const double dv = own ? static_cast<double>(v) : 0.0, dl = own ? static_cast<double>(l) : 0.0;
+  const float vmin = wave_reduce_dpp(valid ? v : INFINITY, MinOp{});
+  const float vmax = wave_reduce_dpp(valid ? v : -INFINITY, MaxOp{});
+  const float lmin = wave_reduce_dpp(valid ? l : INFINITY, MinOp{});
+  const float lmax = wave_reduce_dpp(valid ? l : -INFINITY, MaxOp{});
+  const double dv = valid ? static_cast<double>(v) : 0.0, dl = valid ? static_cast<double>(l) : 0.0;
   const double sv = wave_reduce_dpp(dv, AddOpD{}), sv2 = wave_reduce_dpp(dv * dv, AddOpD{});
   const double sl = wave_reduce_dpp(dl, AddOpD{}), sl2 = wave_reduce_dpp(dl * dl, AddOpD{});
-  const int w = threadIdx.x >> 6;
-  if ((threadIdx.x & 63) == 0) {
-    red_f[w][0] = vmin; red_f[w][1] = vmax; red_f[w][2] = lmin; red_f[w][3] = lmax;
-    red_d[w][0] = sv; red_d[w][1] = sv2; red_d[w][2] = sl; red_d[w][3] = sl2;
-  }
-  __syncthreads();
   if (threadIdx.x == 0) {
     MapPartial r;
-    r.vmin = red_f[0][0]; r.vmax = red_f[0][1]; r.lmin = red_f[0][2]; r.lmax = red_f[0][3];
-    r.sv = red_d[0][0]; r.sv2 = red_d[0][1]; r.sl = red_d[0][2]; r.sl2 = red_d[0][3];
-    for (int q = 1; q < 4; ++q) {
-      r.vmin = fminf(r.vmin, red_f[q][0]); r.vmax = fmaxf(r.vmax, red_f[q][1]);
-      r.lmin = fminf(r.lmin, red_f[q][2]); r.lmax = fmaxf(r.lmax, red_f[q][3]);
-      r.sv += red_d[q][0]; r.sv2 += red_d[q][1]; r.sl += red_d[q][2]; r.sl2 += red_d[q][3];
-    }
-    p.part[blockIdx.x] = r;
+    r.vmin = vmin; r.vmax = vmax; r.lmin = lmin; r.lmax = lmax;
+    r.sv = sv; r.sv2 = sv2; r.sl = sl; r.sl2 = sl2;
+    p.part[lb] = r;
   }
 }
 
@@ -596,7 +588,22 @@ __global__ __launch_bounds__(kSelThreads) void ddae_select_gather(const SelectPa
       }
       __syncthreads();
       const uint32_t ncand = misc[2];
-      if (ncand <= static_cast<uint32_t>(kCandMax)) {
+      if (ncand <= 64u) {
+        // one wave ranks up to 64 candidates, one per lane, the others' keys read by lane
+        // index; rank = candidates ahead in (key descending, index ascending) order
+        if (w == 0) {
+          const bool mine = lane < static_cast<int>(ncand);
+          const uint32_t kt = mine ? cand_key[lane] : 0u;
+          const int it = mine ? cand_idx[lane] : 0;
+          int rank = 0;
+          for (uint32_t u = 0; u < ncand; ++u) {
+            const uint32_t ku = __builtin_amdgcn_readlane(kt, u);
+            const int iu = __builtin_amdgcn_readlane(it, u);
+            rank += (ku > kt || (ku == kt && iu < it)) ? 1 : 0;
+          }
+          if (mine && rank == need - 1) { misc[3] = kt; misc[4] = static_cast<uint32_t>(it); }
+        }
+      } else if (ncand <= static_cast<uint32_t>(kCandMax)) {
         // rank = candidates ahead in (key descending, index ascending) order
         if (tid < static_cast<int>(ncand)) {
           const uint32_t kt = cand_key[tid];
@@ -705,7 +712,7 @@ pace_status_t run_select(SelectParams& p, const void* hidden, size_t row_bytes, 
   const bool fused = nmax <= kSelThreads * kSelR;
   if (!fused) p.part = nullptr;
   if (need_maps && p.nv_total > 0) {
-    hipLaunchKernelGGL(ddae_token_maps, dim3(p.cu_mwg[p.B]), dim3(256), 0, stream, p);
+    hipLaunchKernelGGL(ddae_token_maps, dim3(p.cu_mwg[p.B]), dim3(kMapTokens), 0, stream, p);
     pace_status_t st = check_launch("ddae_token_maps");
     if (st != PACE_OK) return st;
   }
