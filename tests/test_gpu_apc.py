@@ -80,6 +80,36 @@ def test_density_uniform_and_mirrored():
     assert abs(rho[2] - 13 / 15) < 1e-4
 
 
+@pytest.mark.parametrize("n_b", [60, 200, 270])
+def test_density_tail_ties_in_each_ranking_path(n_b):
+    """Exact ties at the tail threshold.  576 patches of two kinds (n_b of kind B, the rest A,
+    at seeded positions): the minority kind lies farther from the mean direction, and all its
+    patches have bitwise equal distances, so the n_tail = 58 largest are 58 of its n_b equal
+    values and the threshold bin holds all n_b of them.  60 candidates are ranked by one wave,
+    200 by the LDS loop and 270 by the radix select; 576 is not a multiple of 1024, so the
+    tail's zero padding slots are present too.  gamma = 100 keeps rho_d = d_top / 100 unclamped."""
+    from paper_2608_27206_amd import pace
+    import torch
+    rng = np.random.default_rng(40 + n_b)
+    a = rng.integers(0, 256, size=(14, 14, 3), dtype=np.uint8)
+    b = rng.integers(0, 256, size=(14, 14, 3), dtype=np.uint8)
+    kinds = np.zeros(24 * 24, bool)
+    kinds[rng.choice(24 * 24, n_b, replace=False)] = True
+    img = np.empty((24 * 14, 24 * 14, 3), np.uint8)
+    for i, is_b in enumerate(kinds):
+        r, c = divmod(i, 24)
+        img[14 * r:14 * r + 14, 14 * c:14 * c + 14] = b if is_b else a
+    say(f"apc density tail ties: {n_b} of 576 patches at the threshold")
+    rho, d = pace.apc_density(dev_u8(img), 14, 0.1, 0.6, 100.0)
+    torch.cuda.synchronize()
+    rho, d = host(rho), host(d)
+    ref = oapc.apc_density(img, 14, 0.1, gamma=100.0)
+    assert len(np.unique(d[kinds])) == 1 and d[kinds][0] > d[~kinds][0]
+    np.testing.assert_allclose(d, ref["d"], atol=1e-4)
+    np.testing.assert_allclose(rho[1] * 100.0, ref["d_top"], atol=1e-5)
+    np.testing.assert_allclose(rho, [ref["rho_g"], ref["rho_d"], ref["rho"], ref["phi"]], atol=1e-4)
+
+
 def _check_resize(img, oh, ow):
     from paper_2608_27206_amd import pace
     import torch
