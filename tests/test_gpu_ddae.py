@@ -27,7 +27,9 @@ def _topk_case(S32, K, hidden_bits):
 
 @pytest.mark.parametrize("n,K,levels", [(196, 20, None), (10549, 1055, None), (5000, 500, 3),
                                         (1000, 1, None), (1000, 999, None), (777, 77, 1),
-                                        (4096, 1024, 50),
+                                        # ~41 and ~82 equal scores per level: ties ranked by
+                                        # the one-wave path and by the LDS loop
+                                        (4096, 1000, 100), (4096, 1024, 50),
                                         # largest image held in registers, and past it (the
                                         # scores are then re-read from memory)
                                         (16384, 1639, None), (16385, 1700, 4), (40000, 4000, None)])
