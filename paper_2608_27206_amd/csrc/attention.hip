@@ -1059,8 +1059,46 @@ __global__ __launch_bounds__(kWinThreads) void attn_window(const FwdParams p, fl
       }
     }
 
+  // O = O^T / l in bf16 through LDS, once both waves are done with K and V, then stored row
+  // by row: a 16-byte chunk per lane, each row's D values contiguous.  (Stored straight from
+  // the accumulators, every store instruction wrote 8-byte pieces of 32 rows 2,560 bytes
+  // apart, which cost the write path about as much as the rest of the kernel.)
+  __syncthreads();
+  {
+    constexpr int OS = D + 8;       // LDS row stride of the staged O (elements, 16-byte rows)
+    constexpr int CPR = D / 8;      // 16-byte chunks per row
+    static_assert(kWinMax * OS * 2 <= kBN * (C::KS + C::VS) * 2, "staged O does not fit");
+    uint16_t* Ob = lds;
+#pragma unroll
+    for (int t2 = 0; t2 < C::NT; ++t2) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int dv = t2 * 32 + g * 4 + 8 * j;
+        if (dv < D) {
+          uint2 pk;
+          pk.x = pack_bf16x2(oacc[t2][4 * j + 0] * inv_l, oacc[t2][4 * j + 1] * inv_l);
+          pk.y = pack_bf16x2(oacc[t2][4 * j + 2] * inv_l, oacc[t2][4 * j + 3] * inv_l);
+          *reinterpret_cast<uint2*>(&Ob[qrow * OS + dv]) = pk;
+        }
+      }
+    }
+    __syncthreads();
+    // rows past the window end fall outside the resource (same extent as Q's): dropped
+    const auto ro = make_rsrc(p.o + static_cast<long long>(s0) * qstride + h * D, seg_bytes_q);
+    typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+#pragma unroll
+    for (int c = tid; c < kWinMax * CPR; c += kWinThreads) {
+      const int r = c / CPR, cc = c - (c / CPR) * CPR;
+      const u32x4 val = *reinterpret_cast<const u32x4*>(&Ob[r * OS + cc * 8]);
+      __builtin_amdgcn_raw_buffer_store_b128(val, ro, r < L ? static_cast<unsigned>(r * qstride + cc * 8) * 2u : kOutOfRange,
+                                            0, 0);
+    }
+  }
+  if (qrow < L && g == 0 && p.lse)
+    p.lse[static_cast<long long>(h) * p.Ntot + s0 + qrow] = (mx + __builtin_amdgcn_logf(l)) * kLn2;
+
   // exact P of this lane's row (zero for rows past the window) into LDS, 4 keys per store,
-  // once both waves are done with K and V
+  // once every thread has read its chunks of the staged O
   __syncthreads();
   const float rowf = (qrow < L) ? inv_l : 0.f;
 #pragma unroll
@@ -1071,25 +1109,6 @@ __global__ __launch_bounds__(kWinThreads) void attn_window(const FwdParams p, fl
                               pv[st][4 * j + 3] * rowf);
       *reinterpret_cast<float4*>(&Pb[qrow * kPbStride + st * 32 + 8 * j + 4 * g]) = v4;
     }
-
-  if (qrow < L) {
-    uint16_t* op = p.o + static_cast<long long>(s0 + qrow) * qstride + h * D;
-#pragma unroll
-    for (int t2 = 0; t2 < C::NT; ++t2) {
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int dv = t2 * 32 + g * 4 + 8 * j;
-        if (dv < D) {
-          uint2 pk;
-          pk.x = pack_bf16x2(oacc[t2][4 * j + 0] * inv_l, oacc[t2][4 * j + 1] * inv_l);
-          pk.y = pack_bf16x2(oacc[t2][4 * j + 2] * inv_l, oacc[t2][4 * j + 3] * inv_l);
-          *reinterpret_cast<uint2*>(op + dv) = pk;
-        }
-      }
-    }
-    if (g == 0 && p.lse)
-      p.lse[static_cast<long long>(h) * p.Ntot + s0 + qrow] = (mx + __builtin_amdgcn_logf(l)) * kLn2;
-  }
   __syncthreads();
   // mass of key k: its column of P summed over the window's rows (rows past the window
   // hold zeros); thread k sums rows 0-31 and thread k + 64 rows 32-63, in a fixed order
