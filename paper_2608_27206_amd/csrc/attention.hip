@@ -111,6 +111,47 @@ __device__ __forceinline__ uint4 buf_load16(__amdgpu_buffer_rsrc_t r, unsigned v
 }
 constexpr unsigned kOutOfRange = 0x7FFFFFF0u;
 
+// A wave's 32 query rows of O, stored through LDS.  Lane (c32, g) holds in its O^T
+// accumulators the values dv = 32 t2 + 8 j + 4 g + i of row c32; they go to the wave's own
+// LDS rows (`stage`, stride D + 8) as bf16 of value * inv_l * 2^unshift, then each lane stores
+// 16-byte chunks, so each row's D values are written contiguously (straight from the
+// accumulators, every store instruction wrote 8-byte pieces of 32 rows one token apart, which
+// the write path serves far more slowly).  `ro` covers the segment's rows of this head, row0
+// is the wave's first row in it; rows at or past the segment end fall outside `ro` and are
+// dropped.  Every wave of the workgroup calls this once its last LDS read is behind a
+// workgroup barrier (the staging rows overlay the tile buffers).
+template <int D, int NT>
+__device__ __forceinline__ void store_o_staged(const f32x16 (&oacc)[NT], float inv_l, int unshift,
+                                               uint16_t* stage, __amdgpu_buffer_rsrc_t ro, int row0,
+                                               int qstride) {
+  constexpr int OS = D + 8, CPR = D / 8;
+  const int lane = threadIdx.x & 63, g = lane >> 5, c32 = lane & 31;
+#pragma unroll
+  for (int t2 = 0; t2 < NT; ++t2) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int dv = t2 * 32 + g * 4 + 8 * j;
+      if (dv < D) {
+        float ov[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) ov[i] = __builtin_amdgcn_ldexpf(oacc[t2][4 * j + i] * inv_l, unshift);
+        uint2 pk;
+        pk.x = pack_bf16x2(ov[0], ov[1]);
+        pk.y = pack_bf16x2(ov[2], ov[3]);
+        *reinterpret_cast<uint2*>(&stage[c32 * OS + dv]) = pk;
+      }
+    }
+  }
+  __syncthreads();
+  typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+#pragma unroll
+  for (int c = lane; c < 32 * CPR; c += 64) {
+    const int r = c / CPR, cc = c - (c / CPR) * CPR;
+    const u32x4 val = *reinterpret_cast<const u32x4*>(&stage[r * OS + cc * 8]);
+    __builtin_amdgcn_raw_buffer_store_b128(val, ro, static_cast<unsigned>((row0 + r) * qstride + cc * 8) * 2u, 0, 0);
+  }
+}
+
 typedef __attribute__((address_space(3))) const char lds_char;
 typedef int i32x4 __attribute__((ext_vector_type(4)));
 
@@ -471,24 +512,14 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd(const FwdParams p) {
   const float lp = (l_part[0] + l_part[1]) + (l_part[2] + l_part[3]);
   const float l = lp + __shfl_xor(lp, 32, 64);
   const float inv_l = 1.f / l;
-  if (qrow < L) {
-    uint16_t* op = p.o + static_cast<long long>(s0 + qrow) * qstride + h * D;
-#pragma unroll
-    for (int t2 = 0; t2 < C::NT; ++t2) {
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int dv = t2 * 32 + g * 4 + 8 * j;
-        if (dv < D) {
-          uint2 pk;
-          pk.x = pack_bf16x2(oacc[t2][4 * j + 0] * inv_l, oacc[t2][4 * j + 1] * inv_l);
-          pk.y = pack_bf16x2(oacc[t2][4 * j + 2] * inv_l, oacc[t2][4 * j + 3] * inv_l);
-          *reinterpret_cast<uint2*>(op + dv) = pk;
-        }
-      }
-    }
-    if (g == 0 && p.lse)
-      p.lse[static_cast<long long>(h) * p.Ntot + s0 + qrow] = (m_used + __builtin_amdgcn_logf(l)) * kLn2;
-  }
+  if (qrow < L && g == 0 && p.lse)
+    p.lse[static_cast<long long>(h) * p.Ntot + s0 + qrow] = (m_used + __builtin_amdgcn_logf(l)) * kLn2;
+  // O through each wave's own rows of the K buffers (4 waves x 32 rows fill them exactly),
+  // once every wave is past its last tile reads
+  static_assert(4 * 32 * (D + 8) <= 2 * kBN * C::KS, "staged O does not fit the K buffers");
+  __syncthreads();
+  store_o_staged<D>(oacc, inv_l, 0, &Ks[0][0] + w * 32 * (D + 8),
+                    make_rsrc(p.o + static_cast<long long>(s0) * qstride + h * D, seg_bytes_q), q0 + w * 32, qstride);
 }
 
 // ---------------------------------------------------------------- forward, rotation
@@ -909,28 +940,15 @@ __global__ __launch_bounds__(kRotThreads, 1) void attn_fwd_rot(const FwdParams p
   const float l = __shfl(oacc[2][8], c32, 64);
   const float inv_l = 1.f / l;
   const int unshift = -vt_shift(p.vt_amax[seg * p.Hkv + kvh]);
-  if (qrow < L) {
-    uint16_t* op = p.o + static_cast<long long>(s0 + qrow) * qstride + h * D;
-#pragma unroll
-    for (int t2 = 0; t2 < C::NT; ++t2) {
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int dv = t2 * 32 + g * 4 + 8 * j;
-        if (dv < D) {
-          float ov[4];
-#pragma unroll
-          for (int i = 0; i < 4; ++i) ov[i] = __builtin_amdgcn_ldexpf(oacc[t2][4 * j + i] * inv_l, unshift);
-          uint2 pk;
-          pk.x = pack_bf16x2(ov[0], ov[1]);
-          pk.y = pack_bf16x2(ov[2], ov[3]);
-          *reinterpret_cast<uint2*>(op + dv) = pk;
-        }
-      }
-    }
-    if (g == 0 && p.lse)
-      p.lse[static_cast<long long>(h) * p.Ntot + s0 + qrow] =
-          (m_off + __builtin_amdgcn_logf(l)) * kLn2;
-  }
+  if (qrow < L && g == 0 && p.lse)
+    p.lse[static_cast<long long>(h) * p.Ntot + s0 + qrow] = (m_off + __builtin_amdgcn_logf(l)) * kLn2;
+  // O through each wave's own 32 rows: waves 0-5 in the V^T buffers, 6-11 in the K buffers
+  // (every wave is past its last tile reads: the barriers above)
+  static_assert(6 * 32 * (D + 8) <= 4 * C::DV * kVtStride && 6 * 32 * (D + 8) <= 3 * kBN * C::KS,
+                "staged O does not fit the tile buffers");
+  uint16_t* stage = (w < 6) ? &Vt[0][0] + w * 32 * (D + 8) : &Ks[0][0] + (w - 6) * 32 * (D + 8);
+  store_o_staged<D>(oacc, inv_l, unshift, stage,
+                    make_rsrc(p.o + static_cast<long long>(s0) * qstride + h * D, seg_bytes_q), q0 + w * 32, qstride);
 }
 
 // ---------------------------------------------------------------- windows, fused mass
