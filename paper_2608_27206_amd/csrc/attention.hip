@@ -14,19 +14,20 @@
 //             half-waves.  Online softmax in the log2 domain, P^T feeds O^T = V^T P^T
 //             straight from registers (no LDS round trip); V^T comes from transposing
 //             LDS reads of the row-major V tile.  For head dim 80 the PV product is
-//             padded to 96 rows.  Writes O (bf16) and the natural-log LSE (fp32).
-//             Causal segments (the prefill), short segments and head dim 128.
+//             padded to 96 rows.  Writes O (bf16, through LDS so that each row is stored
+//             contiguously) and the natural-log LSE (fp32).  Causal segments (the
+//             prefill), short segments and head dim 128.
 //
 //  attn_fwd_rot  the same computation for long segments at head dim 80, with 12 waves
 //             per workgroup in three groups that rotate through three phases (see the
 //             kernel), so that VALU and MFMA work of different waves overlap; its PV
-//             product runs in fp16 on V^T tiles that attn_v_amax + attn_vt_prep write once
-//             per call (scaled per segment and KV head into fp16's range, a row of ones
-//             for the row sums).
+//             product runs in fp16 on V^T tiles that attn_vt_clear + attn_v_amax +
+//             attn_vt_prep write once per call (scaled per segment and KV head into fp16's
+//             range, a row of ones for the row sums).
 //
 //  attn_window  segments of at most 64 tokens (the 8x8-patch windows): O, LSE and the
 //             per-key mass in one pass, since a window's row max and sum are final after
-//             its single key tile.
+//             its single key tile; O goes out through LDS, row by row.
 //
 //  attn_mass  key-stationary.  A workgroup = 4 waves x 64 keys of one (segment,
 //             head); K stays in registers, query tiles of 64 rows stream through LDS
