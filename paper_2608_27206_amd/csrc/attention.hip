@@ -1321,13 +1321,22 @@ __global__ __launch_bounds__(kThreads, (D == 80 && !CAUSAL) ? 3 : 2) void attn_m
     if (ntiles > 0) {
       load_q(0, 0);
       if (ntiles > 1) load_q(1, 1);
-      int buf = 0;
       f32x16 s3 = f32x16{};    // block (1,1) of the previous tile
       float l2p = INFINITY;    // its rows' LSE: +inf makes the first iteration's sums add zeros
-      for (int t = 0; t < ntiles; ++t) {
-        wait_vmem_upto(t + 1 < ntiles ? dma_per_tile : 0);
+      // tile t in buffer buf = t % 3; only the LAST tile can hold rows past the querying range
+      // (ntiles = ceil(ql / 64)), so only it masks them
+      auto tile = [&](int buf, auto LAST, int t) __attribute__((always_inline)) {
+        constexpr bool last = decltype(LAST)::value;
+        wait_vmem_upto(last ? 0 : dma_per_tile);
         __syncthreads();
-        const float l2a = load_lse2(t, buf, 0), l2b = load_lse2(t, buf, 1);
+        float l2a, l2b;
+        if constexpr (last) {
+          l2a = load_lse2(t, buf, 0);
+          l2b = load_lse2(t, buf, 1);
+        } else {
+          l2a = Ls[buf][c32] * kLog2e;
+          l2b = Ls[buf][32 + c32] * kLog2e;
+        }
         const int buf2 = (buf == 0) ? 2 : buf - 1;   // (t + 2) % 3
         if (t + 2 < ntiles) load_q(t + 2, buf2);
         bf16x8 qa[C::KC], qc[C::KC];
@@ -1351,8 +1360,13 @@ __global__ __launch_bounds__(kThreads, (D == 80 && !CAUSAL) ? 3 : 2) void attn_m
         interleave();
         __builtin_amdgcn_sched_barrier(0);
         l2p = l2b;
+      };
+      int buf = 0;
+      for (int t = 0; t + 1 < ntiles; ++t) {
+        tile(buf, std::false_type{}, t);
         buf = (buf == 2) ? 0 : buf + 1;
       }
+      tile(buf, std::true_type{}, ntiles - 1);
       sums(s3, l2p, 1);
     }
   } else if (ntiles > 0) {
