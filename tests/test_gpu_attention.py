@@ -299,3 +299,43 @@ def test_mass_only_entry_matches_fused_call():
     torch.cuda.synchronize()
     np.testing.assert_array_equal(host(mass), host(m2))
     np.testing.assert_array_equal(host(lse), host(lse2))
+
+
+@pytest.mark.parametrize("case", range(8))
+def test_vit_random_shapes(case):
+    """Seeded random shapes: head count, head dim, and segment mixes that cross the kernels'
+    selection rules (all segments of at most 64 tokens -> the fused window kernel; a segment of
+    1,024+ tokens at head dim 80 -> the rotation kernel; otherwise the general forward)."""
+    rng = np.random.default_rng(900 + case)
+    kind = case % 4
+    d = 80 if kind == 2 else int(rng.choice([80, 128]))   # the rotation kernel is head dim 80 only
+    H = int(rng.choice([1, 3, 5]))
+    if kind == 0:     # windows only
+        sizes = rng.integers(1, 65, size=int(rng.integers(1, 12)))
+    elif kind == 1:   # short and mid segments
+        sizes = rng.integers(1, 700, size=int(rng.integers(1, 5)))
+    elif kind == 2:   # one long segment among short ones
+        sizes = np.concatenate([rng.integers(1, 200, size=2), [int(rng.integers(1024, 1600))]])
+    else:             # empty segments mixed in
+        sizes = rng.integers(0, 300, size=int(rng.integers(2, 7)))
+        sizes[rng.integers(0, sizes.size)] = 0
+    sizes = [int(x) for x in sizes]
+    if sum(sizes) == 0:
+        sizes[0] = 1
+    cu = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int32)
+    q, k, v = _vit_case(1000 + case, cu, H, d)
+    _check_vit(q, k, v, cu, d)
+
+
+@pytest.mark.parametrize("case", range(6))
+def test_prefill_random_shapes(case):
+    """Seeded random GQA prefills: groups of 1-7 query heads per KV head, head dim 80 or 128,
+    images of 1-3 sequences with random visual and text lengths (text may be as short as 1)."""
+    rng = np.random.default_rng(950 + case)
+    d = int(rng.choice([80, 128]))
+    hkv = int(rng.choice([1, 2, 4]))
+    group = int(rng.integers(1, 8))
+    nb = int(rng.integers(1, 4))
+    vis = [int(x) for x in rng.integers(1, 400, size=nb)]
+    text = [int(x) for x in rng.integers(1, 150, size=nb)]
+    _check_prefill(_packed(2000 + case, vis, text, hkv * group, hkv, d))
