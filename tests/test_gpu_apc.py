@@ -110,6 +110,26 @@ def test_density_tail_ties_in_each_ranking_path(n_b):
     np.testing.assert_allclose(rho, [ref["rho_g"], ref["rho_d"], ref["rho"], ref["phi"]], atol=1e-4)
 
 
+@pytest.mark.parametrize("case", range(6))
+def test_density_random_shapes(case):
+    """Seeded random images: patch size 7, 14 or 16, 1-40 patches per side, tail fractions in
+    (0, 1]; d_i and rho against the oracle."""
+    from paper_2608_27206_amd import pace
+    import torch
+    rng = np.random.default_rng(300 + case)
+    P = int(rng.choice([7, 14, 16]))
+    gh, gw = int(rng.integers(1, 41)), int(rng.integers(1, 41))
+    tail = float(rng.choice([0.01, 0.1, 0.37, 1.0]))
+    img = rng.integers(0, 256, size=(gh * P, gw * P, 3), dtype=np.uint8)
+    img[: (gh * P) // 2] //= 3                      # some structure: a darker half
+    say(f"apc density random {img.shape} patch={P} tail={tail}")
+    rho, d = pace.apc_density(dev_u8(img), P, tail, 0.6, 1.5)
+    torch.cuda.synchronize()
+    ref = oapc.apc_density(img, P, tail)
+    np.testing.assert_allclose(host(d), ref["d"], atol=1e-4)
+    np.testing.assert_allclose(host(rho), [ref["rho_g"], ref["rho_d"], ref["rho"], ref["phi"]], atol=1e-4)
+
+
 def _check_resize(img, oh, ow):
     from paper_2608_27206_amd import pace
     import torch
@@ -134,6 +154,17 @@ def _check_resize(img, oh, ow):
 def test_resize_parity(shape, out):
     img = wl.make_image(3, *shape)
     _check_resize(img, *out)
+
+
+@pytest.mark.parametrize("case", range(6))
+def test_resize_random_shapes(case):
+    """Seeded random sizes: input sides 1-700, outputs from 1/32 of each side up to the side."""
+    rng = np.random.default_rng(400 + case)
+    H, W = int(rng.integers(1, 701)), int(rng.integers(1, 701))
+    oh = int(rng.integers(max(1, -(-H // 32)), H + 1))
+    ow = int(rng.integers(max(1, -(-W // 32)), W + 1))
+    img = rng.integers(0, 256, size=(H, W, 3), dtype=np.uint8)
+    _check_resize(img, oh, ow)
 
 
 def test_resize_rejects_shrink_beyond_32x():
