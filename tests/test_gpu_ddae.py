@@ -45,6 +45,23 @@ def test_topk_gather_bit_exact_on_oracle_scores(n, K, levels):
     _topk_case(S, K, hidden)
 
 
+@pytest.mark.parametrize("case", range(8))
+def test_topk_gather_random_shapes(case):
+    """Seeded random sizes on both sides of the register path's limit (16,384 scores), random
+    K in [1, n - 1], scores continuous or on a few levels (ties), hidden rows of 64-512 values."""
+    rs = np.random.default_rng(700 + case)
+    n = int(rs.choice([int(rs.integers(2, 3000)), int(rs.integers(3000, 16385)), int(rs.integers(16385, 40000))]))
+    K = int(rs.integers(1, n))
+    levels = None if case % 2 == 0 else int(rs.integers(1, 200))
+    say(f"topk random n={n} K={K} levels={levels}")
+    if levels is None:
+        S = rs.random(n).astype(np.float32)
+    else:
+        S = (rs.integers(0, levels, n) / levels).astype(np.float32)
+    hidden = wl.random_bf16(case, (n, 64 * int(rs.integers(1, 9))))
+    _topk_case(S, K, hidden)
+
+
 def test_topk_negative_and_signed_zero():
     S = np.array([-1.0, -0.0, 0.0, 2.0, -3.5, 1e-30, -1e-30, 0.5] * 30, np.float32)
     hidden = wl.random_bf16(99, (S.size, 64))
