@@ -412,7 +412,8 @@ constexpr int kSPad = 20;        // LDS floats per thread's row of kSelR scores 
 //   2. a histogram of floor((S - S_min) * 4096 / (S_max - S_min)), a map that is monotone
 //      in S also in fp32, and the bin b* that holds the K-th largest score;
 //   3. the tokens of bin b* (few, unless scores tie heavily): ranked by direct comparison
-//      when at most kCandMax, else by a radix select on their keys;
+//      when at most kCandMax (up to 64 by one wave, a lane each), else by a radix select on
+//      their keys;
 //   4. ascending compaction: position = number of kept tokens before it.
 __global__ __launch_bounds__(kSelThreads) void ddae_select_gather(const SelectParams p) {
   __shared__ __align__(16) uint32_t hist[kValBins];
