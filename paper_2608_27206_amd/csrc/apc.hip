@@ -548,7 +548,7 @@ __global__ __launch_bounds__(1024) void apc_finalize_c(const DensityParams p) {
   }
 }
 
-constexpr int kTailR = 48;       // distances per thread held in registers: up to 49,152 patches
+constexpr int kTailR = 48;       // most distances per thread held in registers: up to 49,152 patches
 constexpr int kTailBins = 4096;  // value bins over [0, 2], the range of d
 constexpr int kTailCand = 256;   // candidates ranked by direct comparison
 
@@ -556,10 +556,12 @@ struct TailAdd { __device__ float operator()(float a, float b) const { return a 
 
 // Sum of the n_tail largest distances, then rho_d and rho.  d >= 0, so the raw bit patterns
 // order like the values.  With the distances in registers (thread t holds patches
-// j * 1024 + t): a histogram of floor(d * 2048) (monotone in d, clamped), the bin b* that
+// j * 1024 + t, j < R; R = 4, 16 or 48 by the patch count, so that small images do not walk
+// 48 slots per thread): a histogram of floor(d * 2048) (monotone in d, clamped), the bin b* that
 // holds the n_tail-th largest value, the threshold T (the need-th largest key in bin b*,
 // by direct comparison among the bin's few candidates, or a radix select when it holds
 // many ties), and sum = (sum of d > T) + need_eq * T, reduced in a fixed order.
+template <int R>
 __global__ __launch_bounds__(1024) void apc_tail(const DensityParams p) {
   __shared__ __align__(16) uint32_t hist[kTailBins];
   __shared__ uint32_t rhist[4 * 256];
@@ -572,25 +574,25 @@ __global__ __launch_bounds__(1024) void apc_tail(const DensityParams p) {
   uint32_t T;
   int need_eq;
   float s = 0.f;
-  if (p.N <= 1024 * kTailR) {
+  if (p.N <= 1024 * R) {
     // Slots past N read as +0 (range-checked loads), the smallest possible distance.  They
     // are counted into bin 0 at once, not one contended atomic each, and take part in every
     // later step as ordinary zeros: as n_tail <= N, the top n_tail values, T and the sum are
     // those of the N distances (a tie at 0 adds 0), and no step needs a per-slot range test.
-    const uint32_t pad = static_cast<uint32_t>(1024 * kTailR - p.N);
+    const uint32_t pad = static_cast<uint32_t>(1024 * R - p.N);
     for (int i = tid; i < kTailBins; i += 1024) hist[i] = i == 0 ? pad : 0u;
     rhist[tid] = 0u;
     if (tid < 8) misc[tid] = 0u;
-    uint32_t key[kTailR];
+    uint32_t key[R];
     const auto rd = range_rsrc(p.d, static_cast<unsigned>(p.N) * 4u);
 #pragma unroll
-    for (int j = 0; j < kTailR; ++j)
+    for (int j = 0; j < R; ++j)
       key[j] = __float_as_uint(rload_f32(rd, static_cast<unsigned>(j * 1024 + tid) * 4u));
     __syncthreads();
     const int jfull = p.N >> 10;
     const bool rem_live = tid < (p.N & 1023);
 #pragma unroll
-    for (int j = 0; j < kTailR; ++j) {
+    for (int j = 0; j < R; ++j) {
       const int bin = static_cast<int>(fminf(__uint_as_float(key[j]) * 2048.f, static_cast<float>(kTailBins - 1)));
       if (j < jfull || (j == jfull && rem_live)) atomicAdd(&hist[bin], 1u);
     }
@@ -622,7 +624,7 @@ __global__ __launch_bounds__(1024) void apc_tail(const DensityParams p) {
     const uint32_t span = (bstar == kTailBins - 1) ? 0xffffffffu - lo
                           : __float_as_uint(static_cast<float>(bstar + 1) * (1.f / 2048.f)) - lo;
 #pragma unroll
-    for (int j = 0; j < kTailR; ++j) {
+    for (int j = 0; j < R; ++j) {
       if (key[j] - lo < span) {
         const uint32_t slot = atomicAdd(&misc[2], 1u);
         if (slot < static_cast<uint32_t>(kTailCand)) { cand_key[slot] = key[j]; cand_idx[slot] = j * 1024 + tid; }
@@ -661,18 +663,18 @@ __global__ __launch_bounds__(1024) void apc_tail(const DensityParams p) {
     } else {
       // many equal distances in one bin: radix select over the candidates' keys (+1, so
       // that every candidate ranks above the others' 0)
-      uint32_t ck[kTailR];
+      uint32_t ck[R];
 #pragma unroll
-      for (int j = 0; j < kTailR; ++j) ck[j] = (key[j] - lo < span) ? key[j] + 1u : 0u;
+      for (int j = 0; j < R; ++j) ck[j] = (key[j] - lo < span) ? key[j] + 1u : 0u;
       int ne = 0;
-      const uint32_t T1 = radix_select_prezeroed<kTailR, true>(ck, 1024 * kTailR, need, rhist, &misc[5], &ne);
+      const uint32_t T1 = radix_select_prezeroed<R, true>(ck, 1024 * R, need, rhist, &misc[5], &ne);
       if (tid == 0) { misc[3] = T1 - 1u; misc[4] = static_cast<uint32_t>(ne); }
     }
     __syncthreads();
     T = misc[3];
     need_eq = static_cast<int>(misc[4]);
 #pragma unroll
-    for (int j = 0; j < kTailR; ++j)
+    for (int j = 0; j < R; ++j)
       if (key[j] > T) s += __uint_as_float(key[j]);
   } else {
     int need = 0;
@@ -697,6 +699,14 @@ __global__ __launch_bounds__(1024) void apc_tail(const DensityParams p) {
     p.rho_out[2] = p.alpha * rho_g + (1.0f - p.alpha) * rho_d;
     p.rho_out[3] = p.stats[0];
   }
+}
+
+// The tail kernel for p.N distances: the fewest registers per thread that hold them all, or
+// the largest form (which re-reads them from memory beyond 49,152).
+void launch_tail(const DensityParams& p, hipStream_t stream) {
+  if (p.N <= 1024 * 4) hipLaunchKernelGGL(apc_tail<4>, dim3(1), dim3(1024), 0, stream, p);
+  else if (p.N <= 1024 * 16) hipLaunchKernelGGL(apc_tail<16>, dim3(1), dim3(1024), 0, stream, p);
+  else hipLaunchKernelGGL(apc_tail<kTailR>, dim3(1), dim3(1024), 0, stream, p);
 }
 
 // ---------------------------------------------------------------- resize
@@ -1049,7 +1059,7 @@ pace_status_t launch_feature_density(const DensityParams& p, int mode, hipStream
   else if (mode == kFeatBf16) hipLaunchKernelGGL((apc_feat_pass<1, kFeatBf16>), g1, blk, 0, stream, p);
   else hipLaunchKernelGGL((apc_feat_pass<1, kFeatF32>), g1, blk, 0, stream, p);
   if ((st = check_launch("apc_feat_pass<1>")) != PACE_OK) return st;
-  hipLaunchKernelGGL(apc_tail, dim3(1), dim3(1024), 0, stream, p);
+  launch_tail(p, stream);
   return check_launch("apc_tail");
 }
 
@@ -1111,7 +1121,7 @@ pace_status_t pace_apc_density(const uint8_t* img, int H, int W, int patch, doub
   if ((st = check_launch("apc_reduce_c")) != PACE_OK) return st;
   hipLaunchKernelGGL(apc_patch_pass<1>, dim3(p.n_tiles), dim3(kApcThreads), lds, stream, p);
   if ((st = check_launch("apc_patch_pass<1>")) != PACE_OK) return st;
-  hipLaunchKernelGGL(apc_tail, dim3(1), dim3(1024), 0, stream, p);
+  launch_tail(p, stream);
   return check_launch("apc_tail");
 }
 
