@@ -397,9 +397,9 @@ __device__ __forceinline__ uint32_t block_excl_scan(uint32_t v, uint32_t* wt, ui
 
 constexpr int kValBins = 4096;   // value-range bins of the first selection pass
 constexpr int kCandMax = 256;    // candidates ranked by direct comparison
-constexpr int kSPad = 20;        // LDS floats per thread's row of kSelR scores (16 + 4 pad)
 
-// Selection + gather for images of up to kSelThreads * kSelR tokens.  Image b owns select
+// Selection + gather for images of up to kSelThreads * R tokens (R = 4 or 16 scores per
+// thread, by the largest image of the call).  Image b owns select
 // workgroups [cu_swg[b], cu_swg[b+1]); each one computes the image's whole selection (same
 // inputs, same fixed-order arithmetic, hence the same result in every workgroup), the first
 // one writes idx, the scores and the fusion statistics, and workgroup g of the image copies
@@ -408,14 +408,16 @@ constexpr int kSPad = 20;        // LDS floats per thread's row of kSelR scores 
 // The selection finds the threshold pair (T_key, T_idx): token i is kept iff
 // key_i > T_key, or key_i == T_key and i <= T_idx (ties to the lower index).  Steps:
 //   1. scores from coalesced loads, transposed through LDS so that thread t holds tokens
-//      16 t .. 16 t + 15 (the compaction then needs a single block scan);
+//      R t .. R t + R - 1 (the compaction then needs a single block scan);
 //   2. a histogram of floor((S - S_min) * 4096 / (S_max - S_min)), a map that is monotone
 //      in S also in fp32, and the bin b* that holds the K-th largest score;
 //   3. the tokens of bin b* (few, unless scores tie heavily): ranked by direct comparison
 //      when at most kCandMax (up to 64 by one wave, a lane each), else by a radix select on
 //      their keys;
 //   4. ascending compaction: position = number of kept tokens before it.
+template <int R>
 __global__ __launch_bounds__(kSelThreads) void ddae_select_gather(const SelectParams p) {
+  constexpr int kSPad = R + 4;   // LDS floats per thread's row of R scores (+4: 16-byte rows, banks)
   __shared__ __align__(16) uint32_t hist[kValBins];
   __shared__ uint32_t rhist[4 * 256];
   __shared__ __align__(16) float sbuf[kSelThreads * kSPad];
@@ -449,7 +451,7 @@ __global__ __launch_bounds__(kSelThreads) void ddae_select_gather(const SelectPa
   const bool maps = p.scores_in == nullptr;
   // an image of up to 16,384 tokens has at most 256 map workgroups: wave 0 loads four
   // partials per lane, before anything else
-  static_assert(kSelThreads * kSelR <= 4 * 64 * kMapTokens, "partials per lane");
+  static_assert(kSelThreads * R <= 4 * 64 * kMapTokens, "partials per lane");
   MapPartial r[4];
   const int q0 = p.cu_mwg[b] + lane, q1 = p.cu_mwg[b + 1];
   if (maps && w == 0) {
@@ -457,15 +459,15 @@ __global__ __launch_bounds__(kSelThreads) void ddae_select_gather(const SelectPa
     for (int u = 0; u < 4; ++u)
       if (q0 + 64 * u < q1) r[u] = p.part[q0 + 64 * u];
   }
-  float a[kSelR], c[kSelR];
+  float a[R], c[R];
   {
     const auto ra = range_rsrc(maps ? p.vraw + n0 : p.scores_in + n0, static_cast<unsigned>(n) * 4u);
 #pragma unroll
-    for (int j = 0; j < kSelR; ++j) a[j] = rload_f32(ra, static_cast<unsigned>(j * kSelThreads + tid) * 4u);
+    for (int j = 0; j < R; ++j) a[j] = rload_f32(ra, static_cast<unsigned>(j * kSelThreads + tid) * 4u);
     if (maps) {
       const auto rl = range_rsrc(p.lraw + n0, static_cast<unsigned>(n) * 4u);
 #pragma unroll
-      for (int j = 0; j < kSelR; ++j) c[j] = rload_f32(rl, static_cast<unsigned>(j * kSelThreads + tid) * 4u);
+      for (int j = 0; j < R; ++j) c[j] = rload_f32(rl, static_cast<unsigned>(j * kSelThreads + tid) * 4u);
     }
   }
   float smin_l = INFINITY, smax_l = -INFINITY;
@@ -510,13 +512,13 @@ __global__ __launch_bounds__(kSelThreads) void ddae_select_gather(const SelectPa
     const float vinv = vrange > 0.f ? 1.f / vrange : 0.f, linv = lrange > 0.f ? 1.f / lrange : 0.f;
     const float w_l = static_cast<float>(st_d[2]), w_v = static_cast<float>(st_d[3]);
 #pragma unroll
-    for (int j = 0; j < kSelR; ++j) a[j] = w_l * ((c[j] - lmin) * linv) + w_v * ((a[j] - vmin) * vinv);
+    for (int j = 0; j < R; ++j) a[j] = w_l * ((c[j] - lmin) * linv) + w_v * ((a[j] - vmin) * vinv);
   }
 #pragma unroll
-  for (int j = 0; j < kSelR; ++j) {
+  for (int j = 0; j < R; ++j) {
     const int i = j * kSelThreads + tid;
     if (i < n) {
-      sbuf[i + (i >> 4) * (kSPad - kSelR)] = a[j];
+      sbuf[(i / R) * kSPad + i % R] = a[j];
       smin_l = fminf(smin_l, a[j]);
       smax_l = fmaxf(smax_l, a[j]);
     }
@@ -524,7 +526,7 @@ __global__ __launch_bounds__(kSelThreads) void ddae_select_gather(const SelectPa
   if (maps && lead) {
     const auto rs = range_rsrc(p.scores + n0, static_cast<unsigned>(n) * 4u);
 #pragma unroll
-    for (int j = 0; j < kSelR; ++j)
+    for (int j = 0; j < R; ++j)
       rstore_b32(rs, static_cast<unsigned>(j * kSelThreads + tid) * 4u, __float_as_uint(a[j]));
     if (tid == 0 && p.fuse) {
       p.fuse[4 * b + 0] = static_cast<float>(st_d[0]); p.fuse[4 * b + 1] = static_cast<float>(st_d[1]);
@@ -537,24 +539,24 @@ __global__ __launch_bounds__(kSelThreads) void ddae_select_gather(const SelectPa
   __syncthreads();
   if (K <= 0) return;
 
-  const int base = tid * kSelR;
-  uint32_t key[kSelR];
+  const int base = tid * R;
+  uint32_t key[R];
   {
-    float s[kSelR];
+    float s[R];
 #pragma unroll
-    for (int q = 0; q < kSelR / 4; ++q) {
+    for (int q = 0; q < R / 4; ++q) {
       const float4 f = *reinterpret_cast<const float4*>(&sbuf[tid * kSPad + 4 * q]);
       s[4 * q] = f.x; s[4 * q + 1] = f.y; s[4 * q + 2] = f.z; s[4 * q + 3] = f.w;
     }
 #pragma unroll
-    for (int j = 0; j < kSelR; ++j) key[j] = float_key(s[j]);
+    for (int j = 0; j < R; ++j) key[j] = float_key(s[j]);
     if (K < n) {
       float smin = wmm[0][0], smax = wmm[1][0];
       for (int i = 1; i < kSelThreads / 64; ++i) { smin = fminf(smin, wmm[0][i]); smax = fmaxf(smax, wmm[1][i]); }
       // ---- 2. value-range histogram (monotone non-decreasing bin map, clamped)
       const float cscale = smax > smin ? fminf(static_cast<float>(kValBins) / (smax - smin), 3.4e38f) : 0.f;
 #pragma unroll
-      for (int j = 0; j < kSelR; ++j) {
+      for (int j = 0; j < R; ++j) {
         const int bin = static_cast<int>(fminf((s[j] - smin) * cscale, static_cast<float>(kValBins - 1)));
         // equal scores would all hit one LDS address: the all-equal case is counted below
         if (base + j < n && cscale > 0.f) atomicAdd(&hist[bin], 1u);
@@ -581,7 +583,7 @@ __global__ __launch_bounds__(kSelThreads) void ddae_select_gather(const SelectPa
       const int need = static_cast<int>(misc[1]);   // 1 <= need <= count of bin b*
       // ---- 3. candidates: the tokens of bin b*
 #pragma unroll
-      for (int j = 0; j < kSelR; ++j) {
+      for (int j = 0; j < R; ++j) {
         if (base + j < n && static_cast<int>(s[j]) == bstar) {
           const uint32_t slot = atomicAdd(&misc[2], 1u);
           if (slot < static_cast<uint32_t>(kCandMax)) { cand_key[slot] = key[j]; cand_idx[slot] = base + j; }
@@ -620,21 +622,21 @@ __global__ __launch_bounds__(kSelThreads) void ddae_select_gather(const SelectPa
       } else {
         // many ties in one bin: radix select over the candidates' keys, then the lowest
         // indices among the keys equal to the threshold
-        uint32_t ck[kSelR];
+        uint32_t ck[R];
 #pragma unroll
-        for (int j = 0; j < kSelR; ++j) ck[j] = (base + j < n && static_cast<int>(s[j]) == bstar) ? key[j] : 0u;
+        for (int j = 0; j < R; ++j) ck[j] = (base + j < n && static_cast<int>(s[j]) == bstar) ? key[j] : 0u;
         // keys of non-candidates are 0: below every candidate key only if no candidate key
         // is 0, so they are excluded by count instead (the radix ranks the top `need` of
         // all ck, and every candidate outranks a non-candidate unless keys are 0, i.e. -NaN)
         int need_eq = 0;
-        const uint32_t T = radix_select_prezeroed<kSelR, false>(ck, n, need, rhist, &misc[5], &need_eq);
+        const uint32_t T = radix_select_prezeroed<R, false>(ck, n, need, rhist, &misc[5], &need_eq);
         uint32_t eqc = 0;
 #pragma unroll
-        for (int j = 0; j < kSelR; ++j) eqc += (base + j < n && static_cast<int>(s[j]) == bstar && key[j] == T) ? 1u : 0u;
+        for (int j = 0; j < R; ++j) eqc += (base + j < n && static_cast<int>(s[j]) == bstar && key[j] == T) ? 1u : 0u;
         uint32_t tot_eq = 0;
         uint32_t eq_before = block_excl_scan(eqc, wt[1], &tot_eq);
 #pragma unroll
-        for (int j = 0; j < kSelR; ++j) {
+        for (int j = 0; j < R; ++j) {
           if (base + j < n && static_cast<int>(s[j]) == bstar && key[j] == T) {
             if (eq_before == static_cast<uint32_t>(need_eq - 1)) { misc[3] = T; misc[4] = static_cast<uint32_t>(base + j); }
             ++eq_before;
@@ -645,30 +647,30 @@ __global__ __launch_bounds__(kSelThreads) void ddae_select_gather(const SelectPa
       const uint32_t tkey = misc[3];
       const int tidx = static_cast<int>(misc[4]);
 #pragma unroll
-      for (int j = 0; j < kSelR; ++j)
+      for (int j = 0; j < R; ++j)
         key[j] = (base + j < n && (key[j] > tkey || (key[j] == tkey && base + j <= tidx))) ? 1u : 0u;
     } else {
 #pragma unroll
-      for (int j = 0; j < kSelR; ++j) key[j] = (base + j < n) ? 1u : 0u;   // every token kept
+      for (int j = 0; j < R; ++j) key[j] = (base + j < n) ? 1u : 0u;   // every token kept
     }
   }
   // ---- 4. ascending compaction (key[j] is now the keep flag)
   uint32_t kc = 0;
 #pragma unroll
-  for (int j = 0; j < kSelR; ++j) kc += key[j];
+  for (int j = 0; j < R; ++j) kc += key[j];
   uint32_t tot_keep = 0;
   uint32_t pos = block_excl_scan(kc, wt[2], &tot_keep);
   if (lead) {   // the kept indices (one workgroup stores them; the others only need their slice)
     const auto ri = range_rsrc(p.idx + out0, static_cast<unsigned>(K) * 4u);
     uint32_t ps = pos;
 #pragma unroll
-    for (int j = 0; j < kSelR; ++j) {
+    for (int j = 0; j < R; ++j) {
       rstore_b32(ri, key[j] ? ps * 4u : kNoStore, static_cast<uint32_t>(n0 + base + j));
       ps += key[j];
     }
   }
 #pragma unroll
-  for (int j = 0; j < kSelR; ++j) {
+  for (int j = 0; j < R; ++j) {
     if (key[j] && static_cast<int>(pos) >= r0 && static_cast<int>(pos) < r1) rows_lds[pos - r0] = n0 + base + j;
     pos += key[j];
   }
@@ -720,7 +722,8 @@ pace_status_t run_select(SelectParams& p, const void* hidden, size_t row_bytes, 
   const int ktot = p.cu_keep[p.B];
   if (fused) {
     // rows per select workgroup: at least 4, and about one workgroup per CU (256) for the
-    // gather (a select workgroup's ~105 KB of LDS leaves room for one per CU)
+    // gather (a select workgroup's LDS, ~105 KB with 16 scores per thread, ~57 KB with 4,
+    // leaves room for one or two per CU)
     int R = 1;
     if (hidden != nullptr && ktot > 0) {
       R = (ktot + 255) / 256;
@@ -735,8 +738,12 @@ pace_status_t run_select(SelectParams& p, const void* hidden, size_t row_bytes, 
       const int K = p.cu_keep[b + 1] - p.cu_keep[b];
       p.cu_swg[b + 1] = p.cu_swg[b] + ((hidden != nullptr && K > 0) ? (K + R - 1) / R : 1);
     }
-    hipLaunchKernelGGL(ddae_select_gather, dim3(p.cu_swg[p.B]), dim3(kSelThreads),
-                       static_cast<size_t>(R) * sizeof(int), stream, p);
+    if (nmax <= kSelThreads * 4)
+      hipLaunchKernelGGL(ddae_select_gather<4>, dim3(p.cu_swg[p.B]), dim3(kSelThreads),
+                         static_cast<size_t>(R) * sizeof(int), stream, p);
+    else
+      hipLaunchKernelGGL(ddae_select_gather<kSelR>, dim3(p.cu_swg[p.B]), dim3(kSelThreads),
+                         static_cast<size_t>(R) * sizeof(int), stream, p);
     return check_launch("ddae_select_gather");
   }
   hipLaunchKernelGGL(ddae_select, dim3(p.B), dim3(kSelThreads), 0, stream, p);
