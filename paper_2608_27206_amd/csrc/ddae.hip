@@ -398,8 +398,8 @@ __device__ __forceinline__ uint32_t block_excl_scan(uint32_t v, uint32_t* wt, ui
 constexpr int kValBins = 4096;   // value-range bins of the first selection pass
 constexpr int kCandMax = 256;    // candidates ranked by direct comparison
 
-// Selection + gather for images of up to kSelThreads * R tokens (R = 4 or 16 scores per
-// thread, by the largest image of the call).  Image b owns select
+// Selection + gather for images of up to kSelThreads * R tokens (R = 4, 8, 12 or 16 scores
+// per thread, the fewest that hold the largest image of the call).  Image b owns select
 // workgroups [cu_swg[b], cu_swg[b+1]); each one computes the image's whole selection (same
 // inputs, same fixed-order arithmetic, hence the same result in every workgroup), the first
 // one writes idx, the scores and the fusion statistics, and workgroup g of the image copies
@@ -722,8 +722,8 @@ pace_status_t run_select(SelectParams& p, const void* hidden, size_t row_bytes, 
   const int ktot = p.cu_keep[p.B];
   if (fused) {
     // rows per select workgroup: at least 4, and about one workgroup per CU (256) for the
-    // gather (a select workgroup's LDS, ~105 KB with 16 scores per thread, ~57 KB with 4,
-    // leaves room for one or two per CU)
+    // gather (a select workgroup's LDS, ~105 KB with 16 scores per thread down to ~57 KB
+    // with 4, leaves room for one or two per CU)
     int R = 1;
     if (hidden != nullptr && ktot > 0) {
       R = (ktot + 255) / 256;
@@ -738,12 +738,12 @@ pace_status_t run_select(SelectParams& p, const void* hidden, size_t row_bytes, 
       const int K = p.cu_keep[b + 1] - p.cu_keep[b];
       p.cu_swg[b + 1] = p.cu_swg[b] + ((hidden != nullptr && K > 0) ? (K + R - 1) / R : 1);
     }
-    if (nmax <= kSelThreads * 4)
-      hipLaunchKernelGGL(ddae_select_gather<4>, dim3(p.cu_swg[p.B]), dim3(kSelThreads),
-                         static_cast<size_t>(R) * sizeof(int), stream, p);
-    else
-      hipLaunchKernelGGL(ddae_select_gather<kSelR>, dim3(p.cu_swg[p.B]), dim3(kSelThreads),
-                         static_cast<size_t>(R) * sizeof(int), stream, p);
+    const dim3 grid(p.cu_swg[p.B]);
+    const size_t dyn = static_cast<size_t>(R) * sizeof(int);
+    if (nmax <= kSelThreads * 4) hipLaunchKernelGGL(ddae_select_gather<4>, grid, dim3(kSelThreads), dyn, stream, p);
+    else if (nmax <= kSelThreads * 8) hipLaunchKernelGGL(ddae_select_gather<8>, grid, dim3(kSelThreads), dyn, stream, p);
+    else if (nmax <= kSelThreads * 12) hipLaunchKernelGGL(ddae_select_gather<12>, grid, dim3(kSelThreads), dyn, stream, p);
+    else hipLaunchKernelGGL(ddae_select_gather<kSelR>, grid, dim3(kSelThreads), dyn, stream, p);
     return check_launch("ddae_select_gather");
   }
   hipLaunchKernelGGL(ddae_select, dim3(p.B), dim3(kSelThreads), 0, stream, p);
