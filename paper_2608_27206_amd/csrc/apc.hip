@@ -556,8 +556,8 @@ struct TailAdd { __device__ float operator()(float a, float b) const { return a 
 
 // Sum of the n_tail largest distances, then rho_d and rho.  d >= 0, so the raw bit patterns
 // order like the values.  With the distances in registers (thread t holds patches
-// j * 1024 + t, j < R; R = 4, 16 or 48 by the patch count, so that small images do not walk
-// 48 slots per thread): a histogram of floor(d * 2048) (monotone in d, clamped), the bin b* that
+// j * 1024 + t, j < R; R = 4, 16, 32, 44 or 48, the fewest that hold the patch count, so that
+// smaller images do not walk 48 slots per thread): a histogram of floor(d * 2048) (monotone in d, clamped), the bin b* that
 // holds the n_tail-th largest value, the threshold T (the need-th largest key in bin b*,
 // by direct comparison among the bin's few candidates, or a radix select when it holds
 // many ties), and sum = (sum of d > T) + need_eq * T, reduced in a fixed order.
@@ -706,6 +706,8 @@ __global__ __launch_bounds__(1024) void apc_tail(const DensityParams p) {
 void launch_tail(const DensityParams& p, hipStream_t stream) {
   if (p.N <= 1024 * 4) hipLaunchKernelGGL(apc_tail<4>, dim3(1), dim3(1024), 0, stream, p);
   else if (p.N <= 1024 * 16) hipLaunchKernelGGL(apc_tail<16>, dim3(1), dim3(1024), 0, stream, p);
+  else if (p.N <= 1024 * 32) hipLaunchKernelGGL(apc_tail<32>, dim3(1), dim3(1024), 0, stream, p);
+  else if (p.N <= 1024 * 44) hipLaunchKernelGGL(apc_tail<44>, dim3(1), dim3(1024), 0, stream, p);
   else hipLaunchKernelGGL(apc_tail<kTailR>, dim3(1), dim3(1024), 0, stream, p);
 }
 

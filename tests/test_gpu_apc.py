@@ -188,7 +188,9 @@ def _check_features(bits, tail=0.1, atol=1e-4):
     return host(rho), host(d)
 
 
-@pytest.mark.parametrize("n,dim", [(3000, 1280), (777, 8), (130, 592), (64, 3584), (500, 3), (257, 100)])
+# 20,000 and 46,000 rows reach the tail's 32- and 48-distance forms
+@pytest.mark.parametrize("n,dim", [(3000, 1280), (777, 8), (130, 592), (64, 3584), (500, 3), (257, 100),
+                                   (20000, 16), (46000, 8)])
 def test_density_features_random(n, dim):
     rs = np.random.default_rng(n + dim)
     x = rs.normal(size=(n, dim)).astype(np.float32) + rs.normal(size=(1, dim)).astype(np.float32)
