@@ -126,10 +126,12 @@ __device__ __forceinline__ float feat_of(uint8_t b) { return static_cast<float>(
 // of a tile's patches; patch j of the tile starts at byte j * 3P of each staged row.
 template <int PASS>
 __global__ __launch_bounds__(kApcThreads) void apc_patch_pass(const DensityParams p) {
-  extern __shared__ uint32_t lds[];
+  extern __shared__ __align__(16) uint32_t lds[];
   uint32_t* px = lds;                                             // [P][row_dwords]
   float* inv = reinterpret_cast<float*>(px + p.P * p.row_dwords);  // [64]
-  float* chat = inv + kPatchesPerTile;                            // [D] (pass 1)
+  float* chat = inv + kPatchesPerTile;   // pass 1: c_hat as [P][cstride] (+12 floats of slack)
+  const int pb = 3 * p.P;                // bytes of one patch row
+  const int cstride = (pb + 3) & ~3;
   __shared__ int shift[kMaxPatch];
   __shared__ float red[kApcThreads / 64];
   const int tile = blockIdx.x;
@@ -144,6 +146,12 @@ __global__ __launch_bounds__(kApcThreads) void apc_patch_pass(const DensityParam
       cs[k] = e < p.D ? p.csum[e] : 0.f;
     }
   }
+  const int j = threadIdx.x >> 2, t = threadIdx.x & 3;
+  float s_inv = 0.f;   // pass 1: 1/||f|| of the thread's patch, requested before the tile
+  if (PASS == 1) {
+    const int px0_ = (tile % p.tiles_x) * kPatchesPerTile;
+    if (j < min(kPatchesPerTile, p.gw - px0_)) s_inv = p.inv_norm[(tile / p.tiles_x) * p.gw + px0_ + j];
+  }
   int py, px0;
   const int np = stage_tile(p, tile, px, shift, &py, &px0);
   if (PASS == 1) {
@@ -155,7 +163,7 @@ __global__ __launch_bounds__(kApcThreads) void apc_patch_pass(const DensityParam
     for (int k = 0; k < kCPer; ++k) {
       const int e = static_cast<int>(threadIdx.x) + k * kApcThreads;
       const float c = cs[k] * invN;
-      if (e < p.D) chat[e] = c;
+      if (e < p.D) chat[(e / pb) * cstride + e % pb] = c;
       ss += c * c;
     }
     ss = wave_sum(ss);
@@ -171,7 +179,7 @@ __global__ __launch_bounds__(kApcThreads) void apc_patch_pass(const DensityParam
 #pragma unroll
     for (int k = 0; k < kCPer; ++k) {
       const int e = static_cast<int>(threadIdx.x) + k * kApcThreads;
-      if (e < p.D) chat[e] *= ic;
+      if (e < p.D) chat[(e / pb) * cstride + e % pb] *= ic;
     }
     if (blockIdx.x == 0 && threadIdx.x == 0) {
       p.stats[0] = ss;          // phi
@@ -182,21 +190,40 @@ __global__ __launch_bounds__(kApcThreads) void apc_patch_pass(const DensityParam
   }
   const uint8_t* pxb = reinterpret_cast<const uint8_t*>(px);
   const int rb = p.row_dwords * 4;
-  const int pb = 3 * p.P;                  // bytes of one patch row
-  const int j = threadIdx.x >> 2, t = threadIdx.x & 3;
+  // Thread t of patch j takes bytes [12t, 12t + nb) of each of the patch's rows (nb <= 12, as a
+  // patch row has at most 48 bytes): four dword reads cover them, realigned with alignbyte, so a
+  // row costs a few LDS reads instead of one per byte.  The row's first byte sits at byte
+  // (row start & 3) of its staged LDS row.
+  const int c0 = 12 * t;
+  const int nb = min(12, pb - c0);
+  auto row_bytes = [&](int r, uint32_t x[3]) __attribute__((always_inline)) {
+    const int b0 = (py * p.P + r) * p.W * 3 + px0 * pb;
+    const int o = r * rb + (b0 & 3) + j * pb + c0;
+    const uint32_t* wp = px + (o >> 2);
+    const uint32_t w0 = wp[0], w1 = wp[1], w2 = wp[2], w3 = wp[3];
+    const int al = o & 3;
+    x[0] = __builtin_amdgcn_alignbyte(w1, w0, al);
+    x[1] = __builtin_amdgcn_alignbyte(w2, w1, al);
+    x[2] = __builtin_amdgcn_alignbyte(w3, w2, al);
+  };
   if (PASS == 0) {
     // ||f||^2 = sum (b/127.5 - 1)^2 = (4 sum b^2 - 1020 sum b + 65025 D) / 65025, from exact
-    // integer sums: the four threads of a patch take every fourth dword of each of its rows
-    // (bytes outside the patch masked off) and add b^2 and b with packed-byte dot products
+    // integer sums of b^2 and b (packed-byte dot products; bytes past nb masked off)
     uint32_t sq = 0u, sm = 0u;
-    if (j < np) {
+    if (j < np && nb > 0) {
+      uint32_t keep[3];
+#pragma unroll
+      for (int k = 0; k < 3; ++k) {
+        const int v = min(max(nb - 4 * k, 0), 4);
+        keep[k] = v >= 4 ? 0xffffffffu : ((1u << (8 * v)) - 1u);
+      }
+#pragma unroll 2
       for (int r = 0; r < p.P; ++r) {
-        const int o = r * rb + shift[r] + j * pb;   // first byte of the patch's row r
-        const int k0 = o >> 2, k1 = (o + pb - 1) >> 2;
-        for (int k = k0 + t; k <= k1; k += 4) {
-          const int lo = max(o - 4 * k, 0), hi = min(o + pb - 4 * k, 4);
-          const uint32_t keep = (hi >= 4 ? 0xffffffffu : ((1u << (8 * hi)) - 1u)) & ~((1u << (8 * lo)) - 1u);
-          const uint32_t w = px[k] & keep;
+        uint32_t x[3];
+        row_bytes(r, x);
+#pragma unroll
+        for (int k = 0; k < 3; ++k) {
+          const uint32_t w = x[k] & keep[k];
           sq = __builtin_amdgcn_udot4(w, w, sq, false);
           sm = __builtin_amdgcn_udot4(w, 0x01010101u, sm, false);
         }
@@ -223,17 +250,22 @@ __global__ __launch_bounds__(kApcThreads) void apc_patch_pass(const DensityParam
       p.partial[static_cast<long long>(tile) * p.D + e] = sum;
     }
   } else {
+    // d_i^2 = sum_e (f_e s - c_hat_e)^2 over the thread's bytes of every row, in row order
     float acc = 0.f;
-    if (j < np) {
-      // the four threads of a patch take every fourth byte of each of its rows
-      const float s = p.inv_norm[py * p.gw + px0 + j];
+    if (j < np && nb > 0) {
+#pragma unroll 2
       for (int r = 0; r < p.P; ++r) {
-        const uint8_t* row = pxb + r * rb + shift[r] + j * pb;
-        const float* cr = chat + r * pb;
-#pragma unroll 4
-        for (int cb = t; cb < pb; cb += 4) {
-          const float y = feat_of(row[cb]) * s - cr[cb];
-          acc += y * y;
+        uint32_t x[3];
+        row_bytes(r, x);
+        // 12 values from the thread's first column (the ones past nb, read from the next row or
+        // the slack, are not used)
+        const float4* cr = reinterpret_cast<const float4*>(chat + r * cstride + c0);
+        const float4 ca = cr[0], cb = cr[1], cc = cr[2];
+        const float cv[12] = {ca.x, ca.y, ca.z, ca.w, cb.x, cb.y, cb.z, cb.w, cc.x, cc.y, cc.z, cc.w};
+#pragma unroll
+        for (int i = 0; i < 12; ++i) {
+          const float y = feat_of(static_cast<uint8_t>(x[i >> 2] >> (8 * (i & 3)))) * s_inv - cv[i];
+          acc += (i < nb) ? y * y : 0.f;
         }
       }
     }
@@ -1103,7 +1135,7 @@ pace_status_t pace_apc_density(const uint8_t* img, int H, int W, int patch, doub
   p.D = 3 * patch * patch;
   p.tiles_x = (p.gw + kPatchesPerTile - 1) / kPatchesPerTile;
   p.n_tiles = p.gh * p.tiles_x;
-  p.row_dwords = (kPatchesPerTile * patch * 3 + 3) / 4 + 2;
+  p.row_dwords = ((kPatchesPerTile * patch * 3 + 3) / 4 + 2 + 3) & ~3;
   int nt = pace_keep_count(tail_frac, p.N);
   p.n_tail = nt < 1 ? 1 : nt;
   p.alpha = alpha; p.gamma = gamma;
@@ -1115,7 +1147,8 @@ pace_status_t pace_apc_density(const uint8_t* img, int H, int W, int patch, doub
   float* dws = c.take<float>(p.N);
   p.d = d_out ? d_out : dws;
   p.rho_out = rho_out;
-  const size_t lds = (static_cast<size_t>(patch) * p.row_dwords + kPatchesPerTile + p.D) * sizeof(float);
+  const size_t lds = (static_cast<size_t>(patch) * p.row_dwords + kPatchesPerTile +
+                      static_cast<size_t>(patch) * ((3 * patch + 3) & ~3) + 12) * sizeof(float);
   hipLaunchKernelGGL(apc_patch_pass<0>, dim3(p.n_tiles), dim3(kApcThreads), lds, stream, p);
   pace_status_t st = check_launch("apc_patch_pass<0>");
   if (st != PACE_OK) return st;
