@@ -130,6 +130,24 @@ def test_density_random_shapes(case):
     np.testing.assert_allclose(host(rho), [ref["rho_g"], ref["rho_d"], ref["rho"], ref["phi"]], atol=1e-4)
 
 
+@pytest.mark.parametrize("patch,gh,gw", [(1, 40, 37), (2, 23, 31), (5, 17, 29), (3, 64, 70), (11, 9, 67)])
+def test_density_small_and_odd_patches(patch, gh, gw):
+    """Patch sizes whose rows split unevenly over a patch's four threads (3P bytes: 3, 6, 15, 9
+    and 33), with a tile row of more than 64 patches (a second tile per patch row); d_i and rho
+    against the oracle."""
+    from paper_2608_27206_amd import pace
+    import torch
+    rng = np.random.default_rng(400 + patch)
+    img = rng.integers(0, 256, size=(gh * patch, gw * patch, 3), dtype=np.uint8)
+    img[:, : (gw * patch) // 3] //= 2
+    say(f"apc density {img.shape} patch={patch}")
+    rho, d = pace.apc_density(dev_u8(img), patch, 0.1, 0.6, 1.5)
+    torch.cuda.synchronize()
+    ref = oapc.apc_density(img, patch, 0.1)
+    np.testing.assert_allclose(host(d), ref["d"], atol=1e-4)
+    np.testing.assert_allclose(host(rho), [ref["rho_g"], ref["rho_d"], ref["rho"], ref["phi"]], atol=1e-4)
+
+
 def _check_resize(img, oh, ow):
     from paper_2608_27206_amd import pace
     import torch
