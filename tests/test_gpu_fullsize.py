@@ -202,6 +202,15 @@ def test_frame4k_apc(w4k):
     d_ref = oapc.detail_distances(T, oapc.background_direction(T))
     np.testing.assert_allclose(host(d), d_ref, atol=1e-4)
     np.testing.assert_allclose(host(rho), [gold["rho_g"], gold["rho_d"], gold["rho"], gold["phi"]], atol=1e-4)
+    # at gamma = 1.5 rho_d is clamped at 1 (the tail mean is 1.92); above the tail mean it is
+    # d_top / gamma, which pins the frame's tail mean itself (the 4,220 largest of 42,196 d_i)
+    gamma = 2.5
+    assert gold["d_top"] < gamma
+    rho2, _ = pace.apc_density(dev_u8(img), 14, 0.10, 0.6, gamma)
+    torch.cuda.synchronize()
+    r2 = host(rho2)
+    rho_d = gold["d_top"] / gamma
+    np.testing.assert_allclose(r2[:3], [gold["rho_g"], rho_d, 0.6 * gold["rho_g"] + 0.4 * rho_d], atol=1e-4)
 
 
 def test_frame4k_select(w4k):
