@@ -10,8 +10,9 @@
 //                      rho_g = 1 - phi (Eq. 2) and c_hat = c/||c||, recomputed by every
 //                      workgroup from the sums; then d_i = ||T_i - c_hat|| (the image is
 //                      re-read, mostly from L2/MALL)
-//   apc_tail           radix select of the n_tail-th largest d, tail mean, rho_d, rho
-//                      (up to 49,152 distances held in registers, more re-read from memory)
+//   apc_tail           the n_tail-th largest d (a value histogram, then the candidates of its
+//                      bin ranked), tail mean, rho_d, rho (up to 49,152 distances held in
+//                      registers, more re-read from memory)
 //
 // The per-patch feature is the patch's pixels mapped to x/127.5 - 1 (component order:
 // patch row, pixel column, channel).  The order does not change norms or cosines.
@@ -589,7 +590,8 @@ struct TailAdd { __device__ float operator()(float a, float b) const { return a 
 // Sum of the n_tail largest distances, then rho_d and rho.  d >= 0, so the raw bit patterns
 // order like the values.  With the distances in registers (thread t holds patches
 // j * 1024 + t, j < R; R = 4, 16, 32, 44 or 48, the fewest that hold the patch count, so that
-// smaller images do not walk 48 slots per thread): a histogram of floor(d * 2048) (monotone in d, clamped), the bin b* that
+// smaller images do not walk 48 slots per thread): a histogram of floor(d * 2048) (monotone
+// in d, clamped), the bin b* that
 // holds the n_tail-th largest value, the threshold T (the need-th largest key in bin b*,
 // by direct comparison among the bin's few candidates, or a radix select when it holds
 // many ties), and sum = (sum of d > T) + need_eq * T, reduced in a fixed order.
