@@ -3,14 +3,17 @@
 //
 // Two launches per call when every image has at most 16,384 tokens:
 //   ddae_token_maps      grid-wide, one wave of 64 tokens (one per lane) per workgroup,
-//                        workgroups never straddle two images: head sums (and 2x2 merge + permutation for S_vis) ->
-//                        raw S_vis, S_llm per LLM visual token (HBM-bound read of the
+//                        workgroups never straddle two images: head sums (and the 2x2
+//                        merge + permutation for S_vis) -> raw S_vis, S_llm per LLM
+//                        visual token (HBM-bound read of the
 //                        masses), plus each workgroup's min, max and float64 sum and sum
 //                        of squares of both maps
 //   ddae_select_gather   a few workgroups per image, each running the same deterministic
 //                        selection: the image's statistics from those partials (min-max
 //                        ranges; the std of a min-max map is std(raw) / range), the fused
-//                        scores in registers, radix top-K with lower-index ties, the
+//                        scores in registers (R per thread), top-K by a value-range
+//                        histogram and the ranked candidates of its threshold bin (a radix
+//                        select when that bin holds many ties), lower-index ties, the
 //                        ascending positions of the kept tokens; then each workgroup copies
 //                        its own slice of the kept hidden rows.  Repeating the selection
 //                        in every workgroup costs L2 reads, not latency, and saves a
