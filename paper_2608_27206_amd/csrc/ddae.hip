@@ -5,9 +5,9 @@
 //   ddae_token_maps      grid-wide, one wave of 64 tokens (one per lane) per workgroup,
 //                        workgroups never straddle two images: head sums (and the 2x2
 //                        merge + permutation for S_vis) -> raw S_vis, S_llm per LLM
-//                        visual token (HBM-bound read of the
-//                        masses), plus each workgroup's min, max and float64 sum and sum
-//                        of squares of both maps
+//                        visual token (HBM-bound read of the masses), plus each
+//                        workgroup's min, max and float64 sum and sum of squares of
+//                        both maps
 //   ddae_select_gather   a few workgroups per image, each running the same deterministic
 //                        selection: the image's statistics from those partials (min-max
 //                        ranges; the std of a min-max map is std(raw) / range), the fused
