@@ -234,7 +234,8 @@ pace_status_t pace_gemm_bf16(const uint16_t* A, const uint16_t* B, const float* 
  * (o + 0.5) * X / oX; taps outside the image are dropped and the remaining
  * weights renormalised; accumulation in fp32 without intermediate rounding;
  * result rounded half up and clamped to [0, 255].  Pointers need no alignment.
- * UNSUPPORTED when a side shrinks by more than 32x.
+ * Up to 32x per side, workgroups stage their output tile's input span in LDS; beyond
+ * that, one workgroup per output pixel reads its span from memory (float64 sums).
  */
 pace_status_t pace_apc_downsample(const uint8_t* src, int H, int W, uint8_t* dst, int oH, int oW,
                                   hipStream_t stream);

@@ -749,7 +749,8 @@ void launch_tail(const DensityParams& p, hipStream_t stream) {
 // One workgroup per output tile of ty x tx pixels.  It computes the tile's column and row
 // tap weights once (LDS), stages the input region it needs (range-checked dword loads,
 // so reads never leave the image), runs the horizontal pass into LDS in fp32 and the
-// vertical pass straight to the output.
+// vertical pass straight to the output.  Shrinks beyond 32x per side, whose spans do not fit
+// a staged tile, take apc_resize_direct (one workgroup per output pixel).
 constexpr int kRsThreads = 256;
 constexpr int kRsMaxLds = 64 * 1024;
 
@@ -978,6 +979,79 @@ __global__ __launch_bounds__(kRsThreads) void apc_resize_reg(const ResizeParams 
       const float v = floorf(acc + 0.5f);
       const int u = static_cast<int>(fminf(fmaxf(v, 0.f), 255.f));
       p.dst[(static_cast<long long>(oy0 + r) * p.oW + ox0 + c) * 3 + ch] = static_cast<uint8_t>(u);
+    }
+  }
+}
+
+// Shrinks too strong for a staged tile (beyond 32x per side): one workgroup per output pixel,
+// straight from memory.  Thread t takes the input columns x = lo_x + t, lo_x + t + 256, ...
+// of the pixel's span (consecutive threads read consecutive pixels); for every input row y of
+// the span it adds w_x * x[y][x] over its columns (float64) and then w_y times that into its
+// sums.  The weights are make_taps' (the same exact integer distance numerators, fp32 cubic),
+// normalised at the end by their sums; the workgroup's sums are reduced in a fixed order.
+__device__ __forceinline__ void direct_span(int o, int n, int m, int* lo, int* cnt) {
+  const double centre = (static_cast<double>(o) + 0.5) * n / m;
+  const double support = 2.0 * fmax(1.0, static_cast<double>(n) / m);
+  *lo = max(static_cast<int>(floor(centre - support - 0.5)) - 1, 0);
+  *cnt = min(n, static_cast<int>(ceil(centre + support + 0.5)) + 2) - *lo;
+}
+__device__ __forceinline__ float direct_weight(int i, int o, int n, int m, float inv_den) {
+  const long long num = (2ll * i + 1) * m - (2ll * o + 1) * n;
+  return keys_cubic(static_cast<float>(num) * inv_den);
+}
+
+__global__ __launch_bounds__(kRsThreads) void apc_resize_direct(const ResizeParams p) {
+  __shared__ double red[4][kRsThreads / 64];
+  const int ox = static_cast<int>(blockIdx.x % static_cast<unsigned>(p.oW));
+  const int oy = static_cast<int>(blockIdx.x / static_cast<unsigned>(p.oW));
+  const int tid = threadIdx.x;
+  int lox, nx, loy, ny;
+  direct_span(ox, p.W, p.oW, &lox, &nx);
+  direct_span(oy, p.H, p.oH, &loy, &ny);
+  const float idx = p.invdx, idy = p.invdy;
+  double a0 = 0.0, a1 = 0.0, a2 = 0.0, swx = 0.0, swy = 0.0;
+  for (int j = tid; j < nx; j += kRsThreads) swx += direct_weight(lox + j, ox, p.W, p.oW, idx);
+  for (int yi = 0; yi < ny; ++yi) {
+    const int y = loy + yi;
+    const float wy = direct_weight(y, oy, p.H, p.oH, idy);
+    if (tid == 0) swy += wy;
+    if (wy == 0.f) continue;   // the same for every thread
+    const uint8_t* row = p.src + static_cast<long long>(y) * p.W * 3;
+    double h0 = 0.0, h1 = 0.0, h2 = 0.0;
+    for (int j = tid; j < nx; j += kRsThreads) {
+      const int x = lox + j;
+      const double wx = direct_weight(x, ox, p.W, p.oW, idx);
+      h0 += wx * row[3 * x];
+      h1 += wx * row[3 * x + 1];
+      h2 += wx * row[3 * x + 2];
+    }
+    a0 += wy * h0;
+    a1 += wy * h1;
+    a2 += wy * h2;
+  }
+  double v[4] = {a0, a1, a2, swx};
+#pragma unroll
+  for (int k = 0; k < 4; ++k)
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) v[k] += __shfl_xor(v[k], o, 64);
+  if ((tid & 63) == 0)
+#pragma unroll
+    for (int k = 0; k < 4; ++k) red[k][tid >> 6] = v[k];
+  __syncthreads();
+  if (tid == 0) {
+    double t[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      t[k] = red[k][0];
+#pragma unroll
+      for (int wv = 1; wv < kRsThreads / 64; ++wv) t[k] += red[k][wv];
+    }
+    const double norm = 1.0 / (t[3] * swy);
+    uint8_t* dst = p.dst + (static_cast<long long>(oy) * p.oW + ox) * 3;
+#pragma unroll
+    for (int c = 0; c < 3; ++c) {
+      const double val = floor(t[c] * norm + 0.5);
+      dst[c] = static_cast<uint8_t>(fmin(fmax(val, 0.0), 255.0));
     }
   }
 }
@@ -1289,8 +1363,6 @@ pace_status_t pace_apc_downsample(const uint8_t* src, int H, int W, uint8_t* dst
                "pace_apc_downsample: sizes %dx%d -> %dx%d must shrink or keep", H, W, oH, oW);
   PACE_REQUIRE(static_cast<long long>(H) * W * 3 < (1ll << 31), "pace_apc_downsample: image too large");
   const double sx = static_cast<double>(W) / oW, sy = static_cast<double>(H) / oH;
-  if (sx > 32.0 || sy > 32.0)
-    return set_error(PACE_ERR_UNSUPPORTED, "pace_apc_downsample: shrink factor above 32");
   ResizeParams p{};
   p.src = src; p.dst = dst;
   p.H = H; p.W = W; p.oH = oH; p.oW = oW;
@@ -1298,6 +1370,11 @@ pace_status_t pace_apc_downsample(const uint8_t* src, int H, int W, uint8_t* dst
   p.ry = static_cast<float>(H) / static_cast<float>(oH);
   p.invdx = 1.f / static_cast<float>(2ll * (W > oW ? W : oW));
   p.invdy = 1.f / static_cast<float>(2ll * (H > oH ? H : oH));
+  if (sx > 32.0 || sy > 32.0) {
+    // a staged tile's input span grows with the shrink factor: per output pixel from memory
+    hipLaunchKernelGGL(apc_resize_direct, dim3(static_cast<unsigned>(oW) * oH), dim3(kRsThreads), 0, stream, p);
+    return check_launch("apc_resize_direct");
+  }
   // taps of one output pixel span at most 4*s + 4 inputs (the support plus one zero-weight
   // guard tap on each side)
   p.ntx = static_cast<int>(ceil(4.0 * (sx > 1 ? sx : 1))) + 4;
@@ -1323,7 +1400,10 @@ pace_status_t pace_apc_downsample(const uint8_t* src, int H, int W, uint8_t* dst
   while (lds > kRsMaxLds || p.rows_cap > 256) {
     if (ty > 1) ty >>= 1;
     else if (tx > 1) tx >>= 1;
-    else return set_error(PACE_ERR_UNSUPPORTED, "pace_apc_downsample: shrink factor too large");
+    else {
+      hipLaunchKernelGGL(apc_resize_direct, dim3(static_cast<unsigned>(oW) * oH), dim3(kRsThreads), 0, stream, p);
+      return check_launch("apc_resize_direct");
+    }
     lds = plan(ty, tx, p);
   }
   dim3 grid((oW + tx - 1) / tx, (oH + ty - 1) / ty);

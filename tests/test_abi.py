@@ -131,8 +131,6 @@ def test_errors_before_launch():
     assert st == 1
     st = L.pace_apc_density_features(fake, 100, 16, 0.1, 0.6, 1.5, None, fake, fake, 16, None)
     assert st == 3
-    st = L.pace_apc_downsample(fake, 1000, 1000, fake, 10, 10, None)
-    assert st == 2
 
 
 def test_workspace_sizes_monotone():

@@ -176,20 +176,30 @@ def test_resize_parity(shape, out):
 
 @pytest.mark.parametrize("case", range(6))
 def test_resize_random_shapes(case):
-    """Seeded random sizes: input sides 1-700, outputs from 1/32 of each side up to the side."""
+    """Seeded random sizes: input sides 1-700; in even cases outputs from 1/32 of each side up to
+    the side (the staged kernels), in odd cases shrink factors drawn log-uniformly in [1, 300]
+    per side (beyond 32x the per-pixel kernel runs)."""
     rng = np.random.default_rng(400 + case)
     H, W = int(rng.integers(1, 701)), int(rng.integers(1, 701))
-    oh = int(rng.integers(max(1, -(-H // 32)), H + 1))
-    ow = int(rng.integers(max(1, -(-W // 32)), W + 1))
+    if case % 2:
+        oh = min(H, max(1, round(H / 10 ** rng.uniform(0, np.log10(300)))))
+        ow = min(W, max(1, round(W / 10 ** rng.uniform(0, np.log10(300)))))
+    else:
+        oh = int(rng.integers(max(1, -(-H // 32)), H + 1))
+        ow = int(rng.integers(max(1, -(-W // 32)), W + 1))
     img = rng.integers(0, 256, size=(H, W, 3), dtype=np.uint8)
     _check_resize(img, oh, ow)
 
 
-def test_resize_rejects_shrink_beyond_32x():
-    from paper_2608_27206_amd import pace
-    img = wl.make_image(3, 64, 64)
-    with pytest.raises(pace.PaceError, match="shrink factor"):
-        pace.apc_downsample(dev_u8(img), 1, 1)
+@pytest.mark.parametrize("shape,out", [((64, 64), (1, 1)), ((700, 500), (10, 7)), ((300, 2000), (5, 40)),
+                                       ((1000, 40), (1, 1)), ((90, 4000), (80, 30)), ((2156, 3836), (20, 30))])
+def test_resize_beyond_32x(shape, out):
+    """Shrinks beyond 32x per side (one side or both; down to a single pixel), per output pixel
+    from memory, against the oracle."""
+    rng = np.random.default_rng(shape[0] * 7 + shape[1])
+    img = rng.integers(0, 256, size=(*shape, 3), dtype=np.uint8)
+    img[: shape[0] // 2] //= 2
+    _check_resize(img, *out)
 
 
 # ---------------------------------------------------------------- caller-supplied embeddings
