@@ -336,7 +336,8 @@ size_t pace_ddae_select_workspace_size(int nv_total, int nseg);
  *             LLM-order visual token.
  *   llm_mass  fp32 [Hl, nv_total]: S_llm of token i = sum_h llm_mass[h, i], min-max per image.
  *   nv_host   int [B] (HOST): visual tokens per image; keep_host int [B] (HOST): K_b,
- *             0 <= K_b <= nv_host[b].  B <= PACE_MAX_SEGMENTS.
+ *             0 <= K_b <= nv_host[b].  Any B >= 1: a batch of more than PACE_MAX_SEGMENTS
+ *             images runs as consecutive launches of at most that many.
  *   mode      0: (w_llm, w_vis) = softmax([sigma_llm, sigma_vis] / tau), sigma = population
  *             std of each normalised map; 1: fixed (w_llm_fixed, 1 - w_llm_fixed).
  *   S_final = w_llm * S_llm + w_vis * S_vis.  Top-K per image: highest scores, ties to

@@ -722,7 +722,9 @@ pace_status_t run_select(SelectParams& p, const void* hidden, size_t row_bytes, 
     pace_status_t st = check_launch("ddae_token_maps");
     if (st != PACE_OK) return st;
   }
-  const int ktot = p.cu_keep[p.B];
+  // kept rows of this launch: [cu_keep[0], cu_keep[B]) (offsets are global across launches)
+  const int kfirst = p.cu_keep[0];
+  const int ktot = p.cu_keep[p.B] - kfirst;
   if (fused) {
     // rows per select workgroup: at least 4, and about one workgroup per CU (256) for the
     // gather (a select workgroup's LDS, ~105 KB with 16 scores per thread down to ~57 KB
@@ -755,8 +757,9 @@ pace_status_t run_select(SelectParams& p, const void* hidden, size_t row_bytes, 
   if (hidden != nullptr && ktot > 0) {
     const int words = static_cast<int>(row_bytes / 16);
     hipLaunchKernelGGL(gather_rows, dim3(ktot), dim3(256), 0, stream,
-                       static_cast<const uint4*>(hidden), p.idx, static_cast<uint4*>(out), ktot,
-                       words, p.nv_total);
+                       static_cast<const uint4*>(hidden), p.idx + kfirst,
+                       static_cast<uint4*>(out) + static_cast<long long>(kfirst) * words, ktot, words,
+                       p.nv_total);
     st = check_launch("gather_rows");
     if (st != PACE_OK) return st;
   }
@@ -825,8 +828,7 @@ pace_status_t pace_ddae_select_varlen(const float* vis_mass, int Hv, int merge,
                                       size_t row_bytes, int32_t* idx_out, float* score_out,
                                       float* fuse_out, void* out, void* workspace,
                                       size_t workspace_bytes, hipStream_t stream) {
-  PACE_REQUIRE(B >= 1 && B <= PACE_MAX_SEGMENTS, "pace_ddae_select: B=%d not in [1, %d]", B,
-               PACE_MAX_SEGMENTS);
+  PACE_REQUIRE(B >= 1, "pace_ddae_select: B=%d must be >= 1", B);
   PACE_REQUIRE(nv_host && keep_host, "pace_ddae_select: null host count arrays");
   PACE_REQUIRE(Hv >= 1 && Hl >= 1 && merge >= 1, "pace_ddae_select: Hv=%d Hl=%d merge=%d", Hv, Hl,
                merge);
@@ -834,18 +836,17 @@ pace_status_t pace_ddae_select_varlen(const float* vis_mass, int Hv, int merge,
   PACE_REQUIRE(mode == 1 || (tau > 0.f && isfinite(tau)), "pace_ddae_select: tau must be > 0");
   PACE_REQUIRE(vis_mass && llm_mass && idx_out, "pace_ddae_select: null device pointer");
   SelectParams p{};
-  p.cu_nv[0] = 0;
-  p.cu_keep[0] = 0;
+  std::vector<int> cu_nv(B + 1, 0), cu_keep(B + 1, 0);
   for (int b = 0; b < B; ++b) {
     PACE_REQUIRE(nv_host[b] >= 1, "pace_ddae_select: image %d has %d tokens", b, nv_host[b]);
     PACE_REQUIRE(keep_host[b] >= 0 && keep_host[b] <= nv_host[b],
                  "pace_ddae_select: K=%d outside [0, %d] for image %d", keep_host[b], nv_host[b], b);
-    PACE_REQUIRE(static_cast<long long>(p.cu_nv[b]) + nv_host[b] < (1ll << 30),
+    PACE_REQUIRE(static_cast<long long>(cu_nv[b]) + nv_host[b] < (1ll << 30),
                  "pace_ddae_select: too many tokens");
-    p.cu_nv[b + 1] = p.cu_nv[b] + nv_host[b];
-    p.cu_keep[b + 1] = p.cu_keep[b] + keep_host[b];
+    cu_nv[b + 1] = cu_nv[b] + nv_host[b];
+    cu_keep[b + 1] = cu_keep[b] + keep_host[b];
   }
-  const int nv_total = p.cu_nv[B];
+  const int nv_total = cu_nv[B];
   PACE_REQUIRE(merge != 4 || aligned16(vis_mass), "pace_ddae_select: vis_mass must be 16-byte aligned");
   if (hidden != nullptr) {
     PACE_REQUIRE(out != nullptr, "pace_ddae_select: out is null while hidden is given");
@@ -862,7 +863,7 @@ pace_status_t pace_ddae_select_varlen(const float* vis_mass, int Hv, int merge,
     pace_status_t chk = copy_to_host(perm.data(), vis_perm, nv_total, stream);
     if (chk != PACE_OK) return chk;
     for (int b = 0; b < B; ++b)
-      for (int i = p.cu_nv[b]; i < p.cu_nv[b + 1]; ++i)
+      for (int i = cu_nv[b]; i < cu_nv[b + 1]; ++i)
         PACE_REQUIRE(perm[i] >= 0 && perm[i] < nv_host[b],
                      "pace_ddae_select: vis_perm[%d] = %d outside [0, %d) for image %d", i, perm[i], nv_host[b], b);
   }
@@ -880,9 +881,25 @@ pace_status_t pace_ddae_select_varlen(const float* vis_mass, int Hv, int merge,
   p.scores_in = nullptr;
   p.idx = idx_out;
   p.vis_stride = static_cast<long long>(nv_total) * merge;
-  p.Hv = Hv; p.merge = merge; p.Hl = Hl; p.B = B; p.nv_total = nv_total;
+  p.Hv = Hv; p.merge = merge; p.Hl = Hl; p.nv_total = nv_total;
   p.mode = mode; p.tau = tau; p.w_llm_fixed = w_llm_fixed;
-  return run_select(p, hidden, row_bytes, out, stream, true);
+  // Images are independent: a batch of more than PACE_MAX_SEGMENTS images runs as consecutive
+  // launches of at most that many (the offsets travel in the kernel arguments).  Every kernel
+  // indexes tokens and kept rows by their global offsets, so a launch takes its images' slice
+  // of cu_nv / cu_keep unchanged; only the per-image fusion weights are indexed per launch.
+  for (int b0 = 0; b0 < B; b0 += PACE_MAX_SEGMENTS) {
+    const int nb = B - b0 < PACE_MAX_SEGMENTS ? B - b0 : PACE_MAX_SEGMENTS;
+    SelectParams q = p;
+    for (int j = 0; j <= nb; ++j) {
+      q.cu_nv[j] = cu_nv[b0 + j];
+      q.cu_keep[j] = cu_keep[b0 + j];
+    }
+    q.B = nb;
+    q.fuse = p.fuse + 4 * b0;
+    const pace_status_t st = run_select(q, hidden, row_bytes, out, stream, true);
+    if (st != PACE_OK) return st;
+  }
+  return PACE_OK;
 }
 
 pace_status_t pace_ddae_select(const float* vis_mass, int Hv, int merge, const int32_t* vis_perm,
@@ -905,8 +922,7 @@ pace_status_t pace_ddae_select_varlen_noalloc(const float* vis_mass, int Hv, int
                                               float tau, float w_llm_fixed, const void* hidden,
                                               size_t row_bytes, int32_t* idx_out, float* score_out,
                                               float* fuse_out, void* out, hipStream_t stream) {
-  PACE_REQUIRE(B >= 1 && B <= PACE_MAX_SEGMENTS, "pace_ddae_select_varlen_noalloc: B=%d not in [1, %d]", B,
-               PACE_MAX_SEGMENTS);
+  PACE_REQUIRE(B >= 1, "pace_ddae_select_varlen_noalloc: B=%d must be >= 1", B);
   PACE_REQUIRE(nv_host && keep_host, "pace_ddae_select_varlen_noalloc: null host count arrays");
   long long nv_total = 0;
   for (int b = 0; b < B; ++b) {

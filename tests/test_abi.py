@@ -161,6 +161,6 @@ def test_noalloc_select_rejects_more_than_its_scratch():
     st = L.pace_ddae_select_varlen_noalloc(null, 16, 4, null, null, 28, 1, one(0), one(0), 0, 0.5, 0.5,
                                            null, 0, null, null, null, null, null)
     assert st == 1
-    st = L.pace_ddae_select_varlen_noalloc(null, 16, 4, null, null, 28, 65, one(5), one(1), 0, 0.5, 0.5,
+    st = L.pace_ddae_select_varlen_noalloc(null, 16, 4, null, null, 28, 0, one(5), one(1), 0, 0.5, 0.5,
                                            null, 0, null, null, null, null, null)
     assert st == 1

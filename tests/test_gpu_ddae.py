@@ -179,6 +179,44 @@ def test_determinism():
     np.testing.assert_array_equal(host(r1[1]), host(r2[1]))
 
 
+@pytest.mark.parametrize("big", [False, True])
+def test_varlen_more_images_than_one_launch(big):
+    """150 images in one call (three launches of at most 64 images; one image past the
+    register-resident size when `big`, so its launch takes the general path), against the
+    oracle per image: scores, fusion weights, kept sets and the gathered rows."""
+    from paper_2608_27206_amd import pace
+    import torch
+    import torch as t
+    rs = np.random.default_rng(150 + big)
+    nvs = [int(x) for x in rs.integers(1, 400, size=150)]
+    if big:
+        nvs[100] = 17000
+    keeps = [oddae.keep_count(float(r), n) for r, n in zip(rs.uniform(0.0, 1.0, size=150), nvs)]
+    nt = sum(nvs)
+    say(f"varlen 150 images, {nt} tokens, keep {sum(keeps)}")
+    vis = rs.gamma(0.5, size=(2, nt)).astype(np.float32)
+    llm = rs.gamma(0.3, size=(3, nt)).astype(np.float32)
+    hidden = wl.random_bf16(nt, (nt, 64))
+    idx, sc, fz, out = pace.ddae_select(dev_f32(vis), 1, None, dev_f32(llm), nvs, keeps,
+                                        mode=0, hidden=dev_bf16(hidden))
+    torch.cuda.synchronize()
+    idx, sc, fz = host(idx), host(sc), host(fz)
+    assert idx.size == sum(keeps)
+    off = koff = 0
+    for b, (n, K) in enumerate(zip(nvs, keeps)):
+        S_ref, st = oddae.fuse(vis[:, off:off + n].astype(np.float64),
+                               llm[:, off:off + n].astype(np.float64), 1, None, 0)
+        np.testing.assert_allclose(sc[off:off + n], S_ref, atol=1e-5)
+        np.testing.assert_allclose(fz[b], st, atol=1e-5)
+        got = idx[koff:koff + K] - off
+        ok, msg = kept_sets_agree(got, oddae.topk_indices(S_ref, K), S_ref)
+        assert ok, (b, msg)
+        np.testing.assert_array_equal(got, oddae.topk_indices(sc[off:off + n], K))
+        off += n
+        koff += K
+    np.testing.assert_array_equal(out.view(t.int16).cpu().numpy().view(np.uint16), hidden[idx])
+
+
 def test_varlen_keep_none_all_and_many_rows():
     """Images whose K is 0, all of the image, or spread over many gather workgroups, in one
     batch; and a batch with an image past the register-resident size (every image then takes
