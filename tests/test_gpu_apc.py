@@ -192,7 +192,8 @@ def test_resize_random_shapes(case):
 
 
 @pytest.mark.parametrize("shape,out", [((64, 64), (1, 1)), ((700, 500), (10, 7)), ((300, 2000), (5, 40)),
-                                       ((1000, 40), (1, 1)), ((90, 4000), (80, 30)), ((2156, 3836), (20, 30))])
+                                       ((1000, 40), (1, 1)), ((90, 4000), (80, 30)), ((2156, 3836), (20, 30)),
+                                       ((1, 3000), (1, 20)), ((3000, 1), (2, 1)), ((33, 33), (1, 33))])
 def test_resize_beyond_32x(shape, out):
     """Shrinks beyond 32x per side (one side or both; down to a single pixel), per output pixel
     from memory, against the oracle."""
