@@ -231,7 +231,7 @@ def build_workload_step(a, torch, np, pace, wl, dev):
         imgs = [torch.from_numpy(im).to(dev) for im in w.images]
         ws_apc = [torch.empty(pace.lib().pace_apc_density_workspace_size(im.shape[0], im.shape[1], 14),
                               dtype=torch.uint8, device=dev) for im in w.images]
-        rhos = [torch.empty(4, **f32) for _ in w.images]
+        rhos = [torch.empty(3, **f32) for _ in w.images]
         dps = [torch.empty((im.shape[0] // 14) * (im.shape[1] // 14), **f32) for im in w.images]
         # the resize size and the per-image K follow the density: read once from the GPU here (a caller
         # reads rho back before sizing the resize); the timed steps reuse these sizes
@@ -587,7 +587,7 @@ def measure_preview(pace, wl, img, L, stream, reps=3):
     D, F = wdev["dim"], wdev["ffn"]
     out = torch.empty((N, D), dtype=torch.bfloat16, device=dev)
     ws = torch.empty(pace.lib().pace_apc_preview_workspace_size(N, D, F, 14), dtype=torch.uint8, device=dev)
-    rho = torch.empty(4, dtype=torch.float32, device=dev)
+    rho = torch.empty(3, dtype=torch.float32, device=dev)
     dd = torch.empty(N, dtype=torch.float32, device=dev)
     wsd = torch.empty(pace.lib().pace_apc_density_features_workspace_size(N, D), dtype=torch.uint8, device=dev)
 

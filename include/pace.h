@@ -105,7 +105,7 @@ size_t pace_apc_density_workspace_size(int H, int W, int patch);
  *             n_tail = max(1, pace_keep_count(tail_frac, N)).
  *   alpha, gamma   rho = alpha*rho_g + (1-alpha)*min(d_top/gamma, 1)  (0.6 and 1.5).
  *   d_out     fp32 [N] per-patch distance d_i = ||T_i - c_hat||, or NULL.
- *   rho_out   fp32 [4]: rho_g, rho_d, rho, phi.
+ *   rho_out   fp32 [3]: rho_g, rho_d, rho (phi of Eq. 1 is 1 - rho_g, Eq. 2).
  * Per-patch feature: the patch's 3*patch*patch pixels mapped to x/127.5 - 1 and
  * l2-normalised (a pixel preview; the paper's ViT-block preview needs weights).
  * phi (Eq. 1) is evaluated as ||mean_i T_i||^2, which equals the mean pairwise

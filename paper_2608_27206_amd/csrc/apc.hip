@@ -731,7 +731,6 @@ __global__ __launch_bounds__(1024) void apc_tail(const DensityParams p) {
     p.rho_out[0] = rho_g;
     p.rho_out[1] = rho_d;
     p.rho_out[2] = p.alpha * rho_g + (1.0f - p.alpha) * rho_d;
-    p.rho_out[3] = p.stats[0];
   }
 }
 

@@ -141,14 +141,14 @@ def apc_target_size(rho: float, H: int, W: int, min_pixels: float, max_pixels: f
 def apc_density(img: torch.Tensor, patch: int = 14, tail_frac: float = 0.10, alpha: float = 0.6,
                 gamma: float = 1.5, d_out: Optional[torch.Tensor] = None,
                 rho_out: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None):
-    """img: uint8 [H, W, 3] on the GPU.  Returns (rho [4] = rho_g, rho_d, rho, phi; d [N])."""
+    """img: uint8 [H, W, 3] on the GPU.  Returns (rho [3] = rho_g, rho_d, rho; d [N]); phi = 1 - rho_g."""
     H, W, _ = img.shape
     N = (H // patch) * (W // patch)
     dev = img.device
     if d_out is None:
         d_out = torch.empty(N, dtype=torch.float32, device=dev)
     if rho_out is None:
-        rho_out = torch.empty(4, dtype=torch.float32, device=dev)
+        rho_out = torch.empty(3, dtype=torch.float32, device=dev)
     need = lib().pace_apc_density_workspace_size(H, W, patch)
     if workspace is None:
         workspace = _ws(need, dev)
@@ -161,7 +161,7 @@ def apc_density(img: torch.Tensor, patch: int = 14, tail_frac: float = 0.10, alp
 def apc_density_features(feat: torch.Tensor, tail_frac: float = 0.10, alpha: float = 0.6,
                          gamma: float = 1.5, d_out: Optional[torch.Tensor] = None,
                          rho_out: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None):
-    """feat: bf16 [N, D] preview embeddings on the GPU.  Returns (rho [4] = rho_g, rho_d, rho, phi;
+    """feat: bf16 [N, D] preview embeddings on the GPU.  Returns (rho [3] = rho_g, rho_d, rho;
     d [N])."""
     if feat.dtype != torch.bfloat16 or feat.dim() != 2:
         raise PaceError("feat must be a 2-D bfloat16 tensor")
@@ -170,7 +170,7 @@ def apc_density_features(feat: torch.Tensor, tail_frac: float = 0.10, alpha: flo
     if d_out is None:
         d_out = torch.empty(N, dtype=torch.float32, device=dev)
     if rho_out is None:
-        rho_out = torch.empty(4, dtype=torch.float32, device=dev)
+        rho_out = torch.empty(3, dtype=torch.float32, device=dev)
     if workspace is None:
         workspace = _ws(lib().pace_apc_density_features_workspace_size(N, D), dev)
     _check(lib().pace_apc_density_features(_ptr(feat), N, D, float(tail_frac), float(alpha),
@@ -205,7 +205,7 @@ def apc_pixel_features(img: torch.Tensor, kind: int, patch: int = 14,
 def apc_pixel_density(img: torch.Tensor, kind: int, patch: int = 14, tail_frac: float = 0.10,
                       alpha: float = 0.6, gamma: float = 1.5, d_out: Optional[torch.Tensor] = None,
                       rho_out: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None):
-    """APC density with a pixel-statistic preview.  Returns (rho [4], d [N])."""
+    """APC density with a pixel-statistic preview.  Returns (rho [3]: rho_g, rho_d, rho; d [N])."""
     if img.dtype != torch.uint8 or img.dim() != 3 or img.shape[2] != 3:
         raise PaceError("img must be a uint8 [H, W, 3] tensor")
     H, W, _ = img.shape
@@ -214,7 +214,7 @@ def apc_pixel_density(img: torch.Tensor, kind: int, patch: int = 14, tail_frac: 
     if d_out is None:
         d_out = torch.empty(max(N, 1), dtype=torch.float32, device=dev)
     if rho_out is None:
-        rho_out = torch.empty(4, dtype=torch.float32, device=dev)
+        rho_out = torch.empty(3, dtype=torch.float32, device=dev)
     if workspace is None:
         workspace = _ws(lib().pace_apc_pixel_density_workspace_size(H, W, patch, kind), dev)
     _check(lib().pace_apc_pixel_density(_ptr(img), H, W, patch, kind, float(tail_frac), float(alpha),

@@ -98,3 +98,10 @@ def load_e2e_golden(config_id, workload):
         h.update(np.ascontiguousarray(a).tobytes())
     assert str(z[c + "sha"]) == h.hexdigest(), "workload generator changed since the golden file"
     return z[c + "nv"], z[c + "keep"], z[c + "S"].astype(np.float64), z[c + "idx"].astype(np.int64)
+
+
+def rho4(rho) -> np.ndarray:
+    """The density call's (rho_g, rho_d, rho) with phi = 1 - rho_g (Eq. 2) appended, for
+    comparison with the oracle's (rho_g, rho_d, rho, phi)."""
+    r = np.asarray(host(rho) if not isinstance(rho, np.ndarray) else rho, dtype=np.float64)
+    return np.array([r[0], r[1], r[2], 1.0 - r[0]])

@@ -8,7 +8,7 @@ import pytest
 
 from oracle import apc as oapc
 from paper_2608_27206_amd import workloads as wl
-from tests.gpu_util import dev_u8, host, say
+from tests.gpu_util import dev_u8, host, rho4, say
 
 pytestmark = pytest.mark.gpu
 
@@ -26,7 +26,7 @@ def _check_density(img, tail=0.1):
     rho, d = _density(img, tail)
     ref = oapc.apc_density(img, 14, tail)
     np.testing.assert_allclose(d, ref["d"], atol=1e-4)
-    np.testing.assert_allclose(rho, [ref["rho_g"], ref["rho_d"], ref["rho"], ref["phi"]], atol=1e-4)
+    np.testing.assert_allclose(rho4(rho), [ref["rho_g"], ref["rho_d"], ref["rho"], ref["phi"]], atol=1e-4)
     return rho
 
 
@@ -51,7 +51,7 @@ def test_density_odd_byte_count():
     torch.cuda.synchronize()
     ref = oapc.apc_density(img, 7, 0.1)
     np.testing.assert_allclose(host(d), ref["d"], atol=1e-4)
-    np.testing.assert_allclose(host(rho), [ref["rho_g"], ref["rho_d"], ref["rho"], ref["phi"]], atol=1e-4)
+    np.testing.assert_allclose(rho4(host(rho)), [ref["rho_g"], ref["rho_d"], ref["rho"], ref["phi"]], atol=1e-4)
 
 
 def test_density_more_patches_than_the_register_tail():
@@ -67,7 +67,7 @@ def test_density_more_patches_than_the_register_tail():
     d_ref = oapc.detail_distances(T, oapc.background_direction(T))
     rho_d = min(oapc.tail_mean(d_ref, 0.1) / oapc.GAMMA, 1.0)
     np.testing.assert_allclose(d, d_ref, atol=1e-4)
-    np.testing.assert_allclose(rho, [1 - phi, rho_d, oapc.ALPHA * (1 - phi) + (1 - oapc.ALPHA) * rho_d, phi],
+    np.testing.assert_allclose(rho4(rho), [1 - phi, rho_d, oapc.ALPHA * (1 - phi) + (1 - oapc.ALPHA) * rho_d, phi],
                                atol=1e-4)
 
 
@@ -107,7 +107,7 @@ def test_density_tail_ties_in_each_ranking_path(n_b):
     assert len(np.unique(d[kinds])) == 1 and d[kinds][0] > d[~kinds][0]
     np.testing.assert_allclose(d, ref["d"], atol=1e-4)
     np.testing.assert_allclose(rho[1] * 100.0, ref["d_top"], atol=1e-5)
-    np.testing.assert_allclose(rho, [ref["rho_g"], ref["rho_d"], ref["rho"], ref["phi"]], atol=1e-4)
+    np.testing.assert_allclose(rho4(rho), [ref["rho_g"], ref["rho_d"], ref["rho"], ref["phi"]], atol=1e-4)
 
 
 @pytest.mark.parametrize("case", range(6))
@@ -127,7 +127,7 @@ def test_density_random_shapes(case):
     torch.cuda.synchronize()
     ref = oapc.apc_density(img, P, tail)
     np.testing.assert_allclose(host(d), ref["d"], atol=1e-4)
-    np.testing.assert_allclose(host(rho), [ref["rho_g"], ref["rho_d"], ref["rho"], ref["phi"]], atol=1e-4)
+    np.testing.assert_allclose(rho4(host(rho)), [ref["rho_g"], ref["rho_d"], ref["rho"], ref["phi"]], atol=1e-4)
 
 
 @pytest.mark.parametrize("patch,gh,gw", [(1, 40, 37), (2, 23, 31), (5, 17, 29), (3, 64, 70), (11, 9, 67)])
@@ -145,7 +145,7 @@ def test_density_small_and_odd_patches(patch, gh, gw):
     torch.cuda.synchronize()
     ref = oapc.apc_density(img, patch, 0.1)
     np.testing.assert_allclose(host(d), ref["d"], atol=1e-4)
-    np.testing.assert_allclose(host(rho), [ref["rho_g"], ref["rho_d"], ref["rho"], ref["phi"]], atol=1e-4)
+    np.testing.assert_allclose(rho4(host(rho)), [ref["rho_g"], ref["rho_d"], ref["rho"], ref["phi"]], atol=1e-4)
 
 
 def _check_resize(img, oh, ow):
@@ -213,7 +213,7 @@ def _check_features(bits, tail=0.1, atol=1e-4):
     torch.cuda.synchronize()
     ref = oapc.embedding_density(wl.bf16_bits_to_f64(bits), tail)
     np.testing.assert_allclose(host(d), ref["d"], atol=atol)
-    np.testing.assert_allclose(host(rho), [ref["rho_g"], ref["rho_d"], ref["rho"], ref["phi"]], atol=atol)
+    np.testing.assert_allclose(rho4(host(rho)), [ref["rho_g"], ref["rho_d"], ref["rho"], ref["phi"]], atol=atol)
     return host(rho), host(d)
 
 
@@ -240,7 +240,7 @@ def test_density_features_opposite_identical_and_zero_rows():
     rho, d = _check_features(wl.f32_to_bf16_bits(x))
     assert abs(rho[0] - 1.0) < 1e-5 and d[100] == 0.0
     rho, d = _check_features(wl.f32_to_bf16_bits(np.tile(x[:1], (33, 1))))
-    assert abs(rho[3] - 1.0) < 1e-5 and np.max(d) < 1e-3
+    assert abs(rho[0]) < 1e-5 and np.max(d) < 1e-3   # phi = 1 - rho_g = 1
 
 
 def test_density_features_beyond_the_register_tail():
@@ -279,7 +279,7 @@ def test_pixel_density_parity(kind, shape):
     torch.cuda.synchronize()
     ref = oapc.pixel_density(img, 14, kind)
     np.testing.assert_allclose(host(d), ref["d"], atol=1e-4)
-    np.testing.assert_allclose(host(rho), [ref["rho_g"], ref["rho_d"], ref["rho"], ref["phi"]], atol=1e-4)
+    np.testing.assert_allclose(rho4(host(rho)), [ref["rho_g"], ref["rho_d"], ref["rho"], ref["phi"]], atol=1e-4)
 
 
 def test_pixel_features_full_frame():
@@ -305,11 +305,11 @@ def test_pixel_density_flat_and_tiled():
     for kind in (2, 3):
         rho, d = pace.apc_pixel_density(dev_u8(flat), kind, 14)
         torch.cuda.synchronize()
-        assert host(rho)[3] == 0.0 and host(rho)[0] == 1.0 and np.all(host(d) == 0)
+        assert host(rho)[0] == 1.0 and np.all(host(d) == 0)   # phi = 0
     tile = np.random.default_rng(3).integers(0, 256, size=(14, 14, 3), dtype=np.uint8)
     rho, d = pace.apc_pixel_density(dev_u8(np.tile(tile, (4, 5, 1))), 0, 14)
     torch.cuda.synchronize()
-    assert abs(host(rho)[3] - 1.0) < 1e-5 and np.max(host(d)) < 1e-3
+    assert abs(host(rho)[0]) < 1e-5 and np.max(host(d)) < 1e-3
 
 
 def test_pixel_rejects_bad_kind_and_patch():
@@ -338,7 +338,7 @@ def test_images_on_parallel_streams_match_serial():
             H, W = im.shape[:2]
             out.append({"ws": torch.empty(lib.pace_apc_density_workspace_size(H, W, 14), dtype=torch.uint8, device="cuda"),
                         "d": torch.empty((H // 14) * (W // 14), dtype=torch.float32, device="cuda"),
-                        "rho": torch.empty(4, dtype=torch.float32, device="cuda"),
+                        "rho": torch.empty(3, dtype=torch.float32, device="cuda"),
                         "small": torch.empty((H // 2, W // 2, 3), dtype=torch.uint8, device="cuda")})
         return out
 

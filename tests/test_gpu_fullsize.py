@@ -18,7 +18,7 @@ from oracle import apc as oapc
 from oracle import attention as oatt
 from oracle import ddae as oddae
 from paper_2608_27206_amd import workloads as wl
-from tests.gpu_util import (dev_bf16, dev_f32, dev_i32, dev_u8, host, host_bf16_to_f64,
+from tests.gpu_util import (dev_bf16, dev_f32, dev_i32, dev_u8, host, host_bf16_to_f64, rho4,
                             kept_sets_agree, load_e2e_golden, mass_ok, oracle_mass_parallel, say)
 
 pytestmark = pytest.mark.gpu
@@ -201,7 +201,7 @@ def test_frame4k_apc(w4k):
     T = oapc.l2_normalise(oapc.patch_features(img))
     d_ref = oapc.detail_distances(T, oapc.background_direction(T))
     np.testing.assert_allclose(host(d), d_ref, atol=1e-4)
-    np.testing.assert_allclose(host(rho), [gold["rho_g"], gold["rho_d"], gold["rho"], gold["phi"]], atol=1e-4)
+    np.testing.assert_allclose(rho4(host(rho)), [gold["rho_g"], gold["rho_d"], gold["rho"], gold["phi"]], atol=1e-4)
     # at gamma = 1.5 rho_d is clamped at 1 (the tail mean is 1.92); above the tail mean it is
     # d_top / gamma, which pins the frame's tail mean itself (the 4,220 largest of 42,196 d_i)
     gamma = 2.5
@@ -301,7 +301,7 @@ def test_varlen_apc_keep_and_select(wvar):
         rho, _ = pace.apc_density(dev_u8(img), 14, 0.10, 0.6, 1.5)
         torch.cuda.synchronize()
         r = host(rho)
-        np.testing.assert_allclose(r, [g["rho_g"], g["rho_d"], g["rho"], g["phi"]], atol=1e-4)
+        np.testing.assert_allclose(rho4(r), [g["rho_g"], g["rho_d"], g["rho"], g["phi"]], atol=1e-4)
         keeps_gpu.append(pace.keep_from_density(float(r[2]), nv))
         keeps_ref.append(oddae.keep_from_density(g["rho"], nv))
     assert keeps_gpu == keeps_ref

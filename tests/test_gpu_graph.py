@@ -46,7 +46,7 @@ def _outputs(torch, inp):
     H, Hq, Ntot = inp["q"].shape[1], inp["pq"].shape[1], inp["pq"].shape[0]
     f32 = dict(dtype=torch.float32, device=dev)
     return {
-        "d": torch.empty(N, **f32), "rho": torch.empty(4, **f32),
+        "d": torch.empty(N, **f32), "rho": torch.empty(3, **f32),
         "small": torch.empty((224, 224, 3), dtype=torch.uint8, device=dev),
         "o_win": torch.empty_like(inp["q"]), "lse_win": torch.empty((H, N), **f32),
         "mass_win": torch.empty((H, N), **f32),
