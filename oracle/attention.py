@@ -100,12 +100,13 @@ def vit_attention(q, k, v, cu_seqlens, scale: float, with_mass: bool = True):
     return O, LSE, mass
 
 
-def prefill_attention(q, k, v, cu_seqlens, vis_len, mq_start, mq_len, scale: float):
+def prefill_attention(q, k, v, cu_seqlens, vis_len, mq_start, mq_len, scale: float, vis_start=None):
     """Causal grouped-query attention over packed sequences, with visual-key mass.
 
-    Sequence b spans rows [cu[b], cu[b+1]); its first vis_len[b] tokens are visual.  The mass
-    of visual key j of sequence b sums P over the query rows [mq_start[b], mq_start[b]+mq_len[b])
-    of that sequence (positions relative to the sequence start).
+    Sequence b spans rows [cu[b], cu[b+1]); its tokens [vis_start[b], vis_start[b] + vis_len[b])
+    are visual (vis_start None: the first vis_len[b]).  The mass of visual key j of sequence b
+    sums P over the query rows [mq_start[b], mq_start[b]+mq_len[b]) of that sequence (positions
+    relative to the sequence start).
 
     Returns O [Ntot, Hq, d], LSE [Hq, Ntot], mass [Hq, sum vis_len] (sequences concatenated)."""
     Ntot, hq, d = q.shape
@@ -120,7 +121,8 @@ def prefill_attention(q, k, v, cu_seqlens, vis_len, mq_start, mq_len, scale: flo
                                       mass_rows=np.arange(st, st + ln))
         O[a:b] = o
         LSE[:, a:b] = lse
-        masses.append(m[:, : int(vis_len[s])])
+        vs = 0 if vis_start is None else int(vis_start[s])
+        masses.append(m[:, vs: vs + int(vis_len[s])])
     mass = np.concatenate(masses, axis=1) if masses else np.zeros((hq, 0))
     return O, LSE, mass
 

@@ -69,6 +69,25 @@ def test_prefill_gqa_causal_brute_force():
     np.testing.assert_allclose(M, expect_mass, atol=1e-12)
 
 
+def test_prefill_visual_tokens_after_a_text_prefix_brute_force():
+    """Visual tokens at an offset (a system prompt before the image): the mass of visual key j
+    of sequence b is column vis_start[b] + j of the brute-force mass."""
+    rs = np.random.default_rng(5)
+    cu = [0, 9, 20]
+    vis_start, vis = [2, 3], [4, 5]
+    q = rs.standard_normal((20, 4, 3))
+    k = rs.standard_normal((20, 2, 3))
+    v = rs.standard_normal((20, 2, 3))
+    mq_start, mq_len = [6, 8], [3, 3]
+    O, L, M = oatt.prefill_attention(q, k, v, cu, vis, mq_start, mq_len, 0.5, vis_start=vis_start)
+    segs = [(0, 9), (9, 20)]
+    Ob, Lb, Mb = _brute(q, k, v, segs, True, 0.5, lambda a, b: range(a + (6 if a == 0 else 8), b))
+    np.testing.assert_allclose(O, Ob, atol=1e-12)
+    np.testing.assert_allclose(L, Lb, atol=1e-12)
+    expect_mass = np.concatenate([Mb[:, 2:6], Mb[:, 12:17]], axis=1)
+    np.testing.assert_allclose(M, expect_mass, atol=1e-12)
+
+
 def test_against_torch_sdpa_float64():
     torch = pytest.importorskip("torch")
     import torch.nn.functional as F
