@@ -298,7 +298,10 @@ size_t pace_prefill_attention_workspace_size(int Ntot, int Hq);
  *   q         bf16 [Ntot, Hq, d]; k, v bf16 [Ntot, Hkv, d]; d in {80, 128}; Hq % Hkv == 0;
  *             query head h uses KV head h / (Hq / Hkv).
  *   cu_seqlens int32 [B+1] (device): packed sequences, causal inside each (key <= query).
- *   vis_len   int32 [B] (device): the first vis_len[b] tokens of sequence b are visual.
+ *   vis_start int32 [B] (device) or NULL (= 0): sequence b's visual tokens are its tokens
+ *             [vis_start[b], vis_start[b] + vis_len[b]) (relative positions; a text prefix such
+ *             as a system prompt may come first).
+ *   vis_len   int32 [B] (device): number of visual tokens of sequence b.
  *   cu_vis    int32 [B+1] (device): offset of sequence b's visual keys in mass;
  *             nvis_total (host) = cu_vis[B], the row length of mass.
  *   mq_start, mq_len int32 [B] (device): mass sums P over query rows
@@ -307,12 +310,12 @@ size_t pace_prefill_attention_workspace_size(int Ntot, int Hq);
  *             give "Vision + Text"; the last row gives "Last".
  *   max_seqlen, max_vis_len, max_mq_len  host-side upper bounds.
  *   o         bf16 [Ntot, Hq, d]; lse fp32 [Hq, Ntot] or NULL (then the workspace holds it);
- *   mass      fp32 [Hq, nvis_total]: mass[h, cu_vis[b] + j] = sum_{i in rows_b} P_h[i, j],
+ *   mass      fp32 [Hq, nvis_total]: mass[h, cu_vis[b] + j] = sum_{i in rows_b} P_h[i, vis_start[b] + j],
  *             or NULL to skip the mass pass (vis_len, cu_vis, mq_* are then unused).
  */
 pace_status_t pace_prefill_attention_with_mass(
     const uint16_t* q, const uint16_t* k, const uint16_t* v, int Ntot, int Hq, int Hkv, int d,
-    const int32_t* cu_seqlens, int B, int max_seqlen, const int32_t* vis_len,
+    const int32_t* cu_seqlens, int B, int max_seqlen, const int32_t* vis_start, const int32_t* vis_len,
     const int32_t* cu_vis, int nvis_total, int max_vis_len, const int32_t* mq_start,
     const int32_t* mq_len,
     int max_mq_len, float scale, uint16_t* o, float* lse, float* mass, void* workspace,

@@ -1149,7 +1149,8 @@ struct MassParams {
   const float* lse;          // [Hq, Ntot]
   float* mass;               // [Hq, mass_stride]
   const int32_t* cu;         // [nseg + 1]
-  const int32_t* key_len;    // [nseg] keys receiving mass (prefix of the segment), or null = all
+  const int32_t* key_start;  // [nseg] first key receiving mass (relative), or null = 0
+  const int32_t* key_len;    // [nseg] keys receiving mass, or null = all from key_start
   const int32_t* q_start;    // [nseg] first querying row (relative), or null = 0
   const int32_t* q_len;      // [nseg] querying rows, or null = whole segment
   const int32_t* mass_off;   // [nseg] column offset of the segment's keys in mass, or null = cu[s]
@@ -1191,9 +1192,12 @@ __global__ __launch_bounds__(kThreads, (D == 80 && !CAUSAL) ? 3 : 2) void attn_m
   const int kt = rem - seg * p.nkt;
   const int s0 = p.cu[seg];
   const int L = p.cu[seg + 1] - s0;
-  const int klen = p.key_len ? p.key_len[seg] : L;
-  const int k0 = kt * kMassKeys;
-  if (k0 >= klen) return;
+  // keys [kst, kst + klen) of the segment receive mass
+  const int kst = p.key_start ? p.key_start[seg] : 0;
+  const int klen = p.key_len ? p.key_len[seg] : L - kst;
+  if (kt * kMassKeys >= klen) return;
+  const int k0 = kst + kt * kMassKeys;
+  const int kend = kst + klen;
   const int qs = p.q_start ? p.q_start[seg] : 0;
   const int ql = p.q_len ? p.q_len[seg] : L;
   const long long moff = p.mass_off ? p.mass_off[seg] : s0;
@@ -1207,7 +1211,7 @@ __global__ __launch_bounds__(kThreads, (D == 80 && !CAUSAL) ? 3 : 2) void attn_m
   // K fragments (A operand of S^T = K Q^T) for the wave's two 32-key sets; keys past the
   // receiving range load as zeros (their mass is never written)
   const auto rk = make_rsrc(p.k + static_cast<long long>(s0) * kvstride + kvh * D,
-                            static_cast<unsigned>((klen - 1) * kvstride + D) * 2u);
+                            static_cast<unsigned>((kend - 1) * kvstride + D) * 2u);
   bf16x8 kf[2][C::KC];
 #pragma unroll
   for (int ks = 0; ks < 2; ++ks) {
@@ -1406,7 +1410,7 @@ __global__ __launch_bounds__(kThreads, (D == 80 && !CAUSAL) ? 3 : 2) void attn_m
     for (int r = 0; r < 16; ++r) {
       if (c32 == r) {
         const int key = kw0 + ks * 32 + g * 4 + 8 * (r >> 2) + (r & 3);
-        if (key < klen) mrow[key] = macc[ks][r];
+        if (key < kend) mrow[key - kst] = macc[ks][r];
       }
     }
 }
@@ -1419,7 +1423,8 @@ template <int D>
 pace_status_t launch_attention(FwdParams fp, bool causal, int max_seglen, const MassParams* mp,
                                int nmass, hipStream_t stream) {
   if (!causal && mp != nullptr && nmass > 0 && max_seglen <= kWinMax && mp->mass_stride == fp.Ntot &&
-      mp->key_len == nullptr && mp->q_start == nullptr && mp->q_len == nullptr && mp->mass_off == nullptr) {
+      mp->key_start == nullptr && mp->key_len == nullptr && mp->q_start == nullptr && mp->q_len == nullptr &&
+      mp->mass_off == nullptr) {
     hipLaunchKernelGGL((attn_window<D>), dim3(fp.nseg * fp.Hq), dim3(kWinThreads), 0, stream, fp, mp->mass);
     return check_launch("attn_window");
   }
@@ -1566,7 +1571,7 @@ pace_status_t pace_vit_attention_mass(const uint16_t* q, const uint16_t* k, int 
 
 pace_status_t pace_prefill_attention_with_mass(
     const uint16_t* q, const uint16_t* k, const uint16_t* v, int Ntot, int Hq, int Hkv, int d,
-    const int32_t* cu_seqlens, int B, int max_seqlen, const int32_t* vis_len,
+    const int32_t* cu_seqlens, int B, int max_seqlen, const int32_t* vis_start, const int32_t* vis_len,
     const int32_t* cu_vis, int nvis_total, int max_vis_len, const int32_t* mq_start,
     const int32_t* mq_len, int max_mq_len, float scale, uint16_t* o, float* lse, float* mass,
     void* workspace, size_t workspace_bytes, hipStream_t stream) {
@@ -1599,8 +1604,9 @@ pace_status_t pace_prefill_attention_with_mass(
                                       "pace_prefill_attention_with_mass: cu_seqlens", stream);
     if (chk != PACE_OK) return chk;
     if (want_mass) {
-      std::vector<int32_t> cu(B + 1), vl(B), cv(B + 1), ms(B), ml(B);
-      if ((chk = copy_to_host(cu.data(), cu_seqlens, B + 1, stream)) != PACE_OK ||
+      std::vector<int32_t> cu(B + 1), vs(B, 0), vl(B), cv(B + 1), ms(B), ml(B);
+      if ((vis_start && (chk = copy_to_host(vs.data(), vis_start, B, stream)) != PACE_OK) ||
+          (chk = copy_to_host(cu.data(), cu_seqlens, B + 1, stream)) != PACE_OK ||
           (chk = copy_to_host(vl.data(), vis_len, B, stream)) != PACE_OK ||
           (chk = copy_to_host(cv.data(), cu_vis, B + 1, stream)) != PACE_OK ||
           (chk = copy_to_host(ms.data(), mq_start, B, stream)) != PACE_OK ||
@@ -1609,9 +1615,10 @@ pace_status_t pace_prefill_attention_with_mass(
       PACE_REQUIRE(cv[0] == 0 && cv[B] <= nvis_total, "pace_prefill_attention_with_mass: cu_vis range");
       for (int b = 0; b < B; ++b) {
         const int L = cu[b + 1] - cu[b];
-        PACE_REQUIRE(vl[b] >= 0 && vl[b] <= L && vl[b] <= max_vis_len && cv[b + 1] - cv[b] == vl[b],
-                     "pace_prefill_attention_with_mass: sequence %d: vis_len %d, cu_vis step %d, length %d", b,
-                     vl[b], cv[b + 1] - cv[b], L);
+        PACE_REQUIRE(vs[b] >= 0 && vl[b] >= 0 && vs[b] + vl[b] <= L && vl[b] <= max_vis_len &&
+                         cv[b + 1] - cv[b] == vl[b],
+                     "pace_prefill_attention_with_mass: sequence %d: visual tokens [%d, %d + %d), cu_vis step %d, "
+                     "length %d", b, vs[b], vs[b], vl[b], cv[b + 1] - cv[b], L);
         PACE_REQUIRE(ms[b] >= 0 && ml[b] >= 0 && ml[b] <= max_mq_len && ms[b] + ml[b] <= L,
                      "pace_prefill_attention_with_mass: sequence %d: query rows [%d, %d + %d) outside [0, %d]",
                      b, ms[b], ms[b], ml[b], L);
@@ -1633,7 +1640,7 @@ pace_status_t pace_prefill_attention_with_mass(
   fp.scale_log2 = scale * kLog2e;
   MassParams mp{};
   mp.q = q; mp.k = k; mp.lse = lse_buf; mp.mass = mass; mp.cu = cu_seqlens;
-  mp.key_len = vis_len; mp.q_start = mq_start; mp.q_len = mq_len; mp.mass_off = cu_vis;
+  mp.key_start = vis_start; mp.key_len = vis_len; mp.q_start = mq_start; mp.q_len = mq_len; mp.mass_off = cu_vis;
   mp.mass_stride = nvis_total;
   mp.Ntot = Ntot; mp.Hq = Hq; mp.Hkv = Hkv; mp.group = Hq / Hkv;
   mp.nseg = B; mp.nkt = static_cast<int>(nkt);

@@ -56,7 +56,7 @@ _PROTOS = {
                                         c_float, c_void, c_void, c_void]),
     "pace_prefill_attention_workspace_size": (c_size, [c_int, c_int]),
     "pace_prefill_attention_with_mass": (c_int, [c_void, c_void, c_void, c_int, c_int, c_int, c_int,
-                                                 c_void, c_int, c_int, c_void, c_void, c_int, c_int,
+                                                 c_void, c_int, c_int, c_void, c_void, c_void, c_int, c_int,
                                                  c_void, c_void, c_int, c_float, c_void, c_void,
                                                  c_void, c_void, c_size, c_void]),
     "pace_ddae_select_workspace_size": (c_size, [c_int, c_int]),
@@ -362,9 +362,10 @@ def vit_attention_mass(q: torch.Tensor, k: torch.Tensor, cu_seqlens: torch.Tenso
 def prefill_attention_with_mass(q, k, v, cu_seqlens, max_seqlen: int, vis_len, cu_vis,
                                 nvis_total: int, max_vis_len: int, mq_start, mq_len,
                                 max_mq_len: int, scale: Optional[float] = None, want_mass=True,
-                                o=None, lse=None, mass=None, workspace=None):
+                                o=None, lse=None, mass=None, workspace=None, vis_start=None):
     """Causal GQA prefill.  q bf16 [Ntot, Hq, d]; k, v bf16 [Ntot, Hkv, d]; metadata int32 on the
-    GPU.  Returns (o, lse [Hq, Ntot], mass [Hq, nvis_total] or None)."""
+    GPU (vis_start None: visual tokens first).  Returns (o, lse [Hq, Ntot], mass [Hq, nvis_total]
+    or None)."""
     Ntot, Hq, d = q.shape
     Hkv = k.shape[1]
     dev = q.device
@@ -379,7 +380,7 @@ def prefill_attention_with_mass(q, k, v, cu_seqlens, max_seqlen: int, vis_len, c
         mass = None
     _check(lib().pace_prefill_attention_with_mass(
         _ptr(q), _ptr(k), _ptr(v), Ntot, Hq, Hkv, d, _ptr(cu_seqlens), cu_seqlens.numel() - 1,
-        int(max_seqlen), _ptr(vis_len), _ptr(cu_vis), int(nvis_total), int(max_vis_len),
+        int(max_seqlen), _ptr(vis_start), _ptr(vis_len), _ptr(cu_vis), int(nvis_total), int(max_vis_len),
         _ptr(mq_start), _ptr(mq_len), int(max_mq_len), float(scale), _ptr(o), _ptr(lse),
         _ptr(mass), _ptr(workspace), 0 if workspace is None else workspace.numel(), _stream()),
         "pace_prefill_attention_with_mass")

@@ -86,7 +86,7 @@ def test_errors_before_launch():
     st = L.pace_vit_attention(fake, fake, fake, 2048, 2, 80, fake, 1, 2048, 0.1, fake, fake, None, None, 0, None)
     assert st == 3 and "workspace" in L.pace_last_error().decode()
     # GQA heads not divisible
-    st = L.pace_prefill_attention_with_mass(fake, fake, fake, 10, 6, 4, 128, fake, 1, 10, fake, fake, 5,
+    st = L.pace_prefill_attention_with_mass(fake, fake, fake, 10, 6, 4, 128, fake, 1, 10, None, fake, fake, 5,
                                             5, fake, fake, 5, 0.1, fake, fake, fake, None, 0, None)
     assert st == 1
     # K > N in DDAE selection

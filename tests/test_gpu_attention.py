@@ -251,6 +251,36 @@ def test_prefill_varlen_gqa_d128():
     _check_prefill(_packed(21, [100, 300, 7], [40, 64, 5], 28, 4, 128))
 
 
+@pytest.mark.parametrize("d", [128, 80])
+def test_prefill_visual_tokens_after_a_text_prefix(d):
+    """Sequences laid out [text prefix][visual][text query] (a system prompt before the image):
+    the mass of the visual keys from the query text against the oracle, one sequence with an
+    empty prefix."""
+    from paper_2608_27206_amd import pace
+    import torch
+    prefix, vis, text = [13, 0, 70], [100, 300, 7], [40, 64, 5]
+    seqlens = [a + b + c for a, b, c in zip(prefix, vis, text)]
+    n = sum(seqlens)
+    cu = np.concatenate([[0], np.cumsum(seqlens)]).astype(np.int32)
+    cuv = np.concatenate([[0], np.cumsum(vis)]).astype(np.int32)
+    hq, hkv = (28, 4) if d == 128 else (8, 2)
+    q, k, v = (wl.random_bf16(71 + i, (n, h, d)) for i, h in enumerate((hq, hkv, hkv)))
+    mq_start = np.asarray([a + b for a, b in zip(prefix, vis)], np.int32)
+    mq_len = np.asarray(text, np.int32)
+    say(f"prefill with text prefixes {prefix}, d={d}")
+    o, lse, mass = pace.prefill_attention_with_mass(
+        dev_bf16(q), dev_bf16(k), dev_bf16(v), dev_i32(cu), int(max(seqlens)), dev_i32(np.asarray(vis, np.int32)),
+        dev_i32(cuv), int(cuv[-1]), int(max(vis)), dev_i32(mq_start), dev_i32(mq_len), int(mq_len.max()),
+        vis_start=dev_i32(np.asarray(prefix, np.int32)))
+    torch.cuda.synchronize()
+    Or, Lr, Mr = oatt.prefill_attention(wl.bf16_bits_to_f64(q), wl.bf16_bits_to_f64(k), wl.bf16_bits_to_f64(v),
+                                        cu, vis, mq_start, mq_len, 1 / math.sqrt(d), vis_start=prefix)
+    assert np.max(np.abs(host_bf16_to_f64(o) - Or)) <= O_TOL
+    assert np.max(np.abs(host(lse) - Lr)) <= LSE_TOL
+    err, rel = mass_ok(host(mass)[:, :Mr.shape[1]], Mr, int(mq_len.max()))
+    assert err <= 0, f"mass rel err {rel}"
+
+
 def test_prefill_varlen_d80():
     _check_prefill(_packed(31, [130, 9], [70, 200], 8, 2, 80))
 
